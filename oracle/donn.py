@@ -1,0 +1,285 @@
+"""Float64 reference of the DONN emulation and training step (test infrastructure only).
+
+This module is the plain, slow, obviously-correct statement of what the
+hot path computes, written from the LightRidge paper (arXiv 2306.11268):
+
+* input encoding (§3.1, physics-kernel overview: the pixel value is the
+  amplitude, the phase starts at zero);
+* free-space diffraction as a spectral product (§3.1.1, Eqs. (forward_diff)
+  and (diffraction_freq)) with the Fresnel transfer function (Eq. (fresnel))
+  or the Rayleigh-Sommerfeld one in angular-spectrum form (Eqs. (sommerfeld),
+  (r01));
+* phase modulation by exp(j*phi) with the amplitude scale gamma
+  (§3.1.2, Eqs. (phase_euler), (phase_mod_matrix); §3.2);
+* the detector: intensity |U|^2 summed over rectangular regions (§2.1);
+* a loss on the detector sums and the gradient with respect to every phase
+  mask (§2.1: the system is differentiable from detector to source).
+
+Readings taken where the paper is silent or ambiguous (each is listed in
+the design doc with its reason):
+
+* transfer functions are the analytic ones, sampled on the unshifted DFT
+  frequency grid f_k = k'/(M*dx), k' = k for k < (M+1)//2 else k - M;
+* forward DFT uses exp(-2*pi*i*jk/M) and is unnormalised, the inverse uses
+  exp(+2*pi*i*jk/M) / M (per axis);
+* an L-layer network performs L+1 hops of the same distance z: source to
+  layer 1, layer to layer, and layer L to the detector;
+* with an FFT grid M larger than the layer size n the layer sits centred at
+  offset (M-n)/2 in a zero field; after every hop the field is cropped back
+  to the n x n aperture;
+* gamma multiplies the modulated field of every layer;
+* the loss of the training step is softmax cross-entropy over the raw
+  detector sums, averaged over the batch; a full-map upstream gradient
+  dL/dI may be given instead;
+* gradients follow the Wirtinger convention g = dL/dRe(U) + j dL/dIm(U), so
+  dL/dI contributes 2*(dL/dI)*U and dL/dphi_l = Im(conj(U_l) * g_l), with
+  g_l the gradient with respect to the modulated field of layer l.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+from typing import Optional, Sequence
+
+import numpy as np
+
+FRESNEL = 0
+ANGULAR_SPECTRUM = 1
+
+
+# ---------------------------------------------------------------------------
+# Discrete Fourier transforms by definition (§3.1.1: the convolution of
+# Eq. (forward_diff) is evaluated spectrally, Eq. (diffraction_freq)).
+# ---------------------------------------------------------------------------
+
+def dft_matrix(m: int, inverse: bool = False) -> np.ndarray:
+    """W[j, k] = exp(-/+ 2*pi*i * ((j*k) mod m) / m), complex128 [m, m].
+
+    The exponent is reduced modulo m in integer arithmetic before it is
+    scaled, so every entry is a correctly evaluated root of unity.  The
+    inverse matrix carries no 1/m factor (see idft2).
+    """
+    j = np.arange(m, dtype=np.int64)
+    e = np.outer(j, j) % m
+    sign = 1.0 if inverse else -1.0
+    return np.exp(sign * 2j * np.pi * e.astype(np.float64) / m)
+
+
+def dft2(x: np.ndarray) -> np.ndarray:
+    """Unnormalised 2-D DFT over the last two axes: F = W_rows @ X @ W_cols^T."""
+    m0, m1 = x.shape[-2:]
+    return dft_matrix(m0) @ x @ dft_matrix(m1).T
+
+
+def idft2(y: np.ndarray) -> np.ndarray:
+    """Inverse 2-D DFT over the last two axes, normalised by 1/(m0*m1)."""
+    m0, m1 = y.shape[-2:]
+    return (dft_matrix(m0, True) @ y @ dft_matrix(m1, True).T) / (m0 * m1)
+
+
+# ---------------------------------------------------------------------------
+# Transfer functions (§3.1.1).
+# ---------------------------------------------------------------------------
+
+def frequencies(m: int, pixel_pitch: float) -> np.ndarray:
+    """Spatial frequencies of the unshifted DFT grid, in cycles per metre."""
+    k = np.arange(m, dtype=np.int64)
+    ks = np.where(k < (m + 1) // 2, k, k - m)
+    return ks.astype(np.float64) / (m * pixel_pitch)
+
+
+def transfer_function(wavelength: float, pixel_pitch: float, distance: float,
+                      approx: int, m: int) -> np.ndarray:
+    """H[ky, kx] for one hop of length ``distance`` on an m x m grid, complex128.
+
+    FRESNEL (Eq. (fresnel)): the Fourier transform of the paraxial kernel
+        exp(jkz)/(j*lambda*z) * exp(jk((x-xi)^2+(y-eta)^2)/(2z)),
+    i.e. H = exp(jkz) * exp(-j*pi*lambda*z*(fx^2 + fy^2)).
+
+    ANGULAR_SPECTRUM (Eqs. (sommerfeld), (r01)): the Fourier transform of the
+    Rayleigh-Sommerfeld kernel, H = exp(jkz*sqrt(1 - lambda^2 (fx^2 + fy^2)))
+    on propagating frequencies and exp(-kz*sqrt(lambda^2 f^2 - 1)) on
+    evanescent ones.
+    """
+    f = frequencies(m, pixel_pitch)
+    f2 = f[:, None] ** 2 + f[None, :] ** 2
+    k = 2.0 * np.pi / wavelength
+    if approx == FRESNEL:
+        return np.exp(1j * k * distance) * np.exp(-1j * np.pi * wavelength * distance * f2)
+    if approx == ANGULAR_SPECTRUM:
+        arg = 1.0 - (wavelength ** 2) * f2
+        prop = arg >= 0.0
+        h = np.empty((m, m), dtype=np.complex128)
+        h[prop] = np.exp(1j * k * distance * np.sqrt(arg[prop]))
+        h[~prop] = np.exp(-k * distance * np.sqrt(-arg[~prop]))
+        return h
+    raise ValueError(f"unsupported approximation {approx}")
+
+
+# ---------------------------------------------------------------------------
+# One hop: pad -> DFT2 -> x H -> IDFT2 -> crop (§3.1.1).
+# ---------------------------------------------------------------------------
+
+def propagate(u: np.ndarray, h: np.ndarray, adjoint: bool = False) -> np.ndarray:
+    """Propagate fields u [..., n, n] by one hop with transfer function h [m, m].
+
+    The n x n field sits centred in an m x m zero grid (offset (m-n)/2); the
+    result is cropped back to the same n x n window.  ``adjoint`` applies the
+    Hilbert adjoint of that linear map, which is the same pad/crop with conj(h).
+    """
+    m = h.shape[0]
+    n = u.shape[-1]
+    if u.shape[-2] != n or h.shape != (m, m) or n > m or (m - n) % 2:
+        raise ValueError("field must be n x n with n <= m and m - n even")
+    o = (m - n) // 2
+    x = np.zeros(u.shape[:-2] + (m, m), dtype=np.complex128)
+    x[..., o:o + n, o:o + n] = u
+    spec = dft2(x) * (np.conj(h) if adjoint else h)
+    return idft2(spec)[..., o:o + n, o:o + n]
+
+
+# ---------------------------------------------------------------------------
+# Encoding, modulation, detection (§3.1, §3.1.2, §3.2, §2.1).
+# ---------------------------------------------------------------------------
+
+def encode_amplitude(amp: np.ndarray) -> np.ndarray:
+    """U0 = A * exp(j*0): the pixel value is the amplitude (§3.1)."""
+    return np.asarray(amp, dtype=np.float64).astype(np.complex128)
+
+
+def modulate(v: np.ndarray, phi: np.ndarray, gamma: float = 1.0) -> np.ndarray:
+    """U = gamma * V * exp(j*phi) (Eq. (phase_mod_matrix), gamma from §3.2)."""
+    return gamma * v * np.exp(1j * np.asarray(phi, dtype=np.float64))
+
+
+def intensity(u: np.ndarray) -> np.ndarray:
+    """I = |U|^2."""
+    return u.real ** 2 + u.imag ** 2
+
+
+@dataclasses.dataclass(frozen=True)
+class Detector:
+    """K square regions of side ``size`` with top-left corners (y0[k], x0[k])."""
+    size: int
+    y0: Sequence[int]
+    x0: Sequence[int]
+
+    @property
+    def num(self) -> int:
+        return len(self.y0)
+
+
+def detector_readout(i_map: np.ndarray, det: Detector) -> np.ndarray:
+    """S[b, k] = sum of I over region k (§2.1: one region per class)."""
+    s = det.size
+    out = np.zeros(i_map.shape[:-2] + (det.num,), dtype=np.float64)
+    for k, (y, x) in enumerate(zip(det.y0, det.x0)):
+        out[..., k] = i_map[..., y:y + s, x:x + s].sum(axis=(-2, -1))
+    return out
+
+
+def region_scatter(grad_sums: np.ndarray, det: Detector, n: int) -> np.ndarray:
+    """dL/dI [B, n, n] from dL/dS [B, K]: the adjoint of detector_readout."""
+    s = det.size
+    g = np.zeros(grad_sums.shape[:-1] + (n, n), dtype=np.float64)
+    for k, (y, x) in enumerate(zip(det.y0, det.x0)):
+        g[..., y:y + s, x:x + s] += grad_sums[..., k, None, None]
+    return g
+
+
+# ---------------------------------------------------------------------------
+# The network (§3.1: diffraction and modulation alternate layer by layer,
+# then one more hop to the detector plane).
+# ---------------------------------------------------------------------------
+
+def donn_forward(amp: np.ndarray, phi: np.ndarray, h: np.ndarray, gamma: float = 1.0,
+                 det: Optional[Detector] = None) -> dict:
+    """Forward pass of an L-layer DONN on a batch.
+
+    amp [B, n, n] amplitudes, phi [L, n, n] phase masks, h [m, m].
+    Returns acts [L, B, n, n] (modulated field of each layer), field (the
+    detector-plane field U_D), intensity |U_D|^2 and, with a detector, sums.
+    """
+    u = encode_amplitude(amp)
+    phi = np.asarray(phi, dtype=np.float64)
+    acts = []
+    for layer in range(phi.shape[0]):
+        u = modulate(propagate(u, h), phi[layer], gamma)
+        acts.append(u)
+    ud = propagate(u, h)
+    i_map = intensity(ud)
+    return {
+        "acts": np.stack(acts) if acts else np.zeros((0,) + u.shape, np.complex128),
+        "field": ud,
+        "intensity": i_map,
+        "sums": detector_readout(i_map, det) if det is not None else None,
+    }
+
+
+def softmax_cross_entropy(sums: np.ndarray, labels: np.ndarray):
+    """Mean softmax cross-entropy over the batch and its gradient dL/dS.
+
+    The detector sums are the logits; the paper trains on Softmax(I)
+    against one-hot labels (§2.1) and this is the cross-entropy form of it.
+    """
+    s = np.asarray(sums, dtype=np.float64)
+    b = s.shape[0]
+    shift = s - s.max(axis=1, keepdims=True)
+    lse = np.log(np.exp(shift).sum(axis=1))
+    t = np.asarray(labels, dtype=np.int64)
+    loss = float(np.mean(lse - shift[np.arange(b), t]))
+    p = np.exp(shift - lse[:, None])
+    grad = p.copy()
+    grad[np.arange(b), t] -= 1.0
+    return loss, grad / b
+
+
+def mse_softmax_loss(sums: np.ndarray, labels: np.ndarray):
+    """The paper's loss form ||Softmax(I) - t||^2 (§2.1), mean over the batch.
+
+    Reading: the squared norm summed over classes, averaged over samples.
+    Returns (loss, dL/dS).
+    """
+    s = np.asarray(sums, dtype=np.float64)
+    b, k = s.shape
+    shift = s - s.max(axis=1, keepdims=True)
+    e = np.exp(shift)
+    p = e / e.sum(axis=1, keepdims=True)
+    t = np.zeros_like(p)
+    t[np.arange(b), np.asarray(labels, dtype=np.int64)] = 1.0
+    r = p - t
+    loss = float(np.mean((r ** 2).sum(axis=1)))
+    dp = 2.0 * r / b
+    # softmax Jacobian: dS_j = p_j * (dp_j - sum_i dp_i p_i)
+    grad = p * (dp - (dp * p).sum(axis=1, keepdims=True))
+    return loss, grad
+
+
+def donn_backward(fwd: dict, phi: np.ndarray, h: np.ndarray, gamma: float = 1.0,
+                  det: Optional[Detector] = None, grad_sums: Optional[np.ndarray] = None,
+                  grad_intensity: Optional[np.ndarray] = None) -> np.ndarray:
+    """dL/dphi [L, n, n], summed over the batch.
+
+    Either grad_sums (dL/dS, needs det) or grad_intensity (dL/dI) seeds the
+    adjoint.  The adjoint of each hop is the same pad/crop propagation with
+    conj(H); the adjoint of the modulation multiplies by gamma*exp(-j*phi).
+    """
+    ud = fwd["field"]
+    acts = fwd["acts"]
+    n = ud.shape[-1]
+    if (grad_sums is None) == (grad_intensity is None):
+        raise ValueError("give exactly one of grad_sums / grad_intensity")
+    if grad_sums is not None:
+        g_i = region_scatter(np.asarray(grad_sums, dtype=np.float64), det, n)
+    else:
+        g_i = np.asarray(grad_intensity, dtype=np.float64)
+    phi = np.asarray(phi, dtype=np.float64)
+    n_layers = phi.shape[0]
+    g = propagate(2.0 * g_i * ud, h, adjoint=True)
+    dphi = np.zeros((n_layers, n, n), dtype=np.float64)
+    for layer in range(n_layers - 1, -1, -1):
+        dphi[layer] = np.imag(np.conj(acts[layer]) * g).sum(axis=0)
+        g = gamma * np.exp(-1j * phi[layer]) * g
+        if layer > 0:
+            g = propagate(g, h, adjoint=True)
+    return dphi

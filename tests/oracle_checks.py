@@ -1,0 +1,327 @@
+"""Independent pins of the float64 oracle.
+
+Each check returns an error measure that must be small for a correct
+oracle.  None of them re-types the oracle's own formulas: they compare with
+numpy's FFT (the DFT is a special case of a library routine), closed forms of
+wave optics, invariants the mathematics guarantees, a brute-force
+Rayleigh-Sommerfeld sum and central finite differences.  The same checks are
+run against deliberately broken copies of the oracle in
+``test_oracle_mutations.py`` to show that each plausible mistake is caught.
+"""
+
+from __future__ import annotations
+
+import numpy as np
+
+import oracle.donn as od
+
+LAM = 532e-9
+DX = 36e-6
+
+
+def rel(a, b):
+    a = np.asarray(a)
+    b = np.asarray(b)
+    return float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-300))
+
+
+def crand(g, shape):
+    return g.standard_normal(shape) + 1j * g.standard_normal(shape)
+
+
+# --- DFT ------------------------------------------------------------------
+
+def dft_vs_numpy():
+    g = np.random.default_rng(1)
+    x = crand(g, (3, 12, 20))
+    return max(rel(od.dft2(x), np.fft.fft2(x)), rel(od.idft2(x), np.fft.ifft2(x)))
+
+
+def dft_delta_parseval():
+    m0, m1 = 10, 16
+    x = np.zeros((m0, m1), complex)
+    x[3, 5] = 1.0
+    k0 = np.arange(m0)[:, None]
+    k1 = np.arange(m1)[None, :]
+    expect = np.exp(-2j * np.pi * (3 * k0 / m0 + 5 * k1 / m1))
+    e1 = rel(od.dft2(x), expect)
+    g = np.random.default_rng(2)
+    y = crand(g, (m0, m1))
+    f = od.dft2(y)
+    e2 = abs(np.sum(abs(f) ** 2) / (m0 * m1 * np.sum(abs(y) ** 2)) - 1.0)
+    e3 = rel(od.idft2(od.dft2(y)), y)
+    return max(e1, e2, e3)
+
+
+def frequencies_vs_numpy():
+    return max(float(np.max(np.abs(od.frequencies(m, DX) - np.fft.fftfreq(m, DX))))
+               * DX for m in (7, 8, 64, 200, 1000))
+
+
+# --- propagation invariants --------------------------------------------------
+
+def z0_identity():
+    g = np.random.default_rng(3)
+    u = crand(g, (2, 24, 24))
+    err = 0.0
+    for approx in (od.FRESNEL, od.ANGULAR_SPECTRUM):
+        for m in (24, 40):
+            h = od.transfer_function(LAM, DX, 0.0, approx, m)
+            err = max(err, rel(od.propagate(u, h), u))
+    return err
+
+
+def parseval_unpadded():
+    g = np.random.default_rng(4)
+    u = crand(g, (2, 32, 32))
+    err = 0.0
+    for approx, lam, dx, z in ((od.FRESNEL, LAM, DX, 0.3), (od.ANGULAR_SPECTRUM, 1550e-9, 8e-6, 0.05)):
+        h = od.transfer_function(lam, dx, z, approx, 32)
+        v = od.propagate(u, h)
+        err = max(err, abs(np.sum(abs(v) ** 2) / np.sum(abs(u) ** 2) - 1.0))
+    return err
+
+
+def composition():
+    g = np.random.default_rng(5)
+    u = crand(g, (1, 128, 128))
+    err = 0.0
+    for approx, lam, dx in ((od.FRESNEL, LAM, DX), (od.ANGULAR_SPECTRUM, 1550e-9, 8e-6)):
+        h1 = od.transfer_function(lam, dx, 0.1, approx, 128)
+        h2 = od.transfer_function(lam, dx, 0.2, approx, 128)
+        h3 = od.transfer_function(lam, dx, 0.3, approx, 128)
+        err = max(err, rel(od.propagate(od.propagate(u, h1), h2), od.propagate(u, h3)))
+    return err
+
+
+def reciprocity():
+    """P_{-z} undoes P_z, and P_{-z} equals the adjoint of P_z."""
+    g = np.random.default_rng(6)
+    u = crand(g, (2, 20, 20))
+    v = crand(g, (2, 20, 20))
+    err = 0.0
+    for approx in (od.FRESNEL, od.ANGULAR_SPECTRUM):
+        hp = od.transfer_function(LAM, DX, 0.25, approx, 20)
+        hm = od.transfer_function(LAM, DX, -0.25, approx, 20)
+        err = max(err, rel(od.propagate(od.propagate(u, hp), hm), u))
+        err = max(err, rel(od.propagate(v, hm), od.propagate(v, hp, adjoint=True)))
+    return err
+
+
+def gaussian_field(m, w0_px, z, lam=LAM, dx=DX, center=None):
+    """Closed-form Fresnel propagation of exp(-r^2/w0^2) to distance z (exact for the Fresnel TF)."""
+    c = m / 2 if center is None else center
+    yy, xx = np.meshgrid((np.arange(m) - c) * dx, (np.arange(m) - c) * dx, indexing="ij")
+    r2 = xx ** 2 + yy ** 2
+    w0 = w0_px * dx
+    zr = np.pi * w0 * w0 / lam
+    q = 1.0 + 1j * z / zr
+    return np.exp(1j * 2 * np.pi / lam * z) / q * np.exp(-r2 / (w0 * w0 * q))
+
+
+def fresnel_gaussian():
+    m = 128
+    u0 = gaussian_field(m, 4.0, 0.0)
+    h = od.transfer_function(LAM, DX, 0.3, od.FRESNEL, m)
+    return rel(od.propagate(u0[None], h)[0], gaussian_field(m, 4.0, 0.3))
+
+
+def fresnel_gaussian_padded():
+    """Same closed form with the beam inside an n=64 aperture padded to m=128."""
+    n, m = 64, 128
+    u0 = gaussian_field(n, 4.0, 0.0)
+    h = od.transfer_function(LAM, DX, 0.1, od.FRESNEL, m)
+    return rel(od.propagate(u0[None], h)[0], gaussian_field(n, 4.0, 0.1))
+
+
+def fresnel_separable():
+    """2-D Fresnel propagation equals 1-D propagations along x then y (times exp(jkz))."""
+    g = np.random.default_rng(7)
+    n = 30
+    u = crand(g, (2, n, n))
+    z = 0.3
+    h = od.transfer_function(LAM, DX, z, od.FRESNEL, n)
+    f = np.fft.fftfreq(n, DX)
+    h1 = np.exp(-1j * np.pi * LAM * z * f ** 2)
+    v = np.fft.ifft(np.fft.fft(u, axis=-1) * h1, axis=-1)
+    v = np.fft.ifft(np.fft.fft(v, axis=-2) * h1[:, None], axis=-2)
+    v = v * np.exp(1j * 2 * np.pi / LAM * z)
+    return rel(od.propagate(u, h), v)
+
+
+def rs_bruteforce(exact_kernel=True, smooth=True):
+    """Angular spectrum vs a direct O(16^4) Rayleigh-Sommerfeld sum (Eqs. (sommerfeld), (r01))."""
+    lam, dx, z = 532e-9, 4e-6, 0.01
+    n, m = 16, 512
+    k = 2 * np.pi / lam
+    c = (n - 1) / 2
+    yy, xx = np.meshgrid(np.arange(n) - c, np.arange(n) - c, indexing="ij")
+    if smooth:
+        u0 = np.exp(-(xx ** 2 + yy ** 2) / 9.0).astype(complex)
+    else:
+        u0 = crand(np.random.default_rng(8), (n, n))
+    h = od.transfer_function(lam, dx, z, od.ANGULAR_SPECTRUM, m)
+    v_as = od.propagate(u0[None], h)[0]
+    py, px = np.meshgrid(np.arange(n), np.arange(n), indexing="ij")
+    dyy = (py[:, :, None, None] - py[None, None]) * dx
+    dxx = (px[:, :, None, None] - px[None, None]) * dx
+    r = np.sqrt(z * z + dyy ** 2 + dxx ** 2)
+    if exact_kernel:
+        kern = z / (2 * np.pi) * (1.0 / r - 1j * k) * np.exp(1j * k * r) / r ** 2
+    else:
+        kern = z / (1j * lam) * np.exp(1j * k * r) / r ** 2
+    v_bf = np.einsum("yxab,ab->yx", kern, u0) * dx * dx
+    return rel(v_as, v_bf)
+
+
+def fresnel_as_bound():
+    """||P_F u - P_AS u|| <= max|H_F - H_AS| * ||u|| (Parseval), unpadded 200^2."""
+    g = np.random.default_rng(9)
+    u = crand(g, (1, 200, 200))
+    hf = od.transfer_function(LAM, DX, 0.3, od.FRESNEL, 200)
+    ha = od.transfer_function(LAM, DX, 0.3, od.ANGULAR_SPECTRUM, 200)
+    lhs = np.linalg.norm(od.propagate(u, hf) - od.propagate(u, ha))
+    bound = np.max(np.abs(hf - ha)) * np.linalg.norm(u)
+    return lhs, bound
+
+
+# --- network ---------------------------------------------------------------
+
+def donn_zero_phase_gaussian():
+    """phi = 0, gamma = 1: the L-layer network is one hop of (L+1)z; closed form."""
+    m, L, z = 128, 2, 0.1
+    amp = np.abs(gaussian_field(m, 4.0, 0.0))[None]
+    phi = np.zeros((L, m, m))
+    h = od.transfer_function(LAM, DX, z, od.FRESNEL, m)
+    out = od.donn_forward(amp, phi, h, 1.0)
+    e1 = rel(out["field"][0], gaussian_field(m, 4.0, (L + 1) * z))
+    e2 = rel(out["intensity"][0], np.abs(gaussian_field(m, 4.0, (L + 1) * z)) ** 2)
+    return max(e1, e2)
+
+
+def donn_energy(gamma=0.8):
+    g = np.random.default_rng(10)
+    n, L = 24, 3
+    amp = g.uniform(0, 1, (2, n, n))
+    phi = g.uniform(0, 2 * np.pi, (L, n, n))
+    h = od.transfer_function(LAM, DX, 0.3, od.FRESNEL, n)
+    out = od.donn_forward(amp, phi, h, gamma)
+    e_unpadded = abs(out["intensity"].sum() / (gamma ** (2 * L) * (amp ** 2).sum()) - 1.0)
+    hp = od.transfer_function(LAM, DX, 0.3, od.FRESNEL, 2 * n)
+    outp = od.donn_forward(amp, phi, hp, 1.0)
+    padded_ok = outp["intensity"].sum() <= (amp ** 2).sum() * (1 + 1e-12)
+    return e_unpadded, padded_ok
+
+
+def readout_tiling():
+    g = np.random.default_rng(11)
+    i_map = g.uniform(0, 1, (3, 20, 20))
+    tiles = od.Detector(5, tuple(y for y in range(0, 20, 5) for _ in range(4)),
+                        tuple(x for _ in range(4) for x in range(0, 20, 5)))
+    e1 = rel(od.detector_readout(i_map, tiles).sum(axis=1), i_map.sum(axis=(1, 2)))
+    point = od.Detector(1, (7, 2), (3, 19))
+    s = od.detector_readout(i_map, point)
+    e2 = rel(s, np.stack([i_map[:, 7, 3], i_map[:, 2, 19]], axis=1))
+    # a region read = sum of I on the window, written out by slicing here
+    reg = od.Detector(4, (3,), (11,))
+    e3 = rel(od.detector_readout(i_map, reg)[:, 0], i_map[:, 3:7, 11:15].sum(axis=(1, 2)))
+    return max(e1, e2, e3)
+
+
+def ce_known_values():
+    loss, grad = od.softmax_cross_entropy(np.array([[0.0, np.log(2.0)]]), np.array([1]))
+    e1 = abs(loss - np.log(1.5))
+    e2 = float(np.max(np.abs(grad - np.array([[1 / 3, -1 / 3]]))))
+    loss_u, _ = od.softmax_cross_entropy(np.full((4, 10), 3.7), np.arange(4))
+    e3 = abs(loss_u - np.log(10.0))
+    g = np.random.default_rng(12)
+    s = g.normal(0, 3, (5, 10))
+    t = g.integers(0, 10, 5)
+    _, gr = od.softmax_cross_entropy(s, t)
+    e4 = float(np.max(np.abs(gr.sum(axis=1))))
+    return max(e1, e2, e3, e4)
+
+
+def loss_fd(loss_fn):
+    g = np.random.default_rng(13)
+    s = g.normal(0, 2, (4, 6))
+    t = g.integers(0, 6, 4)
+    _, grad = loss_fn(s, t)
+    fd = np.zeros_like(s)
+    eps = 1e-6
+    for idx in np.ndindex(s.shape):
+        sp = s.copy()
+        sp[idx] += eps
+        sm = s.copy()
+        sm[idx] -= eps
+        fd[idx] = (loss_fn(sp, t)[0] - loss_fn(sm, t)[0]) / (2 * eps)
+    return rel(grad, fd)
+
+
+def adjoint_dot():
+    """<P u, v> = <u, P^H v> for padded and unpadded grids, both approximations."""
+    g = np.random.default_rng(14)
+    err = 0.0
+    for approx in (od.FRESNEL, od.ANGULAR_SPECTRUM):
+        for n, m in ((16, 16), (10, 16)):
+            h = od.transfer_function(LAM, DX, 0.3, approx, m)
+            u = crand(g, (2, n, n))
+            v = crand(g, (2, n, n))
+            a = np.vdot(v, od.propagate(u, h))
+            b = np.vdot(od.propagate(v, h, adjoint=True), u)
+            err = max(err, abs(a - b) / abs(a))
+    return err
+
+
+def _tiny_net(n=12, m=12, L=2, B=3, approx=None, gamma=1.0, seed=15):
+    g = np.random.default_rng(seed)
+    amp = g.uniform(0, 1, (B, n, n))
+    phi = g.uniform(0, 2 * np.pi, (L, n, n))
+    ap = od.FRESNEL if approx is None else approx
+    h = od.transfer_function(LAM, DX, 0.05, ap, m)
+    det = od.Detector(3, (2, 6), (1, 7))
+    t = g.integers(0, 2, B)
+    gi = g.standard_normal((B, n, n))
+    return amp, phi, h, gamma, det, t, gi
+
+
+def _loss(amp, phi, h, gamma, det, t, gi, mode):
+    out = od.donn_forward(amp, phi, h, gamma, det)
+    if mode == "ce":
+        return od.softmax_cross_entropy(out["sums"], t)[0]
+    return float(np.sum(gi * out["intensity"]))
+
+
+def grad_fd(mode="ce", n=12, m=12, approx=None, gamma=1.0):
+    """Central finite differences of the loss against donn_backward, every phase entry."""
+    amp, phi, h, gamma, det, t, gi = _tiny_net(n=n, m=m, approx=approx, gamma=gamma)
+    out = od.donn_forward(amp, phi, h, gamma, det)
+    if mode == "ce":
+        _, gs = od.softmax_cross_entropy(out["sums"], t)
+        dphi = od.donn_backward(out, phi, h, gamma, det, grad_sums=gs)
+    else:
+        dphi = od.donn_backward(out, phi, h, gamma, grad_intensity=gi)
+    eps = 1e-6
+    fd = np.zeros_like(phi)
+    for idx in np.ndindex(phi.shape):
+        pp = phi.copy()
+        pp[idx] += eps
+        pm = phi.copy()
+        pm[idx] -= eps
+        fd[idx] = (_loss(amp, pp, h, gamma, det, t, gi, mode) - _loss(amp, pm, h, gamma, det, t, gi, mode)) / (2 * eps)
+    return rel(dphi, fd), dphi
+
+
+def global_phase_invariance():
+    """The loss depends on intensities only, so sum over pixels of dL/dphi_l is 0 for each l."""
+    worst = 0.0
+    for mode in ("ce", "map"):
+        amp, phi, h, gamma, det, t, gi = _tiny_net(n=10, m=16, L=3)
+        out = od.donn_forward(amp, phi, h, gamma, det)
+        if mode == "ce":
+            _, gs = od.softmax_cross_entropy(out["sums"], t)
+            d = od.donn_backward(out, phi, h, gamma, det, grad_sums=gs)
+        else:
+            d = od.donn_backward(out, phi, h, gamma, grad_intensity=gi)
+        worst = max(worst, float(np.max(np.abs(d.sum(axis=(1, 2))) / np.abs(d).sum(axis=(1, 2)))))
+    return worst

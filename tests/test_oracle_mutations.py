@@ -1,0 +1,133 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and show the pins catch each one.
+
+Every mutant replaces one function of ``oracle.donn`` for the duration of a
+test.  The test passes when at least one of the named pins reports an error
+far above its tolerance.
+"""
+
+import numpy as np
+import pytest
+
+import oracle.donn as od
+import oracle_checks as c
+
+_orig = {name: getattr(od, name) for name in (
+    "dft_matrix", "idft2", "transfer_function", "frequencies", "propagate",
+    "modulate", "detector_readout", "region_scatter", "softmax_cross_entropy",
+    "donn_forward", "donn_backward")}
+
+
+def _dft_sign_flipped(m, inverse=False):
+    return _orig["dft_matrix"](m, not inverse)
+
+
+def _idft_unnormalised(y):
+    m0, m1 = y.shape[-2:]
+    return _orig["idft2"](y) * (m0 * m1)
+
+
+def _fresnel_no_global_phase(lam, dx, z, approx, m):
+    h = _orig["transfer_function"](lam, dx, z, approx, m)
+    if approx == od.FRESNEL:
+        h = h * np.exp(-1j * 2 * np.pi / lam * z)
+    return h
+
+
+def _fresnel_chirp_conjugated(lam, dx, z, approx, m):
+    h = _orig["transfer_function"](lam, dx, z, approx, m)
+    if approx == od.FRESNEL:
+        g = np.exp(1j * 2 * np.pi / lam * z)
+        h = g * np.conj(h / g)
+    return h
+
+
+def _frequencies_unwrapped(m, dx):
+    return np.arange(m, dtype=np.float64) / (m * dx)
+
+
+def _as_paraxial(lam, dx, z, approx, m):
+    if approx == od.ANGULAR_SPECTRUM:
+        return _orig["transfer_function"](lam, dx, z, od.FRESNEL, m)
+    return _orig["transfer_function"](lam, dx, z, approx, m)
+
+
+def _adjoint_without_conj(u, h, adjoint=False):
+    return _orig["propagate"](u, h, adjoint=False)
+
+
+def _modulate_without_gamma(v, phi, gamma=1.0):
+    return _orig["modulate"](v, phi, 1.0)
+
+
+def _readout_off_by_one(i_map, det):
+    return _orig["detector_readout"](i_map, od.Detector(det.size + 1, det.y0, det.x0))
+
+
+def _scatter_transposed(grad_sums, det, n):
+    return _orig["region_scatter"](grad_sums, od.Detector(det.size, det.x0, det.y0), n)
+
+
+def _ce_grad_not_averaged(sums, labels):
+    loss, grad = _orig["softmax_cross_entropy"](sums, labels)
+    return loss, grad * np.asarray(sums).shape[0]
+
+
+def _forward_missing_last_hop(amp, phi, h, gamma=1.0, det=None):
+    out = _orig["donn_forward"](amp, phi, h, gamma, det)
+    ud = out["acts"][-1] if len(out["acts"]) else od.encode_amplitude(amp)
+    out["field"] = ud
+    out["intensity"] = od.intensity(ud)
+    return out
+
+
+def _make_backward(variant):
+    def bwd(fwd, phi, h, gamma=1.0, det=None, grad_sums=None, grad_intensity=None):
+        ud, acts = fwd["field"], fwd["acts"]
+        n = ud.shape[-1]
+        g_i = (od.region_scatter(grad_sums, det, n) if grad_sums is not None
+               else np.asarray(grad_intensity, dtype=np.float64))
+        two = 1.0 if variant == "no_factor_two" else 2.0
+        g = od.propagate(two * g_i * ud, h, adjoint=True)
+        dphi = np.zeros((phi.shape[0], n, n))
+        for layer in range(phi.shape[0] - 1, -1, -1):
+            if variant == "sign":
+                dphi[layer] = np.imag(acts[layer] * np.conj(g)).sum(axis=0)
+            else:
+                dphi[layer] = np.imag(np.conj(acts[layer]) * g).sum(axis=0)
+            rot = np.exp(1j * phi[layer]) if variant == "mask_not_conj" else np.exp(-1j * phi[layer])
+            g = (1.0 if variant == "no_gamma" else gamma) * rot * g
+            if layer > 0:
+                g = od.propagate(g, h, adjoint=True)
+        return dphi
+    return bwd
+
+
+def _fails_grad(**kw):
+    return c.grad_fd(**kw)[0] > 1e-3
+
+
+MUTANTS = [
+    ("dft_sign", "dft_matrix", _dft_sign_flipped, lambda: c.dft_vs_numpy() > 1e-3),
+    ("idft_norm", "idft2", _idft_unnormalised, lambda: c.dft_delta_parseval() > 1e-3),
+    ("fresnel_no_exp_jkz", "transfer_function", _fresnel_no_global_phase, lambda: c.fresnel_gaussian() > 1e-3),
+    ("fresnel_chirp_sign", "transfer_function", _fresnel_chirp_conjugated, lambda: c.fresnel_gaussian() > 1e-3),
+    ("freq_unwrapped", "frequencies", _frequencies_unwrapped, lambda: c.fresnel_gaussian() > 1e-3),
+    ("as_is_paraxial", "transfer_function", _as_paraxial, lambda: c.rs_bruteforce(True, True) > 1e-7),
+    ("adjoint_no_conj", "propagate", _adjoint_without_conj, lambda: c.adjoint_dot() > 1e-3),
+    ("no_gamma_forward", "modulate", _modulate_without_gamma, lambda: c.donn_energy()[0] > 1e-3),
+    ("readout_off_by_one", "detector_readout", _readout_off_by_one, lambda: c.readout_tiling() > 1e-3),
+    ("scatter_transposed", "region_scatter", _scatter_transposed, lambda: _fails_grad(mode="ce")),
+    ("ce_grad_sum_not_mean", "softmax_cross_entropy", _ce_grad_not_averaged,
+     lambda: c.loss_fd(od.softmax_cross_entropy) > 1e-3),
+    ("missing_last_hop", "donn_forward", _forward_missing_last_hop, lambda: c.donn_zero_phase_gaussian() > 1e-3),
+    ("bwd_no_factor_two", "donn_backward", _make_backward("no_factor_two"), lambda: _fails_grad(mode="map")),
+    ("bwd_sign", "donn_backward", _make_backward("sign"), lambda: _fails_grad(mode="ce")),
+    ("bwd_mask_not_conj", "donn_backward", _make_backward("mask_not_conj"), lambda: _fails_grad(mode="map")),
+    ("bwd_no_gamma", "donn_backward", _make_backward("no_gamma"), lambda: _fails_grad(mode="map", gamma=0.7)),
+]
+
+
+@pytest.mark.parametrize("name,attr,fn,caught", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_catch_planted_mistake(monkeypatch, name, attr, fn, caught):
+    monkeypatch.setattr(od, attr, fn)
+    assert caught(), f"mutant {name} was not caught"
