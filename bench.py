@@ -1,0 +1,193 @@
+#!/usr/bin/env python3
+"""Benchmark of the DONN physics kernel on one MI355X.
+
+One step = one training step of the 5-layer, 200 x 200 Fresnel DONN on a
+batch of 500 synthetic stroke images: forward pass (saving activations),
+softmax cross-entropy over the ten detector sums, adjoint backward pass to
+dL/dphi for all five masks.  Inputs are resident in HBM before timing.
+
+Prints one JSON line.  `value` is samples per second over exactly --steps
+steps bracketed by device synchronisation; the per-kernel durations used for
+the roofline come from HIP events recorded around every kernel launch on the
+launch stream during a second, instrumented run of the same steps.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", type=int, default=3, help="workload id (3 = 5-layer N=200 train, batch 500)")
+    ap.add_argument("--batch", type=int, default=None, help="override the batch size")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-samples", type=int, default=None, help="samples in the oracle timing run")
+    return ap.parse_args()
+
+
+def algorithmic_bytes_per_sample(kind: str, n: int) -> float:
+    """Bytes one sample must move through HBM in one launch of each kernel kind.
+
+    Per layer the method reads the incoming field and writes the modulated
+    field (forward, 16 n^2 bytes of complex64), and reads the adjoint field and
+    the saved activation and writes the adjoint field (backward, 24 n^2).
+    Tables (chirps, modulation) are shared by the batch and not counted.
+    """
+    nn = n * n
+    return {
+        "fwd_mid": 16.0 * nn,
+        "bwd_mid": 24.0 * nn,
+    }[kind]
+
+
+def oracle_baseline(w, batch, amp, phi, labels):
+    """Time the float64 oracle on the host: forward, loss and backward."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+
+    import oracle.donn as od
+
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
+    det = od.Detector(w.detector.size, tuple(w.detector.y0), tuple(w.detector.x0))
+    t0 = time.perf_counter()
+    fwd = od.donn_forward(amp[:batch], phi, h, 1.0, det)
+    _, gs = od.softmax_cross_entropy(fwd["sums"], labels[:batch])
+    od.donn_backward(fwd, phi, h, 1.0, det, grad_sums=gs)
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    return {"value": batch / dt, "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"{batch} samples of the same workload (forward + cross-entropy + backward), "
+                      f"{dt:.1f} s on the host, numpy float64 naive DFT",
+            "seconds": round(dt, 3), "blas_threads": int(threads), "host_cpus": len(os.sched_getaffinity(0))}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build measures one GPU only; the batch-sharded design for more "
+                                   "GPUs is described but not launched", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2306_11268_amd import binding as lb
+    from paper_2306_11268_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    lb.load()
+    w = wl.WORKLOADS[args.workload]
+    if w.kind != "train" or w.grad != "ce":
+        raise SystemExit("bench measures the cross-entropy training workload")
+    batch = w.batch if args.batch is None else args.batch
+    amp_np = wl.amplitudes(w, batch)
+    phi_np = wl.phases(w)
+    lab_np = wl.labels(w, batch)
+
+    det = lb.Detector(w.detector.size, w.detector.y0, w.detector.x0)
+    net = lb.Network(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n, w.n_fft, w.layers, 1.0, det)
+    amp = torch.from_numpy(amp_np).cuda()
+    phi = torch.from_numpy(phi_np).cuda()
+    labels = torch.from_numpy(lab_np).cuda()
+    saved = net.new_saved(batch)
+    sums = torch.empty((batch, det.num), dtype=torch.float32, device="cuda")
+    grad = torch.empty_like(phi)
+    net.workspace(batch, lb.LR_OP_FORWARD)
+    net.workspace(batch, lb.LR_OP_BACKWARD)
+
+    def step():
+        lb.lr_donn_forward(net, amp, phi, saved=saved, sums=True, out_sums=sums)
+        return lb.lr_donn_backward(net, phi, saved, sums=sums, labels=labels, out_grad_phi=grad)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ev0 = torch.cuda.Event(enable_timing=True)
+    ev1 = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        _, loss = step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = ev0.elapsed_time(ev1)
+    ms_per_step = gpu_ms / args.steps
+    value = batch / (ms_per_step / 1e3)
+
+    # instrumented replay: HIP events around every kernel launch on its stream
+    lb.kernel_timing(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    kt = lb.kernel_timing_report()
+    lb.kernel_timing(False)
+
+    per_kernel = {k: {"count": v["count"], "avg_us": 1e3 * v["ms"] / v["count"], "total_ms": v["ms"]}
+                  for k, v in kt.items()}
+    dom = max(kt.items(), key=lambda kv: kv[1]["ms"])[0]
+    kind = "bwd_mid" if "bwd_mid" in dom else ("fwd_mid" if "fwd_mid" in dom else None)
+    roof = None
+    if kind is not None:
+        avg_s = kt[dom]["ms"] / kt[dom]["count"] / 1e3
+        bytes_launch = algorithmic_bytes_per_sample(kind, w.n) * batch
+        achieved = bytes_launch / avg_s / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None, "kernel": dom,
+                "avg_launch_us": round(avg_s * 1e6, 2), "algorithmic_bytes_per_launch": int(bytes_launch)}
+
+    # whole-step algorithmic traffic per sample: forward reads the amplitude (4 n^2), writes every
+    # activation and reads it back once (16 n^2 per layer) and keeps the detector regions of U_D
+    # (0.8 n^2); backward reads the regions and U_L and writes G (16.8 n^2), then per inner layer
+    # reads G and U_l and writes G (24 n^2), and finally reads G and U_1 (16 n^2): (40 L - 10.4) n^2
+    nn = w.n * w.n
+    step_bytes = batch * nn * (40.0 * w.layers - 10.4)
+    out = {
+        "metric": "DONN samples/sec (5-layer N=200 fwd+bwd) and achieved HBM GB/s vs peak",
+        "value": round(value, 1),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": w.name, "n": w.n, "n_fft": w.n_fft, "layers": w.layers, "batch": batch,
+                   "approx": "fresnel" if w.approx == 0 else "angular_spectrum",
+                   "wavelength_m": w.wavelength, "pixel_pitch_m": w.pixel_pitch, "distance_m": w.distance,
+                   "loss": "softmax_cross_entropy", "detector_regions": det.num},
+        "roofline": roof,
+        "fields_per_s": round(value * (2 * w.layers + 1), 1),
+        "step_effective_gbps": round(step_bytes / (ms_per_step / 1e3) / 1e9, 1),
+        "wall_s": round(wall, 3),
+        "loss": float(loss) if loss is not None else None,
+        "kernels": per_kernel,
+    }
+    if not args.no_cpu_baseline:
+        cpu_b = args.cpu_samples if args.cpu_samples is not None else min(batch, 500)
+        out["cpu_baseline"] = oracle_baseline(w, cpu_b, amp_np, phi_np, lab_np)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

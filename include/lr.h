@@ -1,0 +1,194 @@
+/*
+ * lr.h -- C ABI of the MI355X (gfx950) DONN physics kernel.
+ *
+ * A diffractive optical neural network (DONN) in the sense of LightRidge
+ * (arXiv 2306.11268) is emulated as a chain of free-space hops and phase
+ * masks:
+ *
+ *   U_0 = A (amplitude, zero phase)                            -- §3.1
+ *   U_l = gamma * P_z(U_{l-1}) * exp(j*phi_l),  l = 1..L        -- §3.1.1-§3.2,
+ *                                                                Eqs. (forward_diff),
+ *                                                                (diffraction_freq),
+ *                                                                (phase_mod_matrix)
+ *   U_D = P_z(U_L),  I = |U_D|^2,  S_k = sum of I over region k -- §2.1
+ *
+ * with P_z(U) = crop(IFFT2(H * FFT2(pad(U)))) and H the Fresnel
+ * (Eq. (fresnel)) or Rayleigh-Sommerfeld angular-spectrum
+ * (Eqs. (sommerfeld), (r01)) transfer function.  Training differentiates
+ * a loss of I (or S) with respect to every phase mask phi_l (§2.1).
+ *
+ * Conventions shared by every entry point:
+ *   - All sizes are in pixels, all lengths in metres.
+ *   - Fields are complex64 (lr_c64, interleaved re/im, the layout of
+ *     torch.complex64), real arrays are float32, all row-major.
+ *   - Pointers named d_* are device (HIP) memory owned by the caller;
+ *     the library allocates nothing on these paths.  Descriptor structs and
+ *     detector coordinate arrays are host memory, read during the call only.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls validate
+ *     their arguments on the host, enqueue their kernels on `stream` and return;
+ *     an argument error returns a non-zero lr_status and enqueues nothing.
+ *     Device-side faults surface at the caller's next synchronisation.
+ *   - No C++ exception crosses the ABI.  Calls on distinct streams are
+ *     thread safe; calls that share a workspace must be ordered by the caller.
+ *   - Supported FFT grid sizes n_fft: 64, 100, 128, 200, 256, 400, 500, 512,
+ *     1000, 1024.  The layer size n satisfies 1 <= n <= n_fft with n_fft - n
+ *     even; the layer sits centred in the n_fft grid and is cropped back
+ *     after every hop.
+ */
+#ifndef LR_H_
+#define LR_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct lr_c64 {
+  float re;
+  float im;
+} lr_c64;
+
+/* Diffraction approximations (§3.1.1). */
+enum lr_approx {
+  LR_FRESNEL = 0,           /* Eq. (fresnel): H = exp(jkz) exp(-j pi lambda z (fx^2+fy^2)) */
+  LR_ANGULAR_SPECTRUM = 1   /* Eqs. (sommerfeld),(r01): H = exp(jkz sqrt(1 - lambda^2 f^2)) */
+};
+
+enum lr_status {
+  LR_OK = 0,
+  LR_E_NULL = 1,       /* a required pointer is NULL */
+  LR_E_SIZE = 2,       /* unsupported n_fft, n > n_fft, odd n_fft - n, batch < 0, ... */
+  LR_E_ARG = 3,        /* non-finite / non-positive physical parameter, bad detector, ... */
+  LR_E_APPROX = 4,     /* unknown approximation */
+  LR_E_HIP = 5,        /* a HIP runtime call failed (launch or copy) */
+  LR_E_WORKSPACE = 6,  /* work_bytes smaller than lr_workspace_size() */
+  LR_E_ALIAS = 7       /* an output buffer aliases an input it must not */
+};
+
+/* Ops for lr_workspace_size(). */
+enum lr_op {
+  LR_OP_PROPAGATE = 0,
+  LR_OP_FORWARD = 1,
+  LR_OP_BACKWARD = 2
+};
+
+#define LR_MAX_REGIONS 64
+#define LR_MAX_LAYERS 64
+
+/* Detector (§2.1; x_loc / y_loc / det_size of the paper's detector layer):
+ * `num` square regions of side `size`, region k covering rows
+ * [y0[k], y0[k]+size) and columns [x0[k], x0[k]+size) of the n x n plane.
+ * num = 0 means no region readout.  y0/x0 are host arrays of length num. */
+typedef struct lr_detector {
+  int32_t num;
+  int32_t size;
+  const int32_t* y0;
+  const int32_t* x0;
+} lr_detector;
+
+/* One DONN: the paper's system parameters (wavelength, pixel size,
+ * diffraction distance, approximation, system size, layer count, detector)
+ * plus the regularisation factor gamma of §3.2 and the transfer function. */
+typedef struct lr_donn {
+  double wavelength;    /* metres, finite and > 0 */
+  double pixel_pitch;   /* metres, finite and > 0 */
+  double distance;      /* metres per hop, finite (0 = identity, < 0 = back-propagation) */
+  int32_t approx;       /* enum lr_approx */
+  int32_t n;            /* layer size (system size) */
+  int32_t n_fft;        /* FFT grid, n <= n_fft, n_fft - n even */
+  int32_t num_layers;   /* L, 1 .. LR_MAX_LAYERS; the network makes L+1 hops */
+  float gamma;          /* amplitude factor applied at every modulation, finite */
+  lr_detector det;
+  const lr_c64* d_H;    /* device [n_fft][n_fft], written by lr_tf_build for the same
+                           wavelength / pixel_pitch / distance / approx / n_fft.
+                           The Fresnel path relies on its separability. */
+} lr_donn;
+
+/* Transfer function of one hop (§3.1.1, Eqs. (fresnel), (sommerfeld), (r01)).
+ * Writes d_H[ky][kx], ky, kx in [0, n_fft), at the unshifted DFT frequencies
+ * f = k'/(n_fft*pixel_pitch), k' = k for k < (n_fft+1)/2 else k - n_fft.
+ * Evaluated in float64 on the host (the phase kz is reduced modulo 2*pi
+ * before the quadratic term is added) and rounded once to complex64.
+ * The angular spectrum decays as exp(-kz sqrt(lambda^2 f^2 - 1)) on
+ * evanescent frequencies.  Blocking: returns after the upload has completed.
+ * Errors: LR_E_NULL (d_H), LR_E_ARG (non-finite or non-positive lambda / pitch,
+ * non-finite z), LR_E_APPROX, LR_E_SIZE (n_fft < 1 or > 4096), LR_E_HIP. */
+int lr_tf_build(double wavelength, double pixel_pitch, double distance, int32_t approx,
+                int32_t n_fft, lr_c64* d_H, void* stream);
+
+/* Bytes of caller-provided workspace needed by `op` for this network and
+ * batch; returns a negative lr_status on invalid arguments. */
+int64_t lr_workspace_size(const lr_donn* net, int32_t batch, int32_t op);
+
+/* Bytes of the saved-state buffer that lr_donn_forward fills for
+ * lr_donn_backward: L activations U_l then U_D, each complex64 [batch][n][n].
+ * Activation l (1-based) is stored transposed ([batch][x][y]) when
+ * lr_saved_layer_transposed() says so, natural ([batch][y][x]) otherwise;
+ * U_D is always natural.  Negative lr_status on invalid arguments. */
+int64_t lr_saved_size(const lr_donn* net, int32_t batch);
+int32_t lr_saved_layer_transposed(const lr_donn* net, int32_t layer);
+
+/* One hop of `batch` fields (§3.1.1): d_out = P_z(d_in), or its Hilbert
+ * adjoint P_z^H (the same pad/crop with conj(H), i.e. back-propagation) when
+ * adjoint != 0.  Uses net->wavelength..net->d_H; net->num_layers, gamma and
+ * det are ignored.  d_in, d_out: complex64 [batch][n][n]; they must not alias.
+ * d_work: >= lr_workspace_size(net, batch, LR_OP_PROPAGATE) bytes. */
+int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* d_out,
+                 int32_t adjoint, void* d_work, size_t work_bytes, void* stream);
+
+/* Detector readout (§2.1): d_sums[b][k] = sum over region k of |d_field[b]|^2.
+ * d_field: complex64 [batch][n][n]; d_sums: float32 [batch][det->num].
+ * Regions must lie inside the n x n plane. */
+int lr_detector_readout(const lr_c64* d_field, int32_t batch, int32_t n, const lr_detector* det,
+                        float* d_sums, void* stream);
+
+/* Forward pass of the network (§3.1, §2.1) on a batch.
+ *   d_amp       float32 [batch][n][n] input amplitudes (the encoded image)
+ *   d_phi       float32 [L][n][n] phase masks, radians
+ *   d_saved     nullable; lr_saved_size() bytes; filled for lr_donn_backward
+ *   d_sums      nullable; float32 [batch][det.num] detector sums (needs det.num > 0)
+ *   d_intensity nullable; float32 [batch][n][n] detector-plane |U_D|^2
+ *   d_field_out nullable; complex64 [batch][n][n] detector-plane field U_D
+ *   d_work      >= lr_workspace_size(net, batch, LR_OP_FORWARD) bytes */
+int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const float* d_phi,
+                    void* d_saved, float* d_sums, float* d_intensity, lr_c64* d_field_out,
+                    void* d_work, size_t work_bytes, void* stream);
+
+/* Gradient of the loss with respect to every phase mask (§2.1), summed over
+ * the batch, using the state saved by lr_donn_forward.  Exactly one seed:
+ *   d_labels (int32 [batch], with d_sums from the forward pass): softmax
+ *       cross-entropy over the detector sums, mean over the batch; the loss
+ *       value is written to d_loss (nullable float32 scalar);
+ *   d_grad_sums (float32 [batch][det.num]): upstream dL/dS;
+ *   d_grad_intensity (float32 [batch][n][n]): upstream dL/dI.
+ * Gradients follow the Wirtinger convention dL/dRe + j dL/dIm, so
+ * d_grad_phi[l] = sum_b Im(conj(U_l) * G_l), G_l the gradient with respect to
+ * the modulated field of layer l.  d_grad_phi: float32 [L][n][n], overwritten.
+ * The batch reduction runs in a fixed order (bitwise reproducible).
+ * d_work: >= lr_workspace_size(net, batch, LR_OP_BACKWARD) bytes. */
+int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, const void* d_saved,
+                     const float* d_sums, const int32_t* d_labels, const float* d_grad_sums,
+                     const float* d_grad_intensity, float* d_loss, float* d_grad_phi,
+                     void* d_work, size_t work_bytes, void* stream);
+
+/* Human-readable name of an lr_status. */
+const char* lr_status_string(int status);
+
+/* Kernel timing for measurement: while enabled, every kernel the library
+ * launches is bracketed by HIP events on its stream.  lr_kernel_timing_report
+ * waits for the recorded events and writes a JSON object
+ * {"<kernel>": {"count": c, "ms": total}, ...} into buf (NUL terminated,
+ * truncated to len); it returns the number of characters needed, or a
+ * negative lr_status.  lr_kernel_timing(1) clears earlier records. */
+int lr_kernel_timing(int32_t enable);
+int lr_kernel_timing_report(char* buf, size_t len);
+
+int32_t lr_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LR_H_ */

@@ -1,0 +1,306 @@
+"""Thin Python binding of liblr.so (the C ABI in include/lr.h).
+
+Argument marshalling only: torch tensors supply device memory and the
+current HIP stream; every computation runs in the library's HIP kernels.
+Importing this module does not load the library; the first call does, and
+raises if liblr.so has not been built.  There is no fallback.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, c_char_p, c_double, c_float, c_int32, c_int64, c_size_t, c_void_p
+from typing import Optional, Sequence
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblr.so")
+
+LR_FRESNEL = 0
+LR_ANGULAR_SPECTRUM = 1
+LR_OP_PROPAGATE = 0
+LR_OP_FORWARD = 1
+LR_OP_BACKWARD = 2
+
+EXPORTS = (
+    "lr_tf_build", "lr_workspace_size", "lr_saved_size", "lr_saved_layer_transposed",
+    "lr_propagate", "lr_detector_readout", "lr_donn_forward", "lr_donn_backward",
+    "lr_status_string", "lr_kernel_timing", "lr_kernel_timing_report", "lr_version",
+)
+
+
+class LrDetector(ctypes.Structure):
+    _fields_ = [("num", c_int32), ("size", c_int32), ("y0", POINTER(c_int32)), ("x0", POINTER(c_int32))]
+
+
+class LrDonn(ctypes.Structure):
+    _fields_ = [
+        ("wavelength", c_double), ("pixel_pitch", c_double), ("distance", c_double),
+        ("approx", c_int32), ("n", c_int32), ("n_fft", c_int32), ("num_layers", c_int32),
+        ("gamma", c_float), ("det", LrDetector), ("d_H", c_void_p),
+    ]
+
+
+class LrError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)} (status {status})")
+        self.status = status
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load liblr.so and declare the ABI; raises if the library is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built; run paper_2306_11268_amd.build.build() first")
+    lib = ctypes.CDLL(LIB_PATH)
+    P = c_void_p
+    lib.lr_tf_build.argtypes = [c_double, c_double, c_double, c_int32, c_int32, P, P]
+    lib.lr_workspace_size.argtypes = [POINTER(LrDonn), c_int32, c_int32]
+    lib.lr_workspace_size.restype = c_int64
+    lib.lr_saved_size.argtypes = [POINTER(LrDonn), c_int32]
+    lib.lr_saved_size.restype = c_int64
+    lib.lr_saved_layer_transposed.argtypes = [POINTER(LrDonn), c_int32]
+    lib.lr_saved_layer_transposed.restype = c_int32
+    lib.lr_propagate.argtypes = [POINTER(LrDonn), c_int32, P, P, c_int32, P, c_size_t, P]
+    lib.lr_detector_readout.argtypes = [P, c_int32, c_int32, POINTER(LrDetector), P, P]
+    lib.lr_donn_forward.argtypes = [POINTER(LrDonn), c_int32, P, P, P, P, P, P, P, c_size_t, P]
+    lib.lr_donn_backward.argtypes = [POINTER(LrDonn), c_int32, P, P, P, P, P, P, P, P, P, c_size_t, P]
+    lib.lr_status_string.argtypes = [ctypes.c_int]
+    lib.lr_status_string.restype = c_char_p
+    lib.lr_kernel_timing.argtypes = [c_int32]
+    lib.lr_kernel_timing_report.argtypes = [ctypes.c_char_p, c_size_t]
+    lib.lr_version.restype = c_int32
+    for name in EXPORTS:
+        getattr(lib, name).restype = getattr(lib, name).restype or ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    try:
+        return load().lr_status_string(int(status)).decode()
+    except Exception:  # library missing while formatting an error
+        return "unknown"
+
+
+def _check(status: int, what: str) -> None:
+    if status != 0:
+        raise LrError(status, what)
+
+
+# ---------------------------------------------------------------------------
+# torch marshalling helpers
+# ---------------------------------------------------------------------------
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream(device) -> c_void_p:
+    torch = _torch()
+    return c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _ptr(t, dtype=None, shape=None, name="tensor") -> Optional[c_void_p]:
+    if t is None:
+        return None
+    torch = _torch()
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a device tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return c_void_p(t.data_ptr())
+
+
+class Detector:
+    """Host copy of a detector layout (square regions of side ``size``)."""
+
+    def __init__(self, size: int, y0: Sequence[int], x0: Sequence[int]):
+        if len(y0) != len(x0):
+            raise ValueError("y0 and x0 differ in length")
+        self.size = int(size)
+        self.y0 = [int(v) for v in y0]
+        self.x0 = [int(v) for v in x0]
+        k = len(self.y0)
+        self._y = (c_int32 * max(k, 1))(*self.y0)
+        self._x = (c_int32 * max(k, 1))(*self.x0)
+        self.c = LrDetector(k, self.size, ctypes.cast(self._y, POINTER(c_int32)),
+                            ctypes.cast(self._x, POINTER(c_int32)))
+
+    @property
+    def num(self) -> int:
+        return len(self.y0)
+
+    @classmethod
+    def none(cls) -> "Detector":
+        return cls(1, [], [])
+
+
+class Network:
+    """An lr_donn descriptor with its transfer function and workspace cache."""
+
+    def __init__(self, wavelength: float, pixel_pitch: float, distance: float, approx: int, n: int,
+                 n_fft: Optional[int] = None, num_layers: int = 1, gamma: float = 1.0,
+                 detector: Optional[Detector] = None, device="cuda"):
+        torch = _torch()
+        self.device = torch.device(device)
+        self.n = int(n)
+        self.n_fft = int(n if n_fft is None else n_fft)
+        self.num_layers = int(num_layers)
+        self.detector = detector if detector is not None else Detector.none()
+        self.H = torch.empty((self.n_fft, self.n_fft), dtype=torch.complex64, device=self.device)
+        lr_tf_build(wavelength, pixel_pitch, distance, approx, self.n_fft, out=self.H)
+        self.c = LrDonn(float(wavelength), float(pixel_pitch), float(distance), int(approx), self.n,
+                        self.n_fft, self.num_layers, float(gamma), self.detector.c, c_void_p(self.H.data_ptr()))
+        self._work = {}
+
+    def workspace_size(self, batch: int, op: int) -> int:
+        r = load().lr_workspace_size(ctypes.byref(self.c), int(batch), int(op))
+        if r < 0:
+            raise LrError(int(-r), "lr_workspace_size")
+        return int(r)
+
+    def saved_size(self, batch: int) -> int:
+        r = load().lr_saved_size(ctypes.byref(self.c), int(batch))
+        if r < 0:
+            raise LrError(int(-r), "lr_saved_size")
+        return int(r)
+
+    def workspace(self, batch: int, op: int):
+        torch = _torch()
+        nbytes = max(self.workspace_size(batch, op), 1)
+        buf = self._work.get(op)
+        if buf is None or buf.numel() < nbytes:
+            buf = torch.empty(nbytes, dtype=torch.uint8, device=self.device)
+            self._work[op] = buf
+        return buf
+
+    def new_saved(self, batch: int):
+        torch = _torch()
+        return torch.empty(max(self.saved_size(batch), 1), dtype=torch.uint8, device=self.device)
+
+    def layer_transposed(self, layer: int) -> bool:
+        return bool(load().lr_saved_layer_transposed(ctypes.byref(self.c), int(layer)))
+
+    def saved_activation(self, saved, batch: int, layer: int):
+        """View of U_layer (1-based; layer L+1 is U_D) from a saved buffer, natural [B, n, n]."""
+        torch = _torch()
+        nn = self.n * self.n
+        flat = saved.view(torch.complex64)[: (self.num_layers + 1) * batch * nn]
+        t = flat[(layer - 1) * batch * nn: layer * batch * nn].view(batch, self.n, self.n)
+        if layer <= self.num_layers and self.layer_transposed(layer):
+            t = t.transpose(1, 2)
+        return t
+
+
+# ---------------------------------------------------------------------------
+# The five entry points, same names as the C ABI
+# ---------------------------------------------------------------------------
+
+def lr_tf_build(wavelength: float, pixel_pitch: float, distance: float, approx: int, n_fft: int,
+                out=None, device="cuda"):
+    """Transfer function H [n_fft, n_fft] complex64 (float64 host evaluation)."""
+    torch = _torch()
+    if out is None:
+        out = torch.empty((n_fft, n_fft), dtype=torch.complex64, device=device)
+    p = _ptr(out, torch.complex64, (n_fft, n_fft), "out")
+    _check(load().lr_tf_build(float(wavelength), float(pixel_pitch), float(distance), int(approx),
+                              int(n_fft), p, _stream(out.device)), "lr_tf_build")
+    return out
+
+
+def lr_propagate(net: Network, field, adjoint: bool = False, out=None):
+    """One hop P_z (or its adjoint) of a complex64 batch [B, n, n]."""
+    torch = _torch()
+    b = int(field.shape[0])
+    if out is None:
+        out = torch.empty_like(field)
+    w = net.workspace(b, LR_OP_PROPAGATE)
+    _check(load().lr_propagate(ctypes.byref(net.c), b,
+                               _ptr(field, torch.complex64, (b, net.n, net.n), "field"),
+                               _ptr(out, torch.complex64, (b, net.n, net.n), "out"),
+                               1 if adjoint else 0, _ptr(w), w.numel(), _stream(net.device)), "lr_propagate")
+    return out
+
+
+def lr_detector_readout(field, detector: Detector, out=None):
+    """Region sums of |field|^2, float32 [B, K]."""
+    torch = _torch()
+    b, n = int(field.shape[0]), int(field.shape[-1])
+    if out is None:
+        out = torch.empty((b, detector.num), dtype=torch.float32, device=field.device)
+    _check(load().lr_detector_readout(_ptr(field, torch.complex64, (b, n, n), "field"), b, n,
+                                      ctypes.byref(detector.c), _ptr(out, torch.float32, (b, detector.num), "out"),
+                                      _stream(field.device)), "lr_detector_readout")
+    return out
+
+
+def lr_donn_forward(net: Network, amp, phi, saved=None, sums: bool = True, intensity: bool = False,
+                    field: bool = False, out_sums=None, out_intensity=None, out_field=None):
+    """Forward pass; returns a dict with the requested outputs (device tensors)."""
+    torch = _torch()
+    b = int(amp.shape[0])
+    n, L = net.n, net.num_layers
+    dev = net.device
+    if sums and net.detector.num > 0 and out_sums is None:
+        out_sums = torch.empty((b, net.detector.num), dtype=torch.float32, device=dev)
+    if intensity and out_intensity is None:
+        out_intensity = torch.empty((b, n, n), dtype=torch.float32, device=dev)
+    if field and out_field is None:
+        out_field = torch.empty((b, n, n), dtype=torch.complex64, device=dev)
+    w = net.workspace(b, LR_OP_FORWARD)
+    if saved is not None and saved.numel() < net.saved_size(b):
+        raise ValueError("saved buffer too small")
+    _check(load().lr_donn_forward(
+        ctypes.byref(net.c), b,
+        _ptr(amp, torch.float32, (b, n, n), "amp"), _ptr(phi, torch.float32, (L, n, n), "phi"),
+        _ptr(saved, torch.uint8, None, "saved"),
+        _ptr(out_sums, torch.float32, None, "sums"), _ptr(out_intensity, torch.float32, None, "intensity"),
+        _ptr(out_field, torch.complex64, None, "field"),
+        _ptr(w), w.numel(), _stream(dev)), "lr_donn_forward")
+    return {"sums": out_sums, "intensity": out_intensity, "field": out_field, "saved": saved}
+
+
+def lr_donn_backward(net: Network, phi, saved, sums=None, labels=None, grad_sums=None, grad_intensity=None,
+                     out_grad_phi=None, want_loss: bool = True):
+    """dL/dphi [L, n, n] (and the loss when labels are given)."""
+    torch = _torch()
+    n, L = net.n, net.num_layers
+    dev = net.device
+    seed = next(t for t in (labels, grad_sums, grad_intensity) if t is not None)
+    b = int(seed.shape[0])
+    if out_grad_phi is None:
+        out_grad_phi = torch.empty((L, n, n), dtype=torch.float32, device=dev)
+    loss = torch.empty((), dtype=torch.float32, device=dev) if (labels is not None and want_loss) else None
+    w = net.workspace(b, LR_OP_BACKWARD)
+    _check(load().lr_donn_backward(
+        ctypes.byref(net.c), b, _ptr(phi, torch.float32, (L, n, n), "phi"), _ptr(saved, torch.uint8, None, "saved"),
+        _ptr(sums, torch.float32, None, "sums"), _ptr(labels, torch.int32, None, "labels"),
+        _ptr(grad_sums, torch.float32, None, "grad_sums"), _ptr(grad_intensity, torch.float32, None, "grad_intensity"),
+        _ptr(loss, torch.float32, None, "loss"), _ptr(out_grad_phi, torch.float32, (L, n, n), "grad_phi"),
+        _ptr(w), w.numel(), _stream(dev)), "lr_donn_backward")
+    return out_grad_phi, loss
+
+
+def kernel_timing(enable: bool) -> None:
+    _check(load().lr_kernel_timing(1 if enable else 0), "lr_kernel_timing")
+
+
+def kernel_timing_report() -> dict:
+    import json
+    lib = load()
+    need = lib.lr_kernel_timing_report(None, 0)
+    if need < 0:
+        raise LrError(-need, "lr_kernel_timing_report")
+    buf = ctypes.create_string_buffer(need + 1)
+    lib.lr_kernel_timing_report(buf, need + 1)
+    return json.loads(buf.value.decode())

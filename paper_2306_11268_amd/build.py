@@ -1,0 +1,79 @@
+"""Build the HIP library liblr.so for gfx950 in-tree.
+
+    python -m paper_2306_11268_amd.build        # or build() from Python
+
+Compiles the HIP sources with hipcc, the pass kernels once per supported FFT
+size (csrc/kern_size.hip with -DLR_FFT_N=<size>), all translation units in
+parallel, and links paper_2306_11268_amd/liblr.so.  Packed fp32 VALU
+instructions are disabled for all device code.
+"""
+
+from __future__ import annotations
+
+import os
+import shutil
+import subprocess
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(PKG, "csrc")
+LIB = os.path.join(PKG, "liblr.so")
+BUILD_DIR = os.path.join(PKG, "_build")
+FFT_SIZES = (64, 100, 128, 200, 256, 400, 500, 512, 1000, 1024)
+# (source, object name, extra flags)
+UNITS = [("kernels.hip", "kernels", []), ("api.hip", "api", [])] + [
+    ("kern_size.hip", f"kern_n{n}", [f"-DLR_FFT_N={n}"]) for n in FFT_SIZES]
+ARCH = os.environ.get("LR_OFFLOAD_ARCH", "gfx950")
+
+COMMON = [
+    "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wall", "-Wno-unused-function", "-Wno-unknown-pragmas",
+    "-Wno-unused-variable", "-Wno-pass-failed",
+]
+
+
+def hipcc() -> str:
+    for cand in (os.environ.get("HIPCC"), shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
+        if cand and os.path.exists(cand):
+            return cand
+    raise RuntimeError("hipcc not found")
+
+
+def _compile(unit) -> str:
+    src, name, extra = unit
+    obj = os.path.join(BUILD_DIR, name + ".o")
+    cmd = [hipcc(), *COMMON, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"hipcc failed for {src}:\n{r.stderr[-8000:]}")
+    noise = [ln for ln in r.stderr.splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
+    if noise:
+        sys.stderr.write("\n".join(noise[-40:]) + "\n")
+    return obj
+
+
+def build(verbose: bool = True) -> str:
+    """Compile every HIP source and link liblr.so; returns the library path."""
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    t0 = time.time()
+    workers = max(1, min(len(UNITS), int(os.environ.get("MAX_JOBS", os.cpu_count() or 4))))
+    # largest units first so the pool drains evenly
+    order = sorted(UNITS, key=lambda u: -int(u[2][0].split("=")[1]) if u[2] else 0)
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        objs = list(ex.map(_compile, order))
+    tmp = LIB + ".tmp"
+    cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"link failed:\n{r.stderr[-8000:]}")
+    os.replace(tmp, LIB)
+    if verbose:
+        print(f"built {LIB} in {time.time() - t0:.1f}s")
+    return LIB
+
+
+if __name__ == "__main__":
+    build()

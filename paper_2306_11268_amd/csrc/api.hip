@@ -1,0 +1,716 @@
+// C ABI of the DONN physics kernel: argument validation, workspace layout,
+// the float64 transfer-function build and the sequence of passes for each
+// entry point.  Every compute step runs in the HIP kernels of kernels.hip.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/lr.h"
+#include "kernels.hpp"
+
+using lr::Axis;
+using lr::PassArgs;
+
+namespace {
+
+constexpr double kTwoPi = 6.283185307179586476925286766559;
+constexpr double kPiD = 3.141592653589793238462643383280;
+
+// ---------------------------------------------------------------------------
+// Kernel timing (measurement mode)
+// ---------------------------------------------------------------------------
+struct TimingRecord {
+  std::string name;
+  hipEvent_t start;
+  hipEvent_t stop;
+};
+
+struct TimingState {
+  std::mutex mu;
+  bool on = false;
+  std::vector<TimingRecord> recs;
+  std::vector<hipEvent_t> pool;
+};
+
+TimingState& timing() {
+  static TimingState s;
+  return s;
+}
+
+hipEvent_t take_event(TimingState& s) {
+  if (!s.pool.empty()) {
+    hipEvent_t e = s.pool.back();
+    s.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <class F>
+int run_timed(const std::string& name, hipStream_t st, F&& launch) {
+  TimingState& s = timing();
+  bool on;
+  {
+    std::lock_guard<std::mutex> g(s.mu);
+    on = s.on;
+  }
+  if (!on) return launch() == hipSuccess ? LR_OK : LR_E_HIP;
+  hipEvent_t a, b;
+  {
+    std::lock_guard<std::mutex> g(s.mu);
+    a = take_event(s);
+    b = take_event(s);
+  }
+  if (!a || !b) return LR_E_HIP;
+  if (hipEventRecord(a, st) != hipSuccess) return LR_E_HIP;
+  const hipError_t e = launch();
+  if (hipEventRecord(b, st) != hipSuccess) return LR_E_HIP;
+  {
+    std::lock_guard<std::mutex> g(s.mu);
+    s.recs.push_back(TimingRecord{name, a, b});
+  }
+  return e == hipSuccess ? LR_OK : LR_E_HIP;
+}
+
+// ---------------------------------------------------------------------------
+// Validation
+// ---------------------------------------------------------------------------
+bool finite_pos(double v) { return std::isfinite(v) && v > 0.0; }
+
+int validate_detector(const lr_detector& d, int n) {
+  if (d.num < 0 || d.num > LR_MAX_REGIONS) return LR_E_ARG;
+  if (d.num == 0) return LR_OK;
+  if (!d.y0 || !d.x0) return LR_E_NULL;
+  if (d.size < 1 || d.size > n) return LR_E_ARG;
+  for (int k = 0; k < d.num; ++k) {
+    if (d.y0[k] < 0 || d.x0[k] < 0 || d.y0[k] + d.size > n || d.x0[k] + d.size > n) return LR_E_ARG;
+  }
+  return LR_OK;
+}
+
+int validate_net(const lr_donn* net, bool need_layers) {
+  if (!net) return LR_E_NULL;
+  if (!finite_pos(net->wavelength) || !finite_pos(net->pixel_pitch) || !std::isfinite(net->distance))
+    return LR_E_ARG;
+  if (net->approx != LR_FRESNEL && net->approx != LR_ANGULAR_SPECTRUM) return LR_E_APPROX;
+  if (!lr::fft_size_supported(net->n_fft)) return LR_E_SIZE;
+  if (net->n < 1 || net->n > net->n_fft || ((net->n_fft - net->n) & 1)) return LR_E_SIZE;
+  if (need_layers) {
+    if (net->num_layers < 1 || net->num_layers > LR_MAX_LAYERS) return LR_E_SIZE;
+    if (!std::isfinite(net->gamma)) return LR_E_ARG;
+    const int dr = validate_detector(net->det, net->n);
+    if (dr != LR_OK) return dr;
+  }
+  if (!net->d_H) return LR_E_NULL;
+  return LR_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Workspace layout
+// ---------------------------------------------------------------------------
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+struct Layout {
+  size_t chirp_x = 0, chirp_y = 0, hp = 0, mod = 0, w0 = 0, w1 = 0;
+  size_t sums_part = 0, grad_sums = 0, dphi_part = 0, regions = 0, total = 0;
+  int ntiles_vec = 0;   // tiles over n vectors
+  int ntiles_spec = 0;  // tiles over n_fft spectrum columns (angular spectrum)
+  int groups = 1;
+  int spg = 1;
+};
+
+int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+Layout make_layout(const lr_donn* net, int batch, int op) {
+  Layout L;
+  const int n = net->n;
+  const int N = net->n_fft;
+  const bool as = net->approx == LR_ANGULAR_SPECTRUM;
+  const lr::TileShape sh = lr::tile_shape(N, 0);
+  L.ntiles_vec = ceil_div(n, sh.T);
+  L.ntiles_spec = ceil_div(N, sh.T);
+  const size_t c64 = 8;
+  const size_t nn = static_cast<size_t>(n) * n;
+  const size_t field = static_cast<size_t>(batch) * (as ? static_cast<size_t>(n) * N : nn) * c64;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align256(bytes);
+    return at;
+  };
+  if (!as) {
+    L.chirp_x = take(N * c64);
+    L.chirp_y = take(N * c64);
+  } else {
+    L.hp = take(static_cast<size_t>(N) * N * c64);
+  }
+  if (op != LR_OP_PROPAGATE) L.mod = take(static_cast<size_t>(net->num_layers) * nn * c64);
+  L.w0 = take(field);
+  L.w1 = take(field);
+  const int K = net->det.num;
+  if (op != LR_OP_PROPAGATE && K > 0) L.regions = take(static_cast<size_t>(K) * 8);
+  if (op == LR_OP_FORWARD && K > 0) L.sums_part = take(static_cast<size_t>(batch) * L.ntiles_vec * K * 4);
+  if (op == LR_OP_BACKWARD) {
+    if (K > 0) L.grad_sums = take(static_cast<size_t>(batch) * K * 4);
+    const int work_tiles = L.ntiles_vec;
+    int spg = ceil_div(batch * work_tiles, 2048);
+    if (spg < 1) spg = 1;
+    if (spg > batch) spg = batch > 0 ? batch : 1;
+    L.spg = spg;
+    L.groups = batch > 0 ? ceil_div(batch, spg) : 1;
+    L.dphi_part = take(static_cast<size_t>(L.groups) * nn * 4);
+  }
+  L.total = off;
+  return L;
+}
+
+template <class T>
+T* at(void* base, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+
+// The separable path alternates axes: pass p (1-based) runs along rows for odd p.
+Axis pass_axis(int p) { return (p & 1) ? lr::kRow : lr::kCol; }
+// Layer l (1-based) is modulated in pass l+1: transposed storage when that pass is a row pass.
+int layer_transposed(const lr_donn* net, int l) {
+  if (net->approx == LR_ANGULAR_SPECTRUM) return 1;
+  return pass_axis(l + 1) == lr::kRow ? 1 : 0;
+}
+
+const char* kind_name(int k) {
+  static const char* names[] = {"prop", "fwd_mid", "fwd_last", "bwd_first", "bwd_mid", "bwd_last"};
+  return names[k];
+}
+const char* as_kind_name(int k) {
+  static const char* names[] = {"row_first", "col", "row_mid", "row_last", "row_bwd_first", "row_bwd_mid",
+                                "row_bwd_last", "row_ifft"};
+  return names[k];
+}
+
+std::string fr_name(int N, int kind, Axis ax) {
+  char b[96];
+  std::snprintf(b, sizeof b, "fresnel_pass_%s_%s_N%d", kind_name(kind), ax == lr::kRow ? "row" : "col", N);
+  return b;
+}
+std::string as_name(int N, int kind) {
+  char b[96];
+  std::snprintf(b, sizeof b, "as_pass_%s_N%d", as_kind_name(kind), N);
+  return b;
+}
+
+int fr_pass(int N, lr::PassKind kind, Axis ax, const PassArgs& a, hipStream_t st) {
+  return run_timed(fr_name(N, kind, ax), st, [&] { return lr::launch_fresnel_pass(N, kind, ax, a, st); });
+}
+int as_pass(int N, lr::AsPassKind kind, const PassArgs& a, hipStream_t st) {
+  return run_timed(as_name(N, kind), st, [&] { return lr::launch_as_pass(N, kind, a, st); });
+}
+
+PassArgs base_args(const lr_donn* net, int batch) {
+  PassArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.n = net->n;
+  a.off = (net->n_fft - net->n) / 2;
+  a.batch = batch;
+  a.spg = 1;
+  return a;
+}
+
+lr::Regions host_regions(const lr_detector& d) {
+  lr::Regions r;
+  std::memset(&r, 0, sizeof r);
+  r.K = d.num;
+  r.s = d.size;
+  for (int k = 0; k < d.num && k < lr::kMaxRegions; ++k) {
+    r.y0[k] = d.y0[k];
+    r.x0[k] = d.x0[k];
+  }
+  return r;
+}
+
+// Region corners go to the workspace once per call; the pass kernels read them there.
+int upload_regions(const lr_donn* net, const Layout& L, void* w, hipStream_t st) {
+  if (net->det.num == 0) return LR_OK;
+  const lr::Regions r = host_regions(net->det);
+  return run_timed("set_regions", st, [&] { return lr::launch_set_regions(r, at<int2>(w, L.regions), st); });
+}
+
+void set_detector(PassArgs& a, const lr_detector& d, const Layout& L, void* w) {
+  a.K = d.num;
+  a.det_size = d.size;
+  a.regions = at<int2>(w, L.regions);
+}
+
+int check_work(const lr_donn* net, int batch, int op, void* d_work, size_t work_bytes, Layout* out) {
+  *out = make_layout(net, batch, op);
+  if (!d_work) return LR_E_NULL;
+  if (work_bytes < out->total) return LR_E_WORKSPACE;
+  return LR_OK;
+}
+
+int prep_tables(const lr_donn* net, const Layout& L, void* w, hipStream_t st) {
+  const float2* H = reinterpret_cast<const float2*>(net->d_H);
+  if (net->approx == LR_FRESNEL) {
+    return run_timed("prep_chirps", st, [&] {
+      return lr::launch_prep_chirps(net->n_fft, H, at<float2>(w, L.chirp_x), at<float2>(w, L.chirp_y), st);
+    });
+  }
+  return run_timed("prep_as_table", st,
+                   [&] { return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), st); });
+}
+
+int prep_mod(const lr_donn* net, const float* d_phi, const Layout& L, void* w, hipStream_t st) {
+  int orient[LR_MAX_LAYERS];
+  for (int l = 0; l < net->num_layers; ++l) orient[l] = layer_transposed(net, l + 1);
+  return run_timed("prep_mod", st, [&] {
+    return lr::launch_prep_mod(d_phi, net->num_layers, net->n, net->gamma, orient, at<float2>(w, L.mod), st);
+  });
+}
+
+#define LR_TRY(x)                  \
+  do {                             \
+    const int _r = (x);            \
+    if (_r != LR_OK) return _r;    \
+  } while (0)
+
+}  // namespace
+
+// ===========================================================================
+// C ABI
+// ===========================================================================
+extern "C" {
+
+int32_t lr_version(void) { return 1; }
+
+const char* lr_status_string(int status) {
+  switch (status) {
+    case LR_OK: return "ok";
+    case LR_E_NULL: return "required pointer is NULL";
+    case LR_E_SIZE: return "unsupported size";
+    case LR_E_ARG: return "invalid argument";
+    case LR_E_APPROX: return "unknown diffraction approximation";
+    case LR_E_HIP: return "HIP runtime error";
+    case LR_E_WORKSPACE: return "workspace too small";
+    case LR_E_ALIAS: return "output aliases an input";
+    default: return "unknown status";
+  }
+}
+
+int lr_tf_build(double wavelength, double pixel_pitch, double distance, int32_t approx, int32_t n_fft,
+                lr_c64* d_H, void* stream) {
+  if (!d_H) return LR_E_NULL;
+  if (!finite_pos(wavelength) || !finite_pos(pixel_pitch) || !std::isfinite(distance)) return LR_E_ARG;
+  if (approx != LR_FRESNEL && approx != LR_ANGULAR_SPECTRUM) return LR_E_APPROX;
+  if (n_fft < 1 || n_fft > 4096) return LR_E_SIZE;
+  const int M = n_fft;
+  const double lam = wavelength;
+  const double z = distance;
+  const double kz = kTwoPi * z / lam;
+  // exp(jkz) with kz reduced modulo 2*pi through the exact fractional wave count z/lambda
+  const double base = kTwoPi * std::fmod(z / lam, 1.0);
+  const double fscale = 1.0 / (static_cast<double>(M) * pixel_pitch);
+  std::vector<double> f(M);
+  for (int k = 0; k < M; ++k) f[k] = static_cast<double>(k < (M + 1) / 2 ? k : k - M) * fscale;
+  std::vector<lr_c64> h(static_cast<size_t>(M) * M);
+  for (int ky = 0; ky < M; ++ky) {
+    for (int kx = 0; kx < M; ++kx) {
+      const double f2 = f[ky] * f[ky] + f[kx] * f[kx];
+      double re, im;
+      if (approx == LR_FRESNEL) {
+        const double ph = base - kPiD * lam * z * f2;
+        re = std::cos(ph);
+        im = std::sin(ph);
+      } else {
+        const double s = lam * lam * f2;
+        if (s <= 1.0) {
+          // kz*sqrt(1-s) = kz - kz*s/(1+sqrt(1-s)), the first term reduced exactly
+          const double ph = base - kz * s / (1.0 + std::sqrt(1.0 - s));
+          re = std::cos(ph);
+          im = std::sin(ph);
+        } else {
+          re = std::exp(-kz * std::sqrt(s - 1.0));
+          im = 0.0;
+        }
+      }
+      h[static_cast<size_t>(ky) * M + kx] = lr_c64{static_cast<float>(re), static_cast<float>(im)};
+    }
+  }
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (hipMemcpyAsync(d_H, h.data(), h.size() * sizeof(lr_c64), hipMemcpyHostToDevice, st) != hipSuccess)
+    return LR_E_HIP;
+  if (hipStreamSynchronize(st) != hipSuccess) return LR_E_HIP;
+  return LR_OK;
+}
+
+int64_t lr_workspace_size(const lr_donn* net, int32_t batch, int32_t op) {
+  if (op != LR_OP_PROPAGATE && op != LR_OP_FORWARD && op != LR_OP_BACKWARD) return -LR_E_ARG;
+  const int r = validate_net(net, op != LR_OP_PROPAGATE);
+  if (r != LR_OK) return -r;
+  if (batch < 0) return -LR_E_SIZE;
+  return static_cast<int64_t>(make_layout(net, batch, op).total);
+}
+
+int64_t lr_saved_size(const lr_donn* net, int32_t batch) {
+  const int r = validate_net(net, true);
+  if (r != LR_OK) return -r;
+  if (batch < 0) return -LR_E_SIZE;
+  return static_cast<int64_t>(net->num_layers + 1) * batch * net->n * net->n * 8;
+}
+
+int32_t lr_saved_layer_transposed(const lr_donn* net, int32_t layer) {
+  if (!net || layer < 1 || layer > net->num_layers) return -LR_E_ARG;
+  return layer_transposed(net, layer);
+}
+
+int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* d_out, int32_t adjoint,
+                 void* d_work, size_t work_bytes, void* stream) {
+  LR_TRY(validate_net(net, false));
+  if (batch < 0) return LR_E_SIZE;
+  if (batch == 0) return LR_OK;
+  if (!d_in || !d_out) return LR_E_NULL;
+  if (static_cast<const void*>(d_in) == static_cast<const void*>(d_out)) return LR_E_ALIAS;
+  Layout L;
+  LR_TRY(check_work(net, batch, LR_OP_PROPAGATE, d_work, work_bytes, &L));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int N = net->n_fft;
+  LR_TRY(prep_tables(net, L, d_work, st));
+  PassArgs a = base_args(net, batch);
+  a.conj_tab = adjoint ? 1 : 0;
+  if (net->approx == LR_FRESNEL) {
+    a.nvec = net->n;
+    a.ntiles = L.ntiles_vec;
+    a.in = d_in;
+    a.out = at<float2>(d_work, L.w0);
+    a.tab = at<float2>(d_work, L.chirp_x);
+    LR_TRY(fr_pass(N, lr::kPropOnce, lr::kRow, a, st));
+    a.in = at<float2>(d_work, L.w0);
+    a.out = reinterpret_cast<float2*>(d_out);
+    a.tab = at<float2>(d_work, L.chirp_y);
+    return fr_pass(N, lr::kPropOnce, lr::kCol, a, st);
+  }
+  a.in = d_in;
+  a.nvec = net->n;
+  a.ntiles = L.ntiles_vec;
+  a.out = at<float2>(d_work, L.w0);
+  LR_TRY(as_pass(N, lr::kAsRowFirst, a, st));
+  a.in = at<float2>(d_work, L.w0);
+  a.out = at<float2>(d_work, L.w1);
+  a.nvec = N;
+  a.ntiles = L.ntiles_spec;
+  a.tab = at<float2>(d_work, L.hp);
+  LR_TRY(as_pass(N, lr::kAsCol, a, st));
+  a.in = at<float2>(d_work, L.w1);
+  a.out = reinterpret_cast<float2*>(d_out);
+  a.nvec = net->n;
+  a.ntiles = L.ntiles_vec;
+  return as_pass(N, lr::kAsRowIfft, a, st);
+}
+
+int lr_detector_readout(const lr_c64* d_field, int32_t batch, int32_t n, const lr_detector* det, float* d_sums,
+                        void* stream) {
+  if (!det) return LR_E_NULL;
+  if (batch < 0 || n < 1) return LR_E_SIZE;
+  LR_TRY(validate_detector(*det, n));
+  if (batch == 0 || det->num == 0) return LR_OK;
+  if (!d_field || !d_sums) return LR_E_NULL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const lr::Regions reg = host_regions(*det);
+  return run_timed("readout", st, [&] {
+    return lr::launch_readout(reinterpret_cast<const float2*>(d_field), batch, n, reg, d_sums, st);
+  });
+}
+
+int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const float* d_phi, void* d_saved,
+                    float* d_sums, float* d_intensity, lr_c64* d_field_out, void* d_work, size_t work_bytes,
+                    void* stream) {
+  LR_TRY(validate_net(net, true));
+  if (batch < 0) return LR_E_SIZE;
+  if (batch == 0) return LR_OK;
+  if (!d_amp || !d_phi) return LR_E_NULL;
+  if (d_sums && net->det.num == 0) return LR_E_ARG;
+  Layout L;
+  LR_TRY(check_work(net, batch, LR_OP_FORWARD, d_work, work_bytes, &L));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int N = net->n_fft;
+  const int n = net->n;
+  const int Lyr = net->num_layers;
+  const size_t nn = static_cast<size_t>(n) * n;
+  float2* saved = static_cast<float2*>(d_saved);
+  float2* ws_mod = at<float2>(d_work, L.mod);
+  float2* w[2] = {at<float2>(d_work, L.w0), at<float2>(d_work, L.w1)};
+
+  LR_TRY(prep_tables(net, L, d_work, st));
+  LR_TRY(prep_mod(net, d_phi, L, d_work, st));
+  if (d_sums) LR_TRY(upload_regions(net, L, d_work, st));
+
+  PassArgs a = base_args(net, batch);
+  if (net->approx == LR_FRESNEL) {
+    a.nvec = n;
+    a.ntiles = L.ntiles_vec;
+    auto chirp = [&](Axis ax) { return at<float2>(d_work, ax == lr::kRow ? L.chirp_x : L.chirp_y); };
+    // pass 1: first sweep of hop 1 along x
+    a.in = d_amp;
+    a.in_real = 1;
+    a.out = w[0];
+    a.tab = chirp(lr::kRow);
+    LR_TRY(fr_pass(N, lr::kPropOnce, lr::kRow, a, st));
+    a.in_real = 0;
+    int cur = 0;
+    // passes 2..L+1: end of hop l, modulation of layer l, start of hop l+1
+    for (int l = 1; l <= Lyr; ++l) {
+      const Axis ax = pass_axis(l + 1);
+      a.in = w[cur];
+      a.out = w[cur ^ 1];
+      a.tab = chirp(ax);
+      a.mod = ws_mod + static_cast<size_t>(l - 1) * nn;
+      a.act_out = saved ? saved + static_cast<size_t>(l - 1) * batch * nn : nullptr;
+      LR_TRY(fr_pass(N, lr::kFwdMid, ax, a, st));
+      cur ^= 1;
+    }
+    // pass L+2: end of hop L+1, detector plane
+    const Axis ax = pass_axis(Lyr + 2);
+    a.in = w[cur];
+    a.out = nullptr;
+    a.tab = chirp(ax);
+    a.mod = nullptr;
+    a.act_out = nullptr;
+    a.intensity = d_intensity;
+    a.field_out = reinterpret_cast<float2*>(d_field_out);
+    a.saved_ud = saved ? saved + static_cast<size_t>(Lyr) * batch * nn : nullptr;
+    if (d_sums) {
+      set_detector(a, net->det, L, d_work);
+      a.sums_part = at<float>(d_work, L.sums_part);
+    }
+    LR_TRY(fr_pass(N, lr::kFwdLast, ax, a, st));
+  } else {
+    a.nvec = n;
+    a.ntiles = L.ntiles_vec;
+    a.in = d_amp;
+    a.in_real = 1;
+    a.out = w[0];
+    LR_TRY(as_pass(N, lr::kAsRowFirst, a, st));
+    a.in_real = 0;
+    int cur = 0;
+    for (int hop = 1; hop <= Lyr + 1; ++hop) {
+      PassArgs c = a;
+      c.in = w[cur];
+      c.out = w[cur ^ 1];
+      c.nvec = N;
+      c.ntiles = L.ntiles_spec;
+      c.tab = at<float2>(d_work, L.hp);
+      LR_TRY(as_pass(N, lr::kAsCol, c, st));
+      cur ^= 1;
+      if (hop <= Lyr) {
+        PassArgs r = a;
+        r.in = w[cur];
+        r.out = w[cur ^ 1];
+        r.mod = ws_mod + static_cast<size_t>(hop - 1) * nn;
+        r.act_out = saved ? saved + static_cast<size_t>(hop - 1) * batch * nn : nullptr;
+        LR_TRY(as_pass(N, lr::kAsRowMid, r, st));
+        cur ^= 1;
+      } else {
+        PassArgs r = a;
+        r.in = w[cur];
+        r.intensity = d_intensity;
+        r.field_out = reinterpret_cast<float2*>(d_field_out);
+        r.saved_ud = saved ? saved + static_cast<size_t>(Lyr) * batch * nn : nullptr;
+        if (d_sums) {
+          set_detector(r, net->det, L, d_work);
+          r.sums_part = at<float>(d_work, L.sums_part);
+        }
+        LR_TRY(as_pass(N, lr::kAsRowLast, r, st));
+      }
+    }
+  }
+  if (d_sums) {
+    LR_TRY(run_timed("finish_sums", st, [&] {
+      return lr::launch_finish_sums(at<float>(d_work, L.sums_part), batch, L.ntiles_vec, net->det.num, d_sums, st);
+    }));
+  }
+  return LR_OK;
+}
+
+int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, const void* d_saved, const float* d_sums,
+                     const int32_t* d_labels, const float* d_grad_sums, const float* d_grad_intensity, float* d_loss,
+                     float* d_grad_phi, void* d_work, size_t work_bytes, void* stream) {
+  LR_TRY(validate_net(net, true));
+  if (batch < 0) return LR_E_SIZE;
+  if (!d_grad_phi) return LR_E_NULL;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int N = net->n_fft;
+  const int n = net->n;
+  const int Lyr = net->num_layers;
+  const size_t nn = static_cast<size_t>(n) * n;
+  if (batch > 0) {
+    if (!d_phi || !d_saved) return LR_E_NULL;
+    const int nseeds = (d_labels ? 1 : 0) + (d_grad_sums ? 1 : 0) + (d_grad_intensity ? 1 : 0);
+    if (nseeds != 1) return LR_E_ARG;
+    if ((d_labels || d_grad_sums) && net->det.num == 0) return LR_E_ARG;
+    if (d_labels && !d_sums) return LR_E_NULL;
+  }
+  Layout L;
+  LR_TRY(check_work(net, batch, LR_OP_BACKWARD, d_work, work_bytes, &L));
+  if (batch == 0) {
+    // an empty batch has a zero gradient: a fixed-order sum over no groups
+    for (int l = 1; l <= Lyr; ++l) {
+      LR_TRY(run_timed("reduce_dphi", st, [&] {
+        return lr::launch_reduce_dphi(nullptr, 0, n, 0, d_grad_phi + static_cast<size_t>(l - 1) * nn, st);
+      }));
+    }
+    return LR_OK;
+  }
+  const float2* saved = static_cast<const float2*>(d_saved);
+  float2* ws_mod = at<float2>(d_work, L.mod);
+  float2* w[2] = {at<float2>(d_work, L.w0), at<float2>(d_work, L.w1)};
+  float* part = at<float>(d_work, L.dphi_part);
+
+  LR_TRY(prep_tables(net, L, d_work, st));
+  LR_TRY(prep_mod(net, d_phi, L, d_work, st));
+
+  if (d_labels || d_grad_sums) LR_TRY(upload_regions(net, L, d_work, st));
+  const float* gsum = d_grad_sums;
+  if (d_labels) {
+    float* g = at<float>(d_work, L.grad_sums);
+    LR_TRY(run_timed("ce_loss", st,
+                     [&] { return lr::launch_ce_loss(d_sums, d_labels, batch, net->det.num, g, d_loss, st); }));
+    gsum = g;
+  }
+
+  PassArgs a = base_args(net, batch);
+  a.conj_tab = 1;
+  a.conj_mod = 1;
+  a.nvec = n;
+  a.ntiles = L.ntiles_vec;
+  auto reduce = [&](int l) {
+    return run_timed("reduce_dphi", st, [&] {
+      return lr::launch_reduce_dphi(part, L.groups, n, layer_transposed(net, l),
+                                    d_grad_phi + static_cast<size_t>(l - 1) * nn, st);
+    });
+  };
+
+  if (net->approx == LR_FRESNEL) {
+    auto chirp = [&](Axis ax) { return at<float2>(d_work, ax == lr::kRow ? L.chirp_x : L.chirp_y); };
+    // adjoint of the last sweep (hop L+1), seeded at the detector plane
+    {
+      PassArgs s = a;
+      const Axis ax = pass_axis(Lyr + 2);
+      s.tab = chirp(ax);
+      s.ud_in = saved + static_cast<size_t>(Lyr) * batch * nn;
+      s.grad_int = d_grad_intensity;
+      s.grad_sums = gsum;
+      if (gsum) set_detector(s, net->det, L, d_work);
+      s.out = w[0];
+      LR_TRY(fr_pass(N, lr::kBwdFirst, ax, s, st));
+    }
+    int cur = 0;
+    for (int l = Lyr; l >= 1; --l) {
+      const Axis ax = pass_axis(l + 1);
+      PassArgs m = a;
+      m.spg = L.spg;
+      m.in = w[cur];
+      m.tab = chirp(ax);
+      m.mod = ws_mod + static_cast<size_t>(l - 1) * nn;
+      m.act_in = saved + static_cast<size_t>(l - 1) * batch * nn;
+      m.dphi_part = part;
+      if (l > 1) {
+        m.out = w[cur ^ 1];
+        LR_TRY(fr_pass(N, lr::kBwdMid, ax, m, st));
+        cur ^= 1;
+      } else {
+        LR_TRY(fr_pass(N, lr::kBwdLast, ax, m, st));
+      }
+      LR_TRY(reduce(l));
+    }
+    return LR_OK;
+  }
+
+  // angular spectrum
+  {
+    PassArgs s = a;
+    s.ud_in = saved + static_cast<size_t>(Lyr) * batch * nn;
+    s.grad_int = d_grad_intensity;
+    s.grad_sums = gsum;
+    if (gsum) set_detector(s, net->det, L, d_work);
+    s.out = w[0];
+    LR_TRY(as_pass(N, lr::kAsRowBwdFirst, s, st));
+  }
+  int cur = 0;
+  for (int l = Lyr; l >= 1; --l) {
+    PassArgs c = a;
+    c.in = w[cur];
+    c.out = w[cur ^ 1];
+    c.nvec = N;
+    c.ntiles = L.ntiles_spec;
+    c.tab = at<float2>(d_work, L.hp);
+    LR_TRY(as_pass(N, lr::kAsCol, c, st));
+    cur ^= 1;
+    PassArgs r = a;
+    r.spg = L.spg;
+    r.in = w[cur];
+    r.mod = ws_mod + static_cast<size_t>(l - 1) * nn;
+    r.act_in = saved + static_cast<size_t>(l - 1) * batch * nn;
+    r.dphi_part = part;
+    if (l > 1) {
+      r.out = w[cur ^ 1];
+      LR_TRY(as_pass(N, lr::kAsRowBwdMid, r, st));
+      cur ^= 1;
+    } else {
+      LR_TRY(as_pass(N, lr::kAsRowBwdLast, r, st));
+    }
+    LR_TRY(reduce(l));
+  }
+  return LR_OK;
+}
+
+int lr_kernel_timing(int32_t enable) {
+  TimingState& s = timing();
+  std::lock_guard<std::mutex> g(s.mu);
+  if (enable) {
+    for (auto& r : s.recs) {
+      s.pool.push_back(r.start);
+      s.pool.push_back(r.stop);
+    }
+    s.recs.clear();
+  }
+  s.on = enable != 0;
+  return LR_OK;
+}
+
+int lr_kernel_timing_report(char* buf, size_t len) {
+  TimingState& s = timing();
+  std::lock_guard<std::mutex> g(s.mu);
+  std::map<std::string, std::pair<long, double>> agg;
+  for (auto& r : s.recs) {
+    if (hipEventSynchronize(r.stop) != hipSuccess) return -LR_E_HIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) return -LR_E_HIP;
+    auto& e = agg[r.name];
+    e.first += 1;
+    e.second += ms;
+  }
+  std::string out = "{";
+  bool first = true;
+  for (auto& kv : agg) {
+    char b[256];
+    std::snprintf(b, sizeof b, "%s\"%s\": {\"count\": %ld, \"ms\": %.6f}", first ? "" : ", ", kv.first.c_str(),
+                  kv.second.first, kv.second.second);
+    out += b;
+    first = false;
+  }
+  out += "}";
+  if (buf && len > 0) {
+    const size_t m = out.size() < len - 1 ? out.size() : len - 1;
+    std::memcpy(buf, out.data(), m);
+    buf[m] = '\0';
+  }
+  return static_cast<int>(out.size());
+}
+
+}  // extern "C"

@@ -1,0 +1,256 @@
+// Helper kernels and the size dispatch of the pass kernels.
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+#include "tile.hpp"
+
+namespace lr {
+
+// Per-size entry points, defined in kern_size.hip (one object per size).
+template <int N> hipError_t launch_fr_n(PassKind, Axis, const PassArgs&, hipStream_t);
+template <int N> hipError_t launch_as_n(AsPassKind, const PassArgs&, hipStream_t);
+template <int N> hipError_t prep_chirps_n(const float2*, float2*, float2*, hipStream_t);
+template <int N> hipError_t prep_as_n(const float2*, float2*, hipStream_t);
+template <int N> TileShape shape_n();
+
+// ---------------------------------------------------------------------------
+// Helper kernels
+// ---------------------------------------------------------------------------
+
+struct OrientArg { int o[64]; };
+
+// mod[l][q][vec] = gamma * exp(j*phi_l[y][x]); (y, x) = (q, vec) or (vec, q) when transposed.
+__global__ void prep_mod_kernel(const float* __restrict__ phi, int layers, int n, float gamma, OrientArg orient,
+                                float2* __restrict__ mod) {
+  const size_t nn = (size_t)n * n;
+  const size_t total = nn * layers;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    const int l = (int)(i / nn);
+    const size_t r = i - (size_t)l * nn;
+    const int y = (int)(r / n);
+    const int x = (int)(r - (size_t)y * n);
+    float s, c;
+    sincosf(phi[i], &s, &c);
+    const size_t o = orient.o[l < 64 ? l : 63] ? (size_t)x * n + y : r;
+    mod[(size_t)l * nn + o] = c2(gamma * c, gamma * s);
+  }
+}
+
+__global__ void finish_sums_kernel(const float* __restrict__ part, int batch, int ntiles, int K, float* __restrict__ sums) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= batch * K) return;
+  const int b = i / K;
+  const int k = i - b * K;
+  float s = 0.f;
+  for (int tl = 0; tl < ntiles; ++tl) s += part[((size_t)b * ntiles + tl) * K + k];
+  sums[i] = s;
+}
+
+// Softmax cross-entropy over the detector sums, averaged over the batch.
+// One workgroup; sample b is handled by thread b % 256 in a fixed order.
+__global__ void __launch_bounds__(256) ce_loss_kernel(const float* __restrict__ sums, const int32_t* __restrict__ labels,
+                                                      int batch, int K, float* __restrict__ grad, float* __restrict__ loss) {
+  __shared__ float red[4];
+  float my = 0.f;
+  const float invb = 1.0f / (float)batch;
+  for (int b = threadIdx.x; b < batch; b += 256) {
+    const float* s = sums + (size_t)b * K;
+    float mx = s[0];
+    for (int k = 1; k < K; ++k) mx = fmaxf(mx, s[k]);
+    float z = 0.f;
+    for (int k = 0; k < K; ++k) z += expf(s[k] - mx);
+    const float lz = logf(z);
+    const int tl = labels[b];
+    const bool valid = (unsigned)tl < (unsigned)K;  // an out-of-range label makes the loss NaN
+    for (int k = 0; k < K; ++k) {
+      const float p = expf(s[k] - mx - lz);
+      grad[(size_t)b * K + k] = (p - (k == tl ? 1.f : 0.f)) * invb;
+    }
+    my += valid ? (lz + mx - s[tl]) : __builtin_nanf("");
+  }
+  const float tot = block_sum<256>(my, red);
+  if (threadIdx.x == 0 && loss) *loss = tot * invb;
+}
+
+// dphi[y][x] = sum over groups of part[g][q][vec], oriented (transposed: q = x).
+__global__ void reduce_dphi_kernel(const float* __restrict__ part, int groups, int n, int transposed, float* __restrict__ out) {
+  const size_t nn = (size_t)n * n;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < nn; i += (size_t)gridDim.x * blockDim.x) {
+    float s = 0.f;
+    for (int g = 0; g < groups; ++g) s += part[(size_t)g * nn + i];
+    const int q = (int)(i / n);
+    const int v = (int)(i - (size_t)q * n);
+    out[transposed ? (size_t)v * n + q : i] = s;
+  }
+}
+
+// Detector readout from a field: one workgroup per (sample, region).
+__global__ void set_regions_kernel(Regions reg, int2* dst) {
+  const int k = threadIdx.x;
+  if (k < reg.K) dst[k] = make_int2(reg.y0[k], reg.x0[k]);
+}
+
+__global__ void __launch_bounds__(256) readout_kernel(const float2* __restrict__ field, int n, Regions reg,
+                                                      float* __restrict__ sums) {
+  __shared__ float red[4];
+  const int b = blockIdx.y;
+  const int k = blockIdx.x;
+  const int K = reg.K;
+  const int s = reg.s;
+  const float2* f = field + (size_t)b * n * n;
+  const int ry = reg.y0[k];
+  const int rx = reg.x0[k];
+  float my = 0.f;
+  for (int e = threadIdx.x; e < s * s; e += 256) {
+    const int dy = e / s;
+    const int dx = e - dy * s;
+    my += cabs2(f[(size_t)(ry + dy) * n + rx + dx]);
+  }
+  const float tot = block_sum<256>(my, red);
+  if (threadIdx.x == 0) sums[(size_t)b * K + k] = tot;
+}
+
+// ---------------------------------------------------------------------------
+// Dispatch
+// ---------------------------------------------------------------------------
+
+bool fft_size_supported(int N) {
+  switch (N) {
+    case 64:
+    case 100:
+    case 128:
+    case 200:
+    case 256:
+    case 400:
+    case 500:
+    case 512:
+    case 1000:
+    case 1024:
+      return true;
+    default:
+      return false;
+  }
+}
+
+TileShape tile_shape(int N, int) {
+  switch (N) {
+    case 64: return shape_n<64>();
+    case 100: return shape_n<100>();
+    case 128: return shape_n<128>();
+    case 200: return shape_n<200>();
+    case 256: return shape_n<256>();
+    case 400: return shape_n<400>();
+    case 500: return shape_n<500>();
+    case 512: return shape_n<512>();
+    case 1000: return shape_n<1000>();
+    case 1024: return shape_n<1024>();
+    default: return TileShape{0, 0};
+  }
+}
+
+hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& a, hipStream_t st) {
+  switch (N) {
+    case 64: return launch_fr_n<64>(kind, axis, a, st);
+    case 100: return launch_fr_n<100>(kind, axis, a, st);
+    case 128: return launch_fr_n<128>(kind, axis, a, st);
+    case 200: return launch_fr_n<200>(kind, axis, a, st);
+    case 256: return launch_fr_n<256>(kind, axis, a, st);
+    case 400: return launch_fr_n<400>(kind, axis, a, st);
+    case 500: return launch_fr_n<500>(kind, axis, a, st);
+    case 512: return launch_fr_n<512>(kind, axis, a, st);
+    case 1000: return launch_fr_n<1000>(kind, axis, a, st);
+    case 1024: return launch_fr_n<1024>(kind, axis, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t st) {
+  switch (N) {
+    case 64: return launch_as_n<64>(kind, a, st);
+    case 100: return launch_as_n<100>(kind, a, st);
+    case 128: return launch_as_n<128>(kind, a, st);
+    case 200: return launch_as_n<200>(kind, a, st);
+    case 256: return launch_as_n<256>(kind, a, st);
+    case 400: return launch_as_n<400>(kind, a, st);
+    case 500: return launch_as_n<500>(kind, a, st);
+    case 512: return launch_as_n<512>(kind, a, st);
+    case 1000: return launch_as_n<1000>(kind, a, st);
+    case 1024: return launch_as_n<1024>(kind, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_prep_chirps(int N, const float2* H, float2* cx, float2* cy, hipStream_t st) {
+  switch (N) {
+    case 64: return prep_chirps_n<64>(H, cx, cy, st);
+    case 100: return prep_chirps_n<100>(H, cx, cy, st);
+    case 128: return prep_chirps_n<128>(H, cx, cy, st);
+    case 200: return prep_chirps_n<200>(H, cx, cy, st);
+    case 256: return prep_chirps_n<256>(H, cx, cy, st);
+    case 400: return prep_chirps_n<400>(H, cx, cy, st);
+    case 500: return prep_chirps_n<500>(H, cx, cy, st);
+    case 512: return prep_chirps_n<512>(H, cx, cy, st);
+    case 1000: return prep_chirps_n<1000>(H, cx, cy, st);
+    case 1024: return prep_chirps_n<1024>(H, cx, cy, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, hipStream_t st) {
+  switch (N) {
+    case 64: return prep_as_n<64>(H, Hp, st);
+    case 100: return prep_as_n<100>(H, Hp, st);
+    case 128: return prep_as_n<128>(H, Hp, st);
+    case 200: return prep_as_n<200>(H, Hp, st);
+    case 256: return prep_as_n<256>(H, Hp, st);
+    case 400: return prep_as_n<400>(H, Hp, st);
+    case 500: return prep_as_n<500>(H, Hp, st);
+    case 512: return prep_as_n<512>(H, Hp, st);
+    case 1000: return prep_as_n<1000>(H, Hp, st);
+    case 1024: return prep_as_n<1024>(H, Hp, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t launch_prep_mod(const float* phi, int layers, int n, float gamma, const int* orient_host, float2* mod,
+                           hipStream_t st) {
+  OrientArg o{};
+  for (int l = 0; l < layers && l < 64; ++l) o.o[l] = orient_host[l];
+  const size_t total = (size_t)n * n * layers;
+  int blocks = (int)((total + 255) / 256);
+  if (blocks > 8192) blocks = 8192;
+  hipLaunchKernelGGL(prep_mod_kernel, dim3(blocks), dim3(256), 0, st, phi, layers, n, gamma, o, mod);
+  return hipGetLastError();
+}
+
+hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, float* sums, hipStream_t st) {
+  const int total = batch * K;
+  hipLaunchKernelGGL(finish_sums_kernel, dim3((total + 255) / 256), dim3(256), 0, st, part, batch, ntiles, K, sums);
+  return hipGetLastError();
+}
+
+hipError_t launch_ce_loss(const float* sums, const int32_t* labels, int batch, int K, float* grad, float* loss,
+                          hipStream_t st) {
+  hipLaunchKernelGGL(ce_loss_kernel, dim3(1), dim3(256), 0, st, sums, labels, batch, K, grad, loss);
+  return hipGetLastError();
+}
+
+hipError_t launch_reduce_dphi(const float* part, int groups, int n, int transposed, float* out, hipStream_t st) {
+  const size_t nn = (size_t)n * n;
+  int blocks = (int)((nn + 255) / 256);
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(reduce_dphi_kernel, dim3(blocks), dim3(256), 0, st, part, groups, n, transposed, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_regions(const Regions& r, int2* dst, hipStream_t st) {
+  hipLaunchKernelGGL(set_regions_kernel, dim3(1), dim3(kMaxRegions), 0, st, r, dst);
+  return hipGetLastError();
+}
+
+hipError_t launch_readout(const float2* field, int batch, int n, const Regions& r, float* sums, hipStream_t st) {
+  hipLaunchKernelGGL(readout_kernel, dim3(r.K, batch), dim3(256), 0, st, field, n, r, sums);
+  return hipGetLastError();
+}
+
+}  // namespace lr

@@ -1,0 +1,100 @@
+// Internal launch interface between the C ABI (api.hip) and the kernels (kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace lr {
+
+constexpr int kMaxRegions = 64;
+
+enum Axis : int { kRow = 0, kCol = 1 };
+
+// What one pass of the separable (Fresnel) path does along its axis.
+enum PassKind : int {
+  kPropOnce = 0,   // load -> one 1-D propagation -> store
+  kFwdMid = 1,     // load -> prop -> x M_l (store U_l) -> prop -> store
+  kFwdLast = 2,    // load -> prop -> detector-plane outputs
+  kBwdFirst = 3,   // seed 2*(dL/dI)*U_D -> adjoint prop -> store
+  kBwdMid = 4,     // load -> adj prop -> dphi_l -> x conj(M_l) -> adj prop -> store
+  kBwdLast = 5,    // load -> adj prop -> dphi_1
+};
+
+// Passes of the non-separable (angular-spectrum) path.  Fields between
+// passes hold rows of x-spectra: [B][n rows][N columns], columns in the
+// plan's location order.
+enum AsPassKind : int {
+  kAsRowFirst = 0,   // rows: pad -> FFT_x (input amplitude or field)
+  kAsCol = 1,        // columns: pad -> FFT_y -> x H -> IFFT_y -> crop
+  kAsRowMid = 2,     // rows: IFFT_x -> crop -> x M_l (store U_l) -> pad -> FFT_x
+  kAsRowLast = 3,    // rows: IFFT_x -> crop -> detector-plane outputs
+  kAsRowBwdFirst = 4,// rows: seed -> pad -> FFT_x
+  kAsRowBwdMid = 5,  // rows: IFFT_x -> crop -> dphi_l -> x conj(M_l) -> pad -> FFT_x
+  kAsRowBwdLast = 6, // rows: IFFT_x -> crop -> dphi_1
+  kAsRowIfft = 7,    // rows: IFFT_x -> crop -> store field (plain propagation)
+};
+
+struct PassArgs {
+  int n;          // layer (aperture) size
+  int off;        // (N - n) / 2
+  int batch;
+  int nvec;       // vectors along the tile axis
+  int spg;        // samples per workgroup (group size of the batch reduction)
+  int ntiles;     // tiles along the vector axis (grid.x)
+  // main field
+  const void* in;
+  int in_real;    // input is a real float amplitude
+  float2* out;
+  // spectral table: B-item-ordered 1-D chirp (separable path) or the
+  // column-permuted 2-D transfer function (angular-spectrum path)
+  const float2* tab;
+  int conj_tab;
+  // modulation gamma*exp(j*phi_l), oriented [q][vec]
+  const float2* mod;
+  int conj_mod;
+  float2* act_out;      // oriented [B][n][n]
+  const float2* act_in; // oriented [B][n][n]
+  float* dphi_part;     // oriented [groups][n][n]
+  // detector-plane outputs (natural [B][n][n] layouts)
+  float* intensity;
+  float2* field_out;
+  float2* saved_ud;
+  float* sums_part;     // [B][ntiles][K]
+  // backward seed
+  const float* grad_sums;  // [B][K]
+  const float* grad_int;   // [B][n][n]
+  const float2* ud_in;     // [B][n][n]
+  // detector regions: K squares of side det_size, corners regions[k] = (y0, x0)
+  int K;
+  int det_size;
+  const int2* regions;
+};
+
+struct TileShape { int T; int S; };
+
+bool fft_size_supported(int N);
+TileShape tile_shape(int N, int axis);
+
+hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& a, hipStream_t st);
+hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t st);
+
+// Small helper kernels.
+hipError_t launch_prep_chirps(int N, const float2* H, float2* chirp_row, float2* chirp_col, hipStream_t st);
+hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, hipStream_t st);
+hipError_t launch_prep_mod(const float* phi, int layers, int n, float gamma, const int* orient_host,
+                           float2* mod, hipStream_t st);
+hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, float* sums, hipStream_t st);
+hipError_t launch_ce_loss(const float* sums, const int32_t* labels, int batch, int K, float* grad_sums,
+                          float* loss, hipStream_t st);
+hipError_t launch_reduce_dphi(const float* part, int groups, int n, int transposed, float* out, hipStream_t st);
+struct Regions {
+  int K;
+  int s;
+  int y0[kMaxRegions];
+  int x0[kMaxRegions];
+};
+// Copy region corners to device memory (dst: int2 [K]).
+hipError_t launch_set_regions(const Regions& r, int2* dst, hipStream_t st);
+hipError_t launch_readout(const float2* field, int batch, int n, const Regions& r, float* sums, hipStream_t st);
+
+}  // namespace lr

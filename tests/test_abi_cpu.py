@@ -1,0 +1,131 @@
+"""The C-ABI library loads, exports every declared symbol and rejects bad
+arguments on the host, without a GPU (no compute call is made here)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2306_11268_amd import binding as lb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lr.h")
+
+needs_lib = pytest.mark.skipif(not os.path.exists(lb.LIB_PATH), reason="liblr.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lr_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_declares_the_five_entry_points():
+    fns = declared_functions()
+    for f in ("lr_tf_build", "lr_propagate", "lr_donn_forward", "lr_donn_backward", "lr_detector_readout"):
+        assert f in fns
+
+
+@needs_lib
+def test_library_exports_every_declared_symbol():
+    lib = lb.load()
+    for f in declared_functions():
+        assert hasattr(lib, f), f
+    assert set(declared_functions()) == set(lb.EXPORTS)
+
+
+def _net(**kw):
+    d = dict(wavelength=532e-9, pixel_pitch=36e-6, distance=0.3, approx=0, n=200, n_fft=200, num_layers=5,
+             gamma=1.0, det=lb.LrDetector(0, 1, None, None), d_H=ctypes.c_void_p(0x1000))
+    d.update(kw)
+    return lb.LrDonn(d["wavelength"], d["pixel_pitch"], d["distance"], d["approx"], d["n"], d["n_fft"],
+                     d["num_layers"], d["gamma"], d["det"], d["d_H"])
+
+
+def _ws(net, batch=4, op=1):
+    return lb.load().lr_workspace_size(ctypes.byref(net), batch, op)
+
+
+@needs_lib
+def test_status_strings_and_version():
+    lib = lb.load()
+    assert lib.lr_version() >= 1
+    for s in range(0, 8):
+        assert isinstance(lib.lr_status_string(s), bytes)
+
+
+@needs_lib
+@pytest.mark.parametrize("kw,status", [
+    (dict(wavelength=float("nan")), 3), (dict(wavelength=-1.0), 3), (dict(pixel_pitch=0.0), 3),
+    (dict(distance=float("inf")), 3), (dict(approx=2), 4), (dict(n_fft=201, n=201), 2),
+    (dict(n=202), 2), (dict(n=199), 2), (dict(n=0), 2), (dict(num_layers=0), 2), (dict(num_layers=65), 2),
+    (dict(gamma=float("nan")), 3), (dict(d_H=ctypes.c_void_p(0)), 1),
+])
+def test_descriptor_validation(kw, status):
+    assert _ws(_net(**kw)) == -status
+
+
+@needs_lib
+def test_detector_validation():
+    ys = (ctypes.c_int32 * 2)(0, 190)
+    xs = (ctypes.c_int32 * 2)(0, 0)
+    P = ctypes.POINTER(ctypes.c_int32)
+    bad = lb.LrDetector(2, 20, ctypes.cast(ys, P), ctypes.cast(xs, P))  # second region leaves the plane
+    assert _ws(_net(det=bad)) == -3
+    null = lb.LrDetector(2, 20, None, None)
+    assert _ws(_net(det=null)) == -1
+    many = lb.LrDetector(65, 1, ctypes.cast(ys, P), ctypes.cast(xs, P))
+    assert _ws(_net(det=many)) == -3
+    ok = lb.LrDetector(1, 20, ctypes.cast(ys, P), ctypes.cast(xs, P))
+    assert _ws(_net(det=ok)) > 0
+
+
+@needs_lib
+def test_workspace_size_grows_with_batch_and_op():
+    net = _net()
+    assert _ws(net, 8, 1) > _ws(net, 4, 1) > 0
+    assert _ws(net, 4, 2) > _ws(net, 4, 0) > 0
+    assert _ws(net, -1, 1) == -2
+    assert _ws(net, 4, 9) == -3
+
+
+@needs_lib
+def test_entry_points_reject_bad_arguments_without_touching_the_gpu():
+    lib = lb.load()
+    net = _net()
+    ref = ctypes.byref(net)
+    P = ctypes.c_void_p
+    dummy = P(0x2000)
+    # transfer function
+    assert lib.lr_tf_build(532e-9, 36e-6, 0.3, 0, 64, None, None) == 1
+    assert lib.lr_tf_build(0.0, 36e-6, 0.3, 0, 64, dummy, None) == 3
+    assert lib.lr_tf_build(532e-9, 36e-6, 0.3, 5, 64, dummy, None) == 4
+    assert lib.lr_tf_build(532e-9, 36e-6, 0.3, 0, 0, dummy, None) == 2
+    # propagate: null fields, aliasing, missing / short workspace
+    assert lib.lr_propagate(ref, 2, None, dummy, 0, dummy, 1 << 30, None) == 1
+    assert lib.lr_propagate(ref, 2, dummy, dummy, 0, dummy, 1 << 30, None) == 7
+    assert lib.lr_propagate(ref, 2, dummy, P(0x3000), 0, None, 1 << 30, None) == 1
+    assert lib.lr_propagate(ref, 2, dummy, P(0x3000), 0, dummy, 16, None) == 6
+    assert lib.lr_propagate(ref, -1, dummy, P(0x3000), 0, dummy, 1 << 30, None) == 2
+    # forward: sums without a detector, null inputs
+    assert lib.lr_donn_forward(ref, 2, dummy, dummy, None, dummy, None, None, dummy, 1 << 30, None) == 3
+    assert lib.lr_donn_forward(ref, 2, None, dummy, None, None, None, None, dummy, 1 << 30, None) == 1
+    # backward: exactly one seed, labels need sums and a detector
+    assert lib.lr_donn_backward(ref, 2, dummy, dummy, None, None, None, None, None, dummy, dummy, 1 << 30,
+                                None) == 3
+    assert lib.lr_donn_backward(ref, 2, dummy, dummy, None, None, dummy, dummy, None, dummy, dummy, 1 << 30,
+                                None) == 3
+    assert lib.lr_donn_backward(ref, 2, dummy, None, None, None, None, dummy, None, dummy, dummy, 1 << 30,
+                                None) == 1
+    # detector readout
+    det = lb.LrDetector(1, 300, None, None)
+    assert lib.lr_detector_readout(dummy, 2, 200, ctypes.byref(det), dummy, None) in (1, 3)
+    assert lib.lr_detector_readout(dummy, 2, 200, None, dummy, None) == 1
+
+
+@needs_lib
+def test_kernel_timing_toggle_without_launches():
+    lb.kernel_timing(True)
+    assert lb.kernel_timing_report() == {}
+    lb.kernel_timing(False)

@@ -1,0 +1,272 @@
+"""HIP path vs the float64 oracle, element by element on the same seeded inputs.
+
+Tolerances (relative L2 over the whole output): 1e-4 for transfer functions,
+fields, intensities and detector sums; 1e-3 for phase gradients.  These are
+the acceptance bounds of the float32 path; the measured errors are ~1e-6.
+"""
+
+import numpy as np
+import pytest
+
+import oracle.donn as od
+from paper_2306_11268_amd import workloads as wl
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+TOL_FIELD = 1e-4
+TOL_GRAD = 1e-3
+
+
+def rel(a, b):
+    a = np.asarray(a)
+    b = np.asarray(b)
+    r = float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-300))
+    print(f"  rel-L2 {r:.3e} over {b.size} values")
+    return r
+
+
+@pytest.fixture(scope="module")
+def lrb():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2306_11268_amd import binding
+    binding.load()
+    return binding
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def make_net(lrb, w, layers=None, det=None, gamma=1.0, n=None, n_fft=None, distance=None):
+    d = det if det is not None else w.detector
+    detector = lrb.Detector(d.size, d.y0, d.x0) if d is not None else None
+    return lrb.Network(w.wavelength, w.pixel_pitch, w.distance if distance is None else distance, w.approx,
+                       w.n if n is None else n, w.n_fft if n_fft is None else n_fft,
+                       w.layers if layers is None else layers, gamma, detector)
+
+
+def oracle_det(d):
+    return od.Detector(d.size, tuple(d.y0), tuple(d.x0)) if d is not None else None
+
+
+def crand(seed, shape):
+    g = np.random.default_rng(seed)
+    return (g.standard_normal(shape) + 1j * g.standard_normal(shape)).astype(np.complex64)
+
+
+# ---------------------------------------------------------------------------
+# transfer function
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("approx,lam,dx,z,m", [
+    (od.FRESNEL, 532e-9, 36e-6, 0.3, 64),
+    (od.FRESNEL, 532e-9, 36e-6, 0.5, 1000),
+    (od.ANGULAR_SPECTRUM, 1550e-9, 8e-6, 0.05, 1024),
+    (od.ANGULAR_SPECTRUM, 532e-9, 4e-6, 0.01, 200),
+    (od.ANGULAR_SPECTRUM, 1550e-9, 1e-6, 0.001, 100),   # has evanescent frequencies
+    (od.FRESNEL, 532e-9, 36e-6, -0.3, 128),
+])
+def test_tf_build(lrb, approx, lam, dx, z, m):
+    h = host(lrb.lr_tf_build(lam, dx, z, approx, m))
+    ref = od.transfer_function(lam, dx, z, approx, m)
+    assert rel(h, ref) < 1e-6
+    assert np.max(np.abs(h - ref)) < 1e-6
+
+
+# ---------------------------------------------------------------------------
+# one hop
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("approx,n,m,lam,dx,z", [
+    (od.FRESNEL, 64, 64, 532e-9, 36e-6, 0.3),            # single-hop workload geometry
+    (od.FRESNEL, 200, 200, 532e-9, 36e-6, 0.3),
+    (od.FRESNEL, 100, 128, 532e-9, 36e-6, 0.3),          # padded, ragged tiles
+    (od.FRESNEL, 1000, 1000, 532e-9, 36e-6, 0.5),
+    (od.ANGULAR_SPECTRUM, 200, 200, 1550e-9, 8e-6, 0.05),
+    (od.ANGULAR_SPECTRUM, 80, 128, 1550e-9, 8e-6, 0.05),  # padded
+    (od.ANGULAR_SPECTRUM, 512, 1024, 1550e-9, 8e-6, 0.05),
+])
+@pytest.mark.parametrize("adjoint", [False, True])
+def test_propagate(lrb, approx, n, m, lam, dx, z, adjoint):
+    b = 3 if n <= 512 else 1
+    u = crand(n + m, (b, n, n))
+    net = lrb.Network(lam, dx, z, approx, n, m, 1)
+    out = host(lrb.lr_propagate(net, dev(u), adjoint=adjoint))
+    h = od.transfer_function(lam, dx, z, approx, m)
+    ref = od.propagate(u.astype(np.complex128), h, adjoint=adjoint)
+    assert rel(out, ref) < TOL_FIELD
+
+
+def test_propagate_identity_and_energy(lrb):
+    u = crand(7, (2, 64, 64))
+    net0 = lrb.Network(532e-9, 36e-6, 0.0, od.FRESNEL, 64, 64, 1)
+    assert rel(host(lrb.lr_propagate(net0, dev(u))), u) < 1e-6
+    net = lrb.Network(532e-9, 36e-6, 0.3, od.FRESNEL, 64, 64, 1)
+    v = host(lrb.lr_propagate(net, dev(u)))
+    assert abs(np.sum(np.abs(v) ** 2) / np.sum(np.abs(u) ** 2) - 1) < 1e-5
+
+
+# ---------------------------------------------------------------------------
+# detector readout
+# ---------------------------------------------------------------------------
+
+def test_detector_readout(lrb):
+    u = crand(11, (5, 200, 200))
+    d = wl.TEN_CLASS_LAYOUT_200
+    det = lrb.Detector(d.size, d.y0, d.x0)
+    s = host(lrb.lr_detector_readout(dev(u), det))
+    ref = od.detector_readout(np.abs(u.astype(np.complex128)) ** 2, oracle_det(d))
+    assert rel(s, ref) < 1e-5
+    edge = lrb.Detector(3, [0, 197, 0], [0, 197, 197])
+    s2 = host(lrb.lr_detector_readout(dev(u), edge))
+    ref2 = od.detector_readout(np.abs(u.astype(np.complex128)) ** 2, od.Detector(3, (0, 197, 0), (0, 197, 197)))
+    assert rel(s2, ref2) < 1e-5
+
+
+# ---------------------------------------------------------------------------
+# forward pass
+# ---------------------------------------------------------------------------
+
+def run_forward(lrb, w, batch, layers=None, gamma=1.0, det=None, train=False):
+    net = make_net(lrb, w, layers=layers, det=det, gamma=gamma)
+    amp = wl.amplitudes(w, batch)
+    phi = wl.phases(w)[: net.num_layers]
+    saved = net.new_saved(batch) if train else None
+    out = lrb.lr_donn_forward(net, dev(amp), dev(phi), saved=saved, sums=net.detector.num > 0,
+                              intensity=True, field=True)
+    d = det if det is not None else w.detector
+    ref = od.donn_forward(amp, phi, od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft),
+                          gamma, oracle_det(d) if (d is not None and d.num > 0) else None)
+    return net, amp, phi, out, ref, saved
+
+
+def test_forward_single_layer_n64(lrb):
+    w = wl.WORKLOADS[1]
+    _, _, _, out, ref, _ = run_forward(lrb, w, w.batch)
+    assert rel(host(out["field"]), ref["field"]) < TOL_FIELD
+    assert rel(host(out["intensity"]), ref["intensity"]) < TOL_FIELD
+
+
+@pytest.mark.parametrize("layers,gamma", [(5, 1.0), (2, 0.9), (1, 1.0)])
+def test_forward_n200_strokes(lrb, layers, gamma):
+    w = wl.WORKLOADS[2]
+    net, _, _, out, ref, saved = run_forward(lrb, w, 6, layers=layers, gamma=gamma, train=True)
+    assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
+    assert rel(host(out["field"]), ref["field"]) < TOL_FIELD
+    assert rel(host(out["intensity"]), ref["intensity"]) < TOL_FIELD
+    for layer in range(1, layers + 1):
+        act = host(net.saved_activation(saved, 6, layer))
+        assert rel(act, ref["acts"][layer - 1]) < TOL_FIELD
+    assert rel(host(net.saved_activation(saved, 6, layers + 1)), ref["field"]) < TOL_FIELD
+
+
+def test_forward_angular_spectrum_padded(lrb):
+    w = wl.WORKLOADS[4]
+    _, _, _, out, ref, _ = run_forward(lrb, w, 2, layers=3)
+    assert rel(host(out["intensity"]), ref["intensity"]) < TOL_FIELD
+    assert rel(host(out["field"]), ref["field"]) < TOL_FIELD
+
+
+def test_forward_n1000(lrb):
+    w = wl.WORKLOADS[5]
+    _, _, _, out, ref, _ = run_forward(lrb, w, 1)
+    assert rel(host(out["intensity"]), ref["intensity"]) < TOL_FIELD
+
+
+# ---------------------------------------------------------------------------
+# backward pass
+# ---------------------------------------------------------------------------
+
+def test_train_step_n200_cross_entropy(lrb):
+    w = wl.WORKLOADS[3]
+    b = 6
+    net, amp, phi, out, ref, saved = run_forward(lrb, w, b, train=True)
+    labels = wl.labels(w, b)
+    grad, loss = lrb.lr_donn_backward(net, dev(phi), saved, sums=out["sums"], labels=dev(labels))
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
+    ref_loss, gs = od.softmax_cross_entropy(ref["sums"], labels)
+    ref_grad = od.donn_backward(ref, phi, h, 1.0, oracle_det(w.detector), grad_sums=gs)
+    assert abs(float(loss) - ref_loss) / abs(ref_loss) < TOL_FIELD
+    assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+def test_backward_full_map_n1000(lrb):
+    w = wl.WORKLOADS[5]
+    b = 1
+    net, amp, phi, out, ref, saved = run_forward(lrb, w, b, train=True)
+    gi = wl.upstream_intensity_grad(w, b)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_intensity=dev(gi))
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
+    ref_grad = od.donn_backward(ref, phi, h, 1.0, grad_intensity=gi)
+    assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+def test_backward_angular_spectrum_padded(lrb):
+    w = wl.WORKLOADS[4]
+    b = 2
+    layers = 2
+    net, amp, phi, out, ref, saved = run_forward(lrb, w, b, layers=layers, train=True)
+    gi = wl.upstream_intensity_grad(w, b)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_intensity=dev(gi))
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
+    ref_grad = od.donn_backward(ref, phi, h, 1.0, grad_intensity=gi)
+    assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+def test_backward_grad_sums_gamma_padded_fresnel(lrb):
+    # padded Fresnel (n=100 in a 128 grid), gamma != 1, upstream dL/dS
+    w = wl.Workload(90, "test", 532e-9, 36e-6, 0.2, od.FRESNEL, 100, 128, 3, 3, "train",
+                    wl.layout_grid(100, 4, 12), "sums", "uniform")
+    net, amp, phi, out, ref, saved = run_forward(lrb, w, 3, gamma=0.8, train=True)
+    assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
+    gs = np.random.default_rng(5).standard_normal((3, 4)).astype(np.float32)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_sums=dev(gs))
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
+    ref_grad = od.donn_backward(ref, phi, h, 0.8, oracle_det(w.detector), grad_sums=gs)
+    assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+def test_backward_is_deterministic(lrb):
+    w = wl.WORKLOADS[3]
+    b = 40
+    net, amp, phi, out, ref, saved = run_forward(lrb, w, b, train=True)
+    labels = dev(wl.labels(w, b))
+    g1, _ = lrb.lr_donn_backward(net, dev(phi), saved, sums=out["sums"], labels=labels)
+    g1 = g1.clone()
+    g2, _ = lrb.lr_donn_backward(net, dev(phi), saved, sums=out["sums"], labels=labels)
+    assert torch.equal(g1, g2)
+    s = host(g1).sum(axis=(1, 2))
+    assert np.all(np.abs(s) <= 1e-4 * np.abs(host(g1)).sum(axis=(1, 2)))
+
+
+# ---------------------------------------------------------------------------
+# edge cases
+# ---------------------------------------------------------------------------
+
+def test_empty_batch(lrb):
+    w = wl.WORKLOADS[2]
+    net = make_net(lrb, w)
+    amp = torch.empty((0, 200, 200), dtype=torch.float32, device="cuda")
+    phi = dev(wl.phases(w))
+    out = lrb.lr_donn_forward(net, amp, phi, sums=True)
+    assert out["sums"].shape == (0, 10)
+    saved = net.new_saved(0)
+    g = torch.full((5, 200, 200), 7.0, device="cuda")
+    lrb.lr_donn_backward(net, phi, saved, grad_sums=torch.empty((0, 10), device="cuda"), out_grad_phi=g)
+    assert float(g.abs().max()) == 0.0
+
+
+def test_tiny_aperture_in_padded_grid(lrb):
+    # n = 2 inside a 64 grid: almost every position is padding
+    u = crand(3, (2, 2, 2))
+    net = lrb.Network(532e-9, 36e-6, 0.01, od.FRESNEL, 2, 64, 1)
+    out = host(lrb.lr_propagate(net, dev(u)))
+    ref = od.propagate(u.astype(np.complex128), od.transfer_function(532e-9, 36e-6, 0.01, od.FRESNEL, 64))
+    assert rel(out, ref) < TOL_FIELD
