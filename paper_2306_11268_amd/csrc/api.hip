@@ -120,7 +120,7 @@ size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 struct Layout {
   size_t chirp_x = 0, chirp_y = 0, hp = 0, mod = 0, w0 = 0, w1 = 0;
-  size_t sums_part = 0, grad_sums = 0, dphi_part = 0, regions = 0, total = 0;
+  size_t sums_part = 0, grad_sums = 0, dphi_part = 0, regions = 0, row_mask = 0, col_mask = 0, total = 0;
   int ntiles_vec = 0;   // tiles over n vectors
   int ntiles_spec = 0;  // tiles over n_fft spectrum columns (angular spectrum)
   int groups = 1;
@@ -156,7 +156,11 @@ Layout make_layout(const lr_donn* net, int batch, int op) {
   L.w0 = take(field);
   L.w1 = take(field);
   const int K = net->det.num;
-  if (op != LR_OP_PROPAGATE && K > 0) L.regions = take(static_cast<size_t>(K) * 8);
+  if (op != LR_OP_PROPAGATE && K > 0) {
+    L.regions = take(static_cast<size_t>(K) * 8);
+    L.row_mask = take(static_cast<size_t>(n) * 8);
+    L.col_mask = take(static_cast<size_t>(n) * 8);
+  }
   if (op == LR_OP_FORWARD && K > 0) L.sums_part = take(static_cast<size_t>(batch) * L.ntiles_vec * K * 4);
   if (op == LR_OP_BACKWARD) {
     if (K > 0) L.grad_sums = take(static_cast<size_t>(batch) * K * 4);
@@ -239,13 +243,18 @@ lr::Regions host_regions(const lr_detector& d) {
 int upload_regions(const lr_donn* net, const Layout& L, void* w, hipStream_t st) {
   if (net->det.num == 0) return LR_OK;
   const lr::Regions r = host_regions(net->det);
-  return run_timed("set_regions", st, [&] { return lr::launch_set_regions(r, at<int2>(w, L.regions), st); });
+  return run_timed("set_regions", st, [&] {
+    return lr::launch_set_regions(r, net->n, at<int2>(w, L.regions), at<unsigned long long>(w, L.row_mask),
+                                  at<unsigned long long>(w, L.col_mask), st);
+  });
 }
 
 void set_detector(PassArgs& a, const lr_detector& d, const Layout& L, void* w) {
   a.K = d.num;
   a.det_size = d.size;
   a.regions = at<int2>(w, L.regions);
+  a.row_mask = at<unsigned long long>(w, L.row_mask);
+  a.col_mask = at<unsigned long long>(w, L.col_mask);
 }
 
 int check_work(const lr_donn* net, int batch, int op, void* d_work, size_t work_bytes, Layout* out) {

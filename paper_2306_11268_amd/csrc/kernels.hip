@@ -73,21 +73,55 @@ __global__ void __launch_bounds__(256) ce_loss_kernel(const float* __restrict__ 
 }
 
 // dphi[y][x] = sum over groups of part[g][q][vec], oriented (transposed: q = x).
-__global__ void reduce_dphi_kernel(const float* __restrict__ part, int groups, int n, int transposed, float* __restrict__ out) {
+// A workgroup covers 64 consecutive elements with 4 slices of 64 threads;
+// slice s sums groups s, s+4, s+8, ... in order and the four partial sums are
+// added in slice order, so the result does not depend on scheduling.
+__global__ void __launch_bounds__(256) reduce_dphi_kernel(const float* __restrict__ part, int groups, int n,
+                                                          int transposed, float* __restrict__ out) {
+  __shared__ float red[4][64];
   const size_t nn = (size_t)n * n;
-  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < nn; i += (size_t)gridDim.x * blockDim.x) {
-    float s = 0.f;
-    for (int g = 0; g < groups; ++g) s += part[(size_t)g * nn + i];
+  const int lane = threadIdx.x & 63;
+  const int slice = threadIdx.x >> 6;
+  const size_t i = (size_t)blockIdx.x * 64 + lane;
+  float s = 0.f;
+  if (i < nn) {
+    int g = slice;
+    for (; g + 12 < groups; g += 16) {
+      const float a0 = part[(size_t)g * nn + i];
+      const float a1 = part[(size_t)(g + 4) * nn + i];
+      const float a2 = part[(size_t)(g + 8) * nn + i];
+      const float a3 = part[(size_t)(g + 12) * nn + i];
+      s += a0;
+      s += a1;
+      s += a2;
+      s += a3;
+    }
+    for (; g < groups; g += 4) s += part[(size_t)g * nn + i];
+  }
+  red[slice][lane] = s;
+  __syncthreads();
+  if (slice == 0 && i < nn) {
+    const float r = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
     const int q = (int)(i / n);
     const int v = (int)(i - (size_t)q * n);
-    out[transposed ? (size_t)v * n + q : i] = s;
+    out[transposed ? (size_t)v * n + q : i] = r;
   }
 }
 
 // Detector readout from a field: one workgroup per (sample, region).
-__global__ void set_regions_kernel(Regions reg, int2* dst) {
-  const int k = threadIdx.x;
-  if (k < reg.K) dst[k] = make_int2(reg.y0[k], reg.x0[k]);
+__global__ void set_regions_kernel(Regions reg, int n, int2* dst, unsigned long long* row_mask,
+                                   unsigned long long* col_mask) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < reg.K) dst[i] = make_int2(reg.y0[i], reg.x0[i]);
+  if (i < n) {
+    unsigned long long rm = 0, cm = 0;
+    for (int k = 0; k < reg.K; ++k) {
+      if ((unsigned)(i - reg.y0[k]) < (unsigned)reg.s) rm |= 1ull << k;
+      if ((unsigned)(i - reg.x0[k]) < (unsigned)reg.s) cm |= 1ull << k;
+    }
+    row_mask[i] = rm;
+    col_mask[i] = cm;
+  }
 }
 
 __global__ void __launch_bounds__(256) readout_kernel(const float2* __restrict__ field, int n, Regions reg,
@@ -122,7 +156,6 @@ bool fft_size_supported(int N) {
     case 200:
     case 256:
     case 400:
-    case 500:
     case 512:
     case 1000:
     case 1024:
@@ -140,7 +173,6 @@ TileShape tile_shape(int N, int) {
     case 200: return shape_n<200>();
     case 256: return shape_n<256>();
     case 400: return shape_n<400>();
-    case 500: return shape_n<500>();
     case 512: return shape_n<512>();
     case 1000: return shape_n<1000>();
     case 1024: return shape_n<1024>();
@@ -156,7 +188,6 @@ hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& 
     case 200: return launch_fr_n<200>(kind, axis, a, st);
     case 256: return launch_fr_n<256>(kind, axis, a, st);
     case 400: return launch_fr_n<400>(kind, axis, a, st);
-    case 500: return launch_fr_n<500>(kind, axis, a, st);
     case 512: return launch_fr_n<512>(kind, axis, a, st);
     case 1000: return launch_fr_n<1000>(kind, axis, a, st);
     case 1024: return launch_fr_n<1024>(kind, axis, a, st);
@@ -172,7 +203,6 @@ hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t
     case 200: return launch_as_n<200>(kind, a, st);
     case 256: return launch_as_n<256>(kind, a, st);
     case 400: return launch_as_n<400>(kind, a, st);
-    case 500: return launch_as_n<500>(kind, a, st);
     case 512: return launch_as_n<512>(kind, a, st);
     case 1000: return launch_as_n<1000>(kind, a, st);
     case 1024: return launch_as_n<1024>(kind, a, st);
@@ -188,7 +218,6 @@ hipError_t launch_prep_chirps(int N, const float2* H, float2* cx, float2* cy, hi
     case 200: return prep_chirps_n<200>(H, cx, cy, st);
     case 256: return prep_chirps_n<256>(H, cx, cy, st);
     case 400: return prep_chirps_n<400>(H, cx, cy, st);
-    case 500: return prep_chirps_n<500>(H, cx, cy, st);
     case 512: return prep_chirps_n<512>(H, cx, cy, st);
     case 1000: return prep_chirps_n<1000>(H, cx, cy, st);
     case 1024: return prep_chirps_n<1024>(H, cx, cy, st);
@@ -204,7 +233,6 @@ hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, hipStream_t 
     case 200: return prep_as_n<200>(H, Hp, st);
     case 256: return prep_as_n<256>(H, Hp, st);
     case 400: return prep_as_n<400>(H, Hp, st);
-    case 500: return prep_as_n<500>(H, Hp, st);
     case 512: return prep_as_n<512>(H, Hp, st);
     case 1000: return prep_as_n<1000>(H, Hp, st);
     case 1024: return prep_as_n<1024>(H, Hp, st);
@@ -237,14 +265,15 @@ hipError_t launch_ce_loss(const float* sums, const int32_t* labels, int batch, i
 
 hipError_t launch_reduce_dphi(const float* part, int groups, int n, int transposed, float* out, hipStream_t st) {
   const size_t nn = (size_t)n * n;
-  int blocks = (int)((nn + 255) / 256);
-  if (blocks > 4096) blocks = 4096;
+  const int blocks = (int)((nn + 63) / 64);
   hipLaunchKernelGGL(reduce_dphi_kernel, dim3(blocks), dim3(256), 0, st, part, groups, n, transposed, out);
   return hipGetLastError();
 }
 
-hipError_t launch_set_regions(const Regions& r, int2* dst, hipStream_t st) {
-  hipLaunchKernelGGL(set_regions_kernel, dim3(1), dim3(kMaxRegions), 0, st, r, dst);
+hipError_t launch_set_regions(const Regions& r, int n, int2* dst, unsigned long long* row_mask,
+                              unsigned long long* col_mask, hipStream_t st) {
+  const int m = n > kMaxRegions ? n : kMaxRegions;
+  hipLaunchKernelGGL(set_regions_kernel, dim3((m + 255) / 256), dim3(256), 0, st, r, n, dst, row_mask, col_mask);
   return hipGetLastError();
 }
 

@@ -64,10 +64,13 @@ struct PassArgs {
   const float* grad_sums;  // [B][K]
   const float* grad_int;   // [B][n][n]
   const float2* ud_in;     // [B][n][n]
-  // detector regions: K squares of side det_size, corners regions[k] = (y0, x0)
+  // detector regions: K squares of side det_size, corners regions[k] = (y0, x0);
+  // row_mask[y] / col_mask[x] have bit k set when region k covers row y / column x
   int K;
   int det_size;
   const int2* regions;
+  const unsigned long long* row_mask;
+  const unsigned long long* col_mask;
 };
 
 struct TileShape { int T; int S; };
@@ -93,8 +96,10 @@ struct Regions {
   int y0[kMaxRegions];
   int x0[kMaxRegions];
 };
-// Copy region corners to device memory (dst: int2 [K]).
-hipError_t launch_set_regions(const Regions& r, int2* dst, hipStream_t st);
+// Region corners (int2 [K]) and per-row / per-column coverage masks (uint64 [n])
+// in device memory.
+hipError_t launch_set_regions(const Regions& r, int n, int2* dst, unsigned long long* row_mask,
+                              unsigned long long* col_mask, hipStream_t st);
 hipError_t launch_readout(const float2* field, int batch, int n, const Regions& r, float* sums, hipStream_t st);
 
 }  // namespace lr

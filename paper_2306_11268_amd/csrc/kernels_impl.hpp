@@ -9,46 +9,76 @@
 // single pass over the field.  The angular-spectrum transfer function does not
 // factor; its hops use a row pass (FFT_x), a column pass (FFT_y, x H, IFFT_y)
 // and a row pass (IFFT_x, modulation, next FFT_x).
+//
+// Every thread owns one A-item (j = its slot) of its vector, so the A-step
+// data of a thread is a plain register array x[N1].  Global I/O of a tile is
+// batched in chunks: a thread issues several loads before it uses them.
+// Per-layer arrays (modulation, activations, dphi) are oriented [q][vec],
+// q the position along the pass axis and vec the vector index.
 #pragma once
 
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "kernels.hpp"
 #include "tile.hpp"
 
 namespace lr {
 
-// ---------------------------------------------------------------------------
-// Natural-layout tile I/O.  The tile covers vectors vec0 .. vec0+nvalid-1 and
-// layer positions q in [0, n); in shared memory position q lives in the
-// slot of natural position q + off.  Element (v, q) is global (y, x) = (vec0+v, q) for a row
-// pass and (q, vec0+v) for a column pass.  Iteration order keeps consecutive
-// threads on consecutive x, so global accesses are coalesced.
-// ---------------------------------------------------------------------------
-template <class C, int AXIS, class F>
-__device__ __forceinline__ void for_tile_elems(int n, int nvalid, F&& fn) {
-  if constexpr (AXIS == kRow) {
-    for (int v = 0; v < nvalid; ++v)
-      for (int q = threadIdx.x; q < n; q += C::P) fn(v, q);
-  } else {
-    const int total = n * C::T;
-    for (int e = threadIdx.x; e < total; e += C::P) {
-      const int q = e / C::T;
-      const int v = e - q * C::T;
-      if (v < nvalid) fn(v, q);
-    }
-  }
+// Global accesses at a uniform base plus a 32-bit unsigned element index: the
+// byte offset is formed in 32 bits so the scalar-base addressing form is used.
+template <class T>
+__device__ __forceinline__ T ld(const T* base, unsigned idx) {
+  return *reinterpret_cast<const T*>(reinterpret_cast<const char*>(base) + idx * (unsigned)sizeof(T));
+}
+template <class T>
+__device__ __forceinline__ void st(T* base, unsigned idx, T v) {
+  *reinterpret_cast<T*>(reinterpret_cast<char*>(base) + idx * (unsigned)sizeof(T)) = v;
 }
 
+// threadIdx.x behind an empty asm statement: values derived from it are not
+// hoisted out of the per-sample loop (which would keep dozens of index
+// registers alive through the whole kernel); they are recomputed next to
+// their use instead.
+__device__ __forceinline__ int opaque_tid() {
+  int t = (int)threadIdx.x;
+  asm volatile("" : "+v"(t));
+  return t;
+}
+
+// Workgroups are dispatched round-robin over the 8 XCDs (each with its own
+// L2).  The 1-D grid is remapped so that the workgroups one XCD runs at the
+// same time take consecutive tiles of the same samples: neighbouring column
+// tiles share cache lines, which then come from that XCD's L2 once.
+struct WorkItem {
+  int tile;
+  int group;
+  bool valid;
+};
+__device__ __forceinline__ WorkItem work_item(int ntiles, int ngroups) {
+  const int total = ntiles * ngroups;
+  const int per = (total + 7) / 8;
+  const int l = (int)blockIdx.x;
+  const int logical = (l & 7) * per + (l >> 3);
+  return WorkItem{logical % ntiles, logical / ntiles, logical < total};
+}
+inline int work_grid(int ntiles, int ngroups) { return 8 * ((ntiles * ngroups + 7) / 8); }
+
+// Offsets inside one sample fit in 32 bits (n <= 1024).
 template <int AXIS>
-__device__ __forceinline__ size_t nat_index(int n, int vec, int q) {
-  return AXIS == kRow ? (size_t)vec * n + q : (size_t)q * n + vec;
+__device__ __forceinline__ int nat_index(int n, int vec, int q) {
+  return AXIS == kRow ? vec * n + q : q * n + vec;
 }
 
-// Shared-memory slot of natural position p of vector v.
+// Shared-memory index of natural position p of vector v.
 template <class C>
 __device__ __forceinline__ int lds_index(int p, int v) {
   return C::Plan::slot_of_pos(p) * C::TP + v;
+}
+
+__device__ __forceinline__ bool in_region(int y, int x, int y0, int x0, int s) {
+  return (unsigned)(y - y0) < (unsigned)s && (unsigned)(x - x0) < (unsigned)s;
 }
 
 // Zero the padding positions [0, off) and [off+n, N) of every vector.
@@ -64,60 +94,132 @@ __device__ __forceinline__ void zero_padding(float2* lds, int n, int off) {
   }
 }
 
-__device__ __forceinline__ bool in_region(int y, int x, int y0, int x0, int s) {
-  return (unsigned)(y - y0) < (unsigned)s && (unsigned)(x - x0) < (unsigned)s;
+// ---------------------------------------------------------------------------
+// Batched tile walks.  A tile has nvalid vectors of n elements; thread tid
+// handles elements e = tid + i*P, i < N1 (N1 * P = T * N covers the tile).
+//   row tiles:    element e is (v, q) = divmod(e, n) of a contiguous block;
+//   column tiles: element e is (v, q) = (e mod T, e div T).
+// The walk runs in chunks of W elements: first(i, v, q) is called for the
+// whole chunk (issue loads), then second(i, v, q) (consume them).  Loads use
+// one chunk of N1 (every load of the thread in flight before the first wait);
+// stores, which do not wait, use smaller chunks.  Only valid elements are
+// visited.
+// ---------------------------------------------------------------------------
+template <class C, int AXIS, int W, class F1, class F2>
+__device__ __forceinline__ void tile_walk2(int n, int nvalid, F1&& first, F2&& second) {
+  constexpr int NCH = (C::N1 + W - 1) / W;
+  if constexpr (AXIS == kRow) {
+    const int total = nvalid * n;
+    const int dv = C::P / n;
+    const int dq = C::P - dv * n;
+    static_for<0, NCH>([&](auto c) {
+      constexpr int e0 = decltype(c)::value * W * C::P;
+      auto visit = [&](auto& f) {
+        const int tid = opaque_tid();
+        int v = (tid + e0) / n;
+        int q = (tid + e0) - v * n;
+        static_for<0, W>([&](auto i) {
+          constexpr int ii = decltype(c)::value * W + decltype(i)::value;
+          if constexpr (ii < C::N1) {
+            if (tid + ii * C::P < total) f(i, v, q);
+            q += dq;
+            v += dv;
+            if (q >= n) { q -= n; ++v; }
+          }
+        });
+      };
+      visit(first);
+      visit(second);
+    });
+  } else {
+    static_for<0, NCH>([&](auto c) {
+      auto visit = [&](auto& f) {
+        const int tid = opaque_tid();
+        static_for<0, W>([&](auto i) {
+          constexpr int ii = decltype(c)::value * W + decltype(i)::value;
+          if constexpr (ii < C::N1) {
+            const int e = tid + ii * C::P;
+            const int q = e / C::T;
+            const int v = e - q * C::T;
+            if (q < n && v < nvalid) f(i, v, q);
+          }
+        });
+      };
+      visit(first);
+      visit(second);
+    });
+  }
 }
 
-// ---------------------------------------------------------------------------
-// Loading a tile in natural order (zero padding, optional adjoint seed).
-// ---------------------------------------------------------------------------
-template <class C, int AXIS, bool SEED>
-__device__ __forceinline__ void load_tile(float2* lds, const PassArgs& a, int b, int vec0, int nvalid) {
+constexpr int kStoreChunk = 8;
+
+// Load a tile of complex (or real) natural-layout rows/columns into shared memory.
+template <class C, int AXIS>
+__device__ __forceinline__ void load_tile(float2* lds, const void* src, bool real, int n, int off, int vec0,
+                                          int nvalid) {
+  zero_padding<C>(lds, n, off);
+  float2 buf[C::N1];
+  if (real) {
+    const float* __restrict__ in = static_cast<const float*>(src);
+    tile_walk2<C, AXIS, C::N1>(n, nvalid,
+        [&](auto i, int v, int q) { buf[i.value] = c2(ld(in, nat_index<AXIS>(n, vec0 + v, q)), 0.f); },
+        [&](auto i, int v, int q) { lds[lds_index<C>(q + off, v)] = buf[i.value]; });
+  } else {
+    const float2* __restrict__ in = static_cast<const float2*>(src);
+    tile_walk2<C, AXIS, C::N1>(n, nvalid,
+        [&](auto i, int v, int q) { buf[i.value] = ld(in, nat_index<AXIS>(n, vec0 + v, q)); },
+        [&](auto i, int v, int q) { lds[lds_index<C>(q + off, v)] = buf[i.value]; });
+  }
+}
+
+// Adjoint seed at the detector plane: G_D = 2 * (dL/dI) * U_D, with dL/dI a
+// full map or constant over each detector region (from dL/dS).
+template <class C, int AXIS>
+__device__ __forceinline__ void load_seed(float2* lds, const PassArgs& a, int b, int vec0, int nvalid) {
   const int n = a.n;
   const int off = a.off;
   const size_t nn = (size_t)n * n;
   zero_padding<C>(lds, n, off);
-  if constexpr (SEED) {
-    // G_D = 2 * (dL/dI) * U_D with dL/dI a full map or region-constant from dL/dS
-    const float2* __restrict__ ud = a.ud_in + (size_t)b * nn;
-    const float* __restrict__ gint = a.grad_int ? a.grad_int + (size_t)b * nn : nullptr;
-    const float* __restrict__ gsum = a.grad_sums ? a.grad_sums + (size_t)b * a.K : nullptr;
-    const int2* __restrict__ regions = a.regions;
-    const int K = a.K;
-    const int dsz = a.det_size;
-    for_tile_elems<C, AXIS>(n, nvalid, [&](int v, int q) {
-      const int y = AXIS == kRow ? vec0 + v : q;
-      const int x = AXIS == kRow ? q : vec0 + v;
-      const size_t idx = (size_t)y * n + x;
-      float g = 0.f;
-      if (gint) {
-        g = gint[idx];
-      } else {
-        for (int k = 0; k < K; ++k) {
-          const int2 r = regions[k];
-          if (in_region(y, x, r.x, r.y, dsz)) g += gsum[k];
+  const float2* __restrict__ ud = a.ud_in + (size_t)b * nn;
+  const float* __restrict__ gint = a.grad_int ? a.grad_int + (size_t)b * nn : nullptr;
+  const float* __restrict__ gsum = a.grad_sums ? a.grad_sums + (size_t)b * a.K : nullptr;
+  float2 buf[C::N1];
+  float g[C::N1];
+  tile_walk2<C, AXIS, C::N1>(n, nvalid,
+      [&](auto i, int v, int q) {
+        const int y = AXIS == kRow ? vec0 + v : q;
+        const int x = AXIS == kRow ? q : vec0 + v;
+        float gv = 0.f;
+        if (gint) {
+          gv = ld(gint, y * n + x);
+        } else {
+          // dL/dI is dL/dS_k on region k: sum over the regions covering (y, x)
+          unsigned long long mask = ld(a.row_mask, y) & ld(a.col_mask, x);
+          while (mask) {
+            gv += gsum[__builtin_ctzll(mask)];
+            mask &= mask - 1;
+          }
         }
-      }
-      lds[lds_index<C>(q + off, v)] = g != 0.f ? cscale(ud[idx], 2.f * g) : c2(0.f, 0.f);
-    });
-  } else if (a.in_real) {
-    const float* __restrict__ in = static_cast<const float*>(a.in) + (size_t)b * nn;
-    for_tile_elems<C, AXIS>(n, nvalid, [&](int v, int q) {
-      lds[lds_index<C>(q + off, v)] = c2(in[nat_index<AXIS>(n, vec0 + v, q)], 0.f);
-    });
-  } else {
-    const float2* __restrict__ in = static_cast<const float2*>(a.in) + (size_t)b * nn;
-    for_tile_elems<C, AXIS>(n, nvalid, [&](int v, int q) {
-      lds[lds_index<C>(q + off, v)] = in[nat_index<AXIS>(n, vec0 + v, q)];
-    });
-  }
+        g[i.value] = gv;
+        buf[i.value] = gv != 0.f ? ld(ud, y * n + x) : c2(0.f, 0.f);
+      },
+      [&](auto i, int v, int q) { lds[lds_index<C>(q + off, v)] = cscale(buf[i.value], 2.f * g[i.value]); });
+}
+
+template <class C, int AXIS>
+__device__ __forceinline__ void store_tile(const float2* lds, float2* __restrict__ out, int n, int off, int vec0,
+                                           int nvalid) {
+  float2 buf[kStoreChunk];
+  tile_walk2<C, AXIS, kStoreChunk>(n, nvalid,
+      [&](auto i, int v, int q) { buf[i.value] = lds[lds_index<C>(q + off, v)]; },
+      [&](auto i, int v, int q) { st(out, nat_index<AXIS>(n, vec0 + v, q), buf[i.value]); });
 }
 
 // Detector-plane outputs from a tile that holds U_D in natural order:
 // |U|^2, U_D copies, and per-(sample, tile, region) partial sums.
 template <class C, int AXIS>
 __device__ __forceinline__ void tile_outputs(const float2* lds, float* red, const PassArgs& a, int b, int vec0,
-                                             int nvalid) {
+                                             int nvalid, int tile) {
   const int n = a.n;
   const int off = a.off;
   const size_t nn = (size_t)n * n;
@@ -125,13 +227,15 @@ __device__ __forceinline__ void tile_outputs(const float2* lds, float* red, cons
   float2* sv = a.saved_ud ? a.saved_ud + (size_t)b * nn : nullptr;
   float* io = a.intensity ? a.intensity + (size_t)b * nn : nullptr;
   if (fo || sv || io) {
-    for_tile_elems<C, AXIS>(n, nvalid, [&](int v, int q) {
-      const float2 u = lds[lds_index<C>(q + off, v)];
-      const size_t idx = nat_index<AXIS>(n, vec0 + v, q);
-      if (fo) fo[idx] = u;
-      if (sv) sv[idx] = u;
-      if (io) io[idx] = cabs2(u);
-    });
+    float2 buf[kStoreChunk];
+    tile_walk2<C, AXIS, kStoreChunk>(n, nvalid,
+        [&](auto i, int v, int q) { buf[i.value] = lds[lds_index<C>(q + off, v)]; },
+        [&](auto i, int v, int q) {
+          const int idx = nat_index<AXIS>(n, vec0 + v, q);
+          if (fo) st(fo, idx, buf[i.value]);
+          if (sv) st(sv, idx, buf[i.value]);
+          if (io) st(io, idx, cabs2(buf[i.value]));
+        });
   }
   if (a.sums_part) {
     const int K = a.K;
@@ -153,95 +257,49 @@ __device__ __forceinline__ void tile_outputs(const float2* lds, float* red, cons
         }
         part = block_sum<C::P>(my, red);
       }
-      if (threadIdx.x == 0) a.sums_part[((size_t)b * a.ntiles + blockIdx.x) * K + k] = part;
+      if (threadIdx.x == 0) a.sums_part[((size_t)b * a.ntiles + tile) * K + k] = part;
     }
   }
 }
 
-// Forward A-step (DFT over the N1 elements of each A-item).
-template <class C>
-__device__ __forceinline__ void a_forward(const Tile<C>& t) {
-  for_a_items<C>(t, [&](int j) {
-    float2 x[C::N1];
-    read_a(t, j, x);
-    Dft<C::N1, -1>::run(x);
-    write_a(t, j, x);
-  });
-}
-// Inverse A-step.
-template <class C>
-__device__ __forceinline__ void a_inverse(const Tile<C>& t) {
-  for_a_items<C>(t, [&](int j) {
-    float2 x[C::N1];
-    read_a(t, j, x);
-    Dft<C::N1, 1>::run(x);
-    write_a(t, j, x);
-  });
-}
-
-// Inverse A-step, the layer operation at every cropped position, forward A-step.
-// Forward: U_l = V * M_l (optionally stored).  Backward: dphi += Im(conj(U_l) G),
-// G *= conj(M_l); with FWD_AFTER false (last backward pass) only the
-// accumulation is done.  Oriented arrays are indexed [q][vec].
-template <class C, bool BWD, bool FWD_AFTER, class ACC>
-__device__ __forceinline__ void a_layer_op(const Tile<C>& t, const PassArgs& a, int b, int vec, bool vok, ACC& acc) {
+// ---------------------------------------------------------------------------
+// Column tiles read and write their A-items straight from/to global memory:
+// element x of A-item j is row pos(x, j) - off of column vec (pitch floats2).
+// ---------------------------------------------------------------------------
+// Walk the N1 elements of this thread's A-item along the pass axis:
+// f(k, idx, valid) with idx = (pos(k, j) - off) * pitch + vec, computed
+// incrementally (no multiplications per element).
+template <class C, class F>
+__device__ __forceinline__ void for_a_elems(int off, int n, int pitch, int vec, bool vok, F&& f) {
   using PL = typename C::Plan;
-  const int n = a.n;
-  const int off = a.off;
-  const size_t nn = (size_t)n * n;
-  const float2* __restrict__ mod = a.mod;
-  const float2* __restrict__ act_in = BWD ? a.act_in + (size_t)b * nn : nullptr;
-  float2* __restrict__ act_out = (!BWD && a.act_out) ? a.act_out + (size_t)b * nn : nullptr;
-  auto body = [&](auto ic, int j) {
-    constexpr int ii = decltype(ic)::value;
-    const int pb = PL::pos_base(j);
-    float2 x[C::N1];
-    read_a(t, j, x);
-    Dft<C::N1, 1>::run(x);
-    static_for<0, C::N1>([&](auto kc) {
-      constexpr int k = decltype(kc)::value;
-      const int q = PL::pos_at(pb, k) - off;
-      const bool in = vok && (unsigned)q < (unsigned)n;
-      float2 u = c2(0.f, 0.f);
-      if (in) {
-        const size_t oi = (size_t)q * n + vec;
-        if constexpr (!BWD) {
-          u = cmul(x[k], mod[oi]);
-          if (act_out) act_out[oi] = u;
-        } else {
-          const float2 ul = act_in[oi];
-          acc[ii][k] += ul.x * x[k].y - ul.y * x[k].x;  // Im(conj(U_l) * G)
-          if constexpr (FWD_AFTER) u = cmulc(x[k], mod[oi]);
-        }
+  const int j = opaque_tid() / C::T;
+  int p = PL::pos_base(j);
+  int idx = (p - off) * pitch + vec;
+  static_for<0, C::N1>([&](auto k) {
+    f(k, idx, vok && (unsigned)(p - off) < (unsigned)n);
+    p += C::N2;
+    idx += C::N2 * pitch;
+    if constexpr (PL::PFA) {
+      if (p >= C::N) {
+        p -= C::N;
+        idx -= C::N * pitch;
       }
-      x[k] = u;
-    });
-    if constexpr (FWD_AFTER) {
-      Dft<C::N1, -1>::run(x);
-      write_a(t, j, x);
     }
-  };
-  if constexpr (BWD) {
-    for_a_items_static<C>(t, body);
-  } else {
-    for_a_items<C>(t, [&](int i2) { body(std::integral_constant<int, 0>{}, i2); });
-  }
+  });
 }
 
-template <class C, class ACC>
-__device__ __forceinline__ void write_dphi(const Tile<C>& t, const PassArgs& a, int vec, bool vok, ACC& acc) {
-  using PL = typename C::Plan;
-  const int n = a.n;
-  const int off = a.off;
-  float* __restrict__ dp = a.dphi_part + (size_t)blockIdx.y * n * n;
-  for_a_items_static<C>(t, [&](auto ic, int j) {
-    constexpr int ii = decltype(ic)::value;
-    const int pb = PL::pos_base(j);
-    static_for<0, C::N1>([&](auto kc) {
-      constexpr int k = decltype(kc)::value;
-      const int q = PL::pos_at(pb, k) - off;
-      if (vok && (unsigned)q < (unsigned)n) dp[(size_t)q * n + vec] = acc[ii][k];
-    });
+template <class C>
+__device__ __forceinline__ void load_a_direct(const float2* __restrict__ in, int pitch, int n, int off, int vec,
+                                              bool vok, float2 (&x)[C::N1]) {
+  for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
+    x[k.value] = valid ? ld(in, idx) : c2(0.f, 0.f);
+  });
+}
+template <class C>
+__device__ __forceinline__ void store_a_direct(float2* __restrict__ out, int pitch, int n, int off, int vec,
+                                               bool vok, const float2 (&x)[C::N1]) {
+  for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
+    if (valid) st(out, idx, x[k.value]);
   });
 }
 
@@ -249,58 +307,126 @@ __device__ __forceinline__ void write_dphi(const Tile<C>& t, const PassArgs& a, 
 // Separable (Fresnel) pass.
 // ---------------------------------------------------------------------------
 template <class C, int KIND, int AXIS>
-__global__ void __launch_bounds__(C::P, C::WAVES) fresnel_pass(PassArgs a) {
+__global__ void __launch_bounds__(C::P, (KIND == kBwdMid || KIND == kBwdLast) ? C::WAVES_ACC : C::WAVES)
+    fresnel_pass(PassArgs a) {
   __shared__ float2 lds[C::LDS_ELEMS];
   __shared__ float red[C::P / 64];
+  using PL = typename C::Plan;
+  constexpr int N1 = C::N1;
   constexpr bool ACC = (KIND == kBwdMid || KIND == kBwdLast);
   constexpr bool TWO = (KIND == kFwdMid || KIND == kBwdMid);
+  constexpr bool DIRECT_IN = AXIS == kCol && (KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid ||
+                                              KIND == kBwdLast);
+  constexpr bool DIRECT_OUT = AXIS == kCol && (KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid ||
+                                               KIND == kBwdFirst);
   const Tile<C> t{lds, (int)(threadIdx.x % C::T), (int)(threadIdx.x / C::T)};
+  const int j = t.s;
 
+  const WorkItem wi = work_item(a.ntiles, (a.batch + a.spg - 1) / a.spg);
+  if (!wi.valid) return;
   const int n = a.n;
   const int off = a.off;
-  const int vec0 = blockIdx.x * C::T;
+  const size_t nn = (size_t)n * n;
+  const int vec0 = wi.tile * C::T;
   const int vec = vec0 + t.v;
   const int nvalid = min(C::T, a.nvec - vec0);
   const bool vok = t.v < nvalid;
-  const int b0 = blockIdx.y * a.spg;
+  const int b0 = wi.group * a.spg;
   const int b1 = min(a.batch, b0 + a.spg);
   const bool conj_tab = a.conj_tab != 0;
 
-  float acc[ACC ? C::IA : 1][ACC ? C::N1 : 1];
+  float acc[ACC ? N1 : 1];
   if constexpr (ACC) {
-    static_for<0, C::IA>([&](auto i) { static_for<0, C::N1>([&](auto k) { acc[i.value][k.value] = 0.f; }); });
+    static_for<0, N1>([&](auto k) { acc[k.value] = 0.f; });
   }
+  stage_table<C>(lds, a.tab);  // visible after the first barrier below
 
   for (int b = b0; b < b1; ++b) {
-    __syncthreads();
-    load_tile<C, AXIS, KIND == kBwdFirst>(lds, a, b, vec0, nvalid);
-    __syncthreads();
-    a_forward<C>(t);
-    __syncthreads();
-    b_spectral(t, a.tab, conj_tab);
-    __syncthreads();
-    if constexpr (TWO) {
-      a_layer_op<C, ACC, true>(t, a, b, vec, vok, acc);
-      __syncthreads();
-      b_spectral(t, a.tab, conj_tab);
-      __syncthreads();
-    }
-    if constexpr (KIND == kBwdLast) {
-      a_layer_op<C, true, false>(t, a, b, vec, vok, acc);
-      continue;
-    }
-    a_inverse<C>(t);
-    __syncthreads();
-    if constexpr (KIND == kFwdLast) {
-      tile_outputs<C, AXIS>(lds, red, a, b, vec0, nvalid);
+    float2 x[N1];
+    __syncthreads();  // shared memory reuse across samples
+    if constexpr (DIRECT_IN) {
+      load_a_direct<C>(static_cast<const float2*>(a.in) + (size_t)b * nn, n, n, off, vec, vok, x);
     } else {
-      float2* __restrict__ out = a.out + (size_t)b * n * n;
-      for_tile_elems<C, AXIS>(n, nvalid, [&](int v, int q) {
-        out[nat_index<AXIS>(n, vec0 + v, q)] = lds[lds_index<C>(q + off, v)];
+      if constexpr (KIND == kBwdFirst) {
+        load_seed<C, AXIS>(lds, a, b, vec0, nvalid);
+      } else {
+        const size_t es = a.in_real ? sizeof(float) : sizeof(float2);
+        load_tile<C, AXIS>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * es, a.in_real != 0, n, off, vec0,
+                           nvalid);
+      }
+      __syncthreads();
+      read_a(t, j, x);
+    }
+    Dft<N1, -1>::run(x);
+    write_a(t, j, x);
+
+    // per-element layer data, loaded now so it arrives during the B-step:
+    // modulation gamma*exp(j*phi_l) and (backward) the saved activation U_l
+    float2 m[TWO ? N1 : 1];
+    float2 ul[ACC ? N1 : 1];
+    if constexpr (TWO || ACC) {
+      const float2* __restrict__ ai = ACC ? a.act_in + (size_t)b * nn : nullptr;
+      for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
+        if constexpr (TWO) m[k.value] = in ? ld(a.mod, idx) : c2(0.f, 0.f);
+        if constexpr (ACC) ul[k.value] = in ? ld(ai, idx) : c2(0.f, 0.f);
       });
     }
+    __syncthreads();
+    b_spectral(t, conj_tab);
+    __syncthreads();
+    read_a(t, j, x);
+    Dft<N1, 1>::run(x);
+
+    if constexpr (TWO) {
+      if constexpr (KIND == kFwdMid) {
+        float2* __restrict__ ao = a.act_out ? a.act_out + (size_t)b * nn : nullptr;
+        static_for<0, N1>([&](auto k) {
+          const float2 u = cmul(x[k.value], m[k.value]);  // zero outside the aperture (crop)
+          x[k.value] = u;
+        });
+        if (ao) {
+          for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
+            if (in) st(ao, idx, x[k.value]);
+          });
+        }
+      } else {
+        static_for<0, N1>([&](auto k) {
+          const float2 g = x[k.value];
+          acc[k.value] += ul[k.value].x * g.y - ul[k.value].y * g.x;  // Im(conj(U_l) * G)
+          x[k.value] = cmulc(g, m[k.value]);
+        });
+      }
+      Dft<N1, -1>::run(x);
+      write_a(t, j, x);
+      __syncthreads();
+      b_spectral(t, conj_tab);
+      __syncthreads();
+      read_a(t, j, x);
+      Dft<N1, 1>::run(x);
+    }
+
+    if constexpr (KIND == kBwdLast) {
+      static_for<0, N1>([&](auto k) { acc[k.value] += ul[k.value].x * x[k.value].y - ul[k.value].y * x[k.value].x; });
+      continue;
+    }
+    if constexpr (DIRECT_OUT) {
+      store_a_direct<C>(a.out + (size_t)b * nn, n, n, off, vec, vok, x);
+    } else {
+      write_a(t, j, x);
+      __syncthreads();
+      if constexpr (KIND == kFwdLast) {
+        tile_outputs<C, AXIS>(lds, red, a, b, vec0, nvalid, wi.tile);
+      } else {
+        store_tile<C, AXIS>(lds, a.out + (size_t)b * nn, n, off, vec0, nvalid);
+      }
+    }
   }
-  if constexpr (ACC) write_dphi(t, a, vec, vok, acc);
+  if constexpr (ACC) {
+    float* __restrict__ dp = a.dphi_part + (size_t)wi.group * nn;
+    for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
+      if (in) st(dp, idx, acc[k.value]);
+    });
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -332,46 +458,80 @@ __device__ __forceinline__ void b_inverse_all(const Tile<C>& t) {
   }
 }
 
+// Spectrum rows (pitch N, slot order) of a row tile <-> shared memory.
+template <class C>
+__device__ __forceinline__ void load_spec_rows(float2* lds, const float2* __restrict__ in, int vec0, int nvalid) {
+  float2 buf[C::N1];
+  const int total = nvalid * C::N;
+  static_for<0, C::N1>([&](auto i) {
+    const int e = threadIdx.x + i.value * C::P;
+    if (e < total) buf[i.value] = ld(in, vec0 * C::N + e);
+  });
+  static_for<0, C::N1>([&](auto i) {
+    const int e = threadIdx.x + i.value * C::P;
+    const int v = e / C::N;
+    if (e < total) lds[(e - v * C::N) * C::TP + v] = buf[i.value];
+  });
+}
+template <class C>
+__device__ __forceinline__ void store_spec_rows(const float2* lds, float2* __restrict__ out, int vec0, int nvalid) {
+  float2 buf[C::N1];
+  const int total = nvalid * C::N;
+  static_for<0, C::N1>([&](auto i) {
+    const int e = threadIdx.x + i.value * C::P;
+    const int v = e / C::N;
+    if (e < total) buf[i.value] = lds[(e - v * C::N) * C::TP + v];
+  });
+  static_for<0, C::N1>([&](auto i) {
+    const int e = threadIdx.x + i.value * C::P;
+    if (e < total) st(out, vec0 * C::N + e, buf[i.value]);
+  });
+}
+
 template <class C, int KIND>
-__global__ void __launch_bounds__(C::P, C::WAVES) as_pass(PassArgs a) {
+__global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowBwdLast || KIND == kAsRowMid)
+                                            ? C::WAVES_ACC : C::WAVES)
+    as_pass(PassArgs a) {
   __shared__ float2 lds[C::LDS_ELEMS];
   __shared__ float red[C::P / 64];
   using PL = typename C::Plan;
   constexpr int N = C::N;
+  constexpr int N1 = C::N1;
   constexpr bool ACC = (KIND == kAsRowBwdMid || KIND == kAsRowBwdLast);
+  constexpr bool LAYER = (KIND == kAsRowMid || ACC);
   constexpr bool SPECTRAL_IN = (KIND == kAsRowMid || KIND == kAsRowLast || KIND == kAsRowBwdMid ||
                                 KIND == kAsRowBwdLast || KIND == kAsRowIfft);
   constexpr bool FWD_OUT = (KIND == kAsRowFirst || KIND == kAsRowMid || KIND == kAsRowBwdFirst ||
                             KIND == kAsRowBwdMid);
   const Tile<C> t{lds, (int)(threadIdx.x % C::T), (int)(threadIdx.x / C::T)};
+  const int j = t.s;
 
+  const WorkItem wi = work_item(a.ntiles, (a.batch + a.spg - 1) / a.spg);
+  if (!wi.valid) return;
   const int n = a.n;
   const int off = a.off;
-  const int vec0 = blockIdx.x * C::T;
+  const size_t nn = (size_t)n * n;
+  const int vec0 = wi.tile * C::T;
   const int vec = vec0 + t.v;
   const int nvalid = min(C::T, a.nvec - vec0);
   const bool vok = t.v < nvalid;
-  const int b0 = blockIdx.y * a.spg;
+  const int b0 = wi.group * a.spg;
   const int b1 = min(a.batch, b0 + a.spg);
 
-  float acc[ACC ? C::IA : 1][ACC ? C::N1 : 1];
+  float acc[ACC ? N1 : 1];
   if constexpr (ACC) {
-    static_for<0, C::IA>([&](auto i) { static_for<0, C::N1>([&](auto k) { acc[i.value][k.value] = 0.f; }); });
+    static_for<0, N1>([&](auto k) { acc[k.value] = 0.f; });
   }
 
   for (int b = b0; b < b1; ++b) {
-    __syncthreads();
+    float2 x[N1];
     if constexpr (KIND == kAsCol) {
-      // vectors: spectrum columns (slot order); positions: rows y of the padded grid
-      zero_padding<C>(lds, n, off);
+      // vectors: spectrum columns (slot order); positions: rows of the padded grid
       const float2* __restrict__ in = static_cast<const float2*>(a.in) + (size_t)b * n * N;
-      for (int e = threadIdx.x; e < n * C::T; e += C::P) {
-        const int q = e / C::T;
-        const int v = e - q * C::T;
-        if (v < nvalid) lds[lds_index<C>(q + off, v)] = in[(size_t)q * N + vec0 + v];
-      }
       __syncthreads();
-      a_forward<C>(t);
+      load_a_direct<C>(in, N, n, off, vec, vok, x);
+      Dft<N1, -1>::run(x);
+      write_a(t, j, x);
       __syncthreads();
       // B-step with the 2-D table: element k2 of item k1 is ky = freq(k1, k2)
       const bool cj = a.conj_tab != 0;
@@ -385,7 +545,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES) as_pass(PassArgs a) {
         if (vok) {
           static_for<0, C::N2>([&](auto kc) {
             constexpr int k2 = decltype(kc)::value;
-            const float2 h = a.tab[(size_t)PL::freq(k1, k2) * N + vec];
+            const float2 h = ld(a.tab, PL::freq(k1, k2) * N + vec);
             y[k2] = cj ? cmulc(y[k2], h) : cmul(y[k2], h);
           });
         }
@@ -393,61 +553,72 @@ __global__ void __launch_bounds__(C::P, C::WAVES) as_pass(PassArgs a) {
         write_b(t, k1, y);
       }
       __syncthreads();
-      a_inverse<C>(t);
-      __syncthreads();
-      float2* __restrict__ out = a.out + (size_t)b * n * N;
-      for (int e = threadIdx.x; e < n * C::T; e += C::P) {
-        const int q = e / C::T;
-        const int v = e - q * C::T;
-        if (v < nvalid) out[(size_t)q * N + vec0 + v] = lds[lds_index<C>(q + off, v)];
-      }
+      read_a(t, j, x);
+      Dft<N1, 1>::run(x);
+      store_a_direct<C>(a.out + (size_t)b * n * N, N, n, off, vec, vok, x);
       continue;
     }
 
     // ---- row passes: vectors are layer rows y = vec0 + v
+    __syncthreads();
     if constexpr (SPECTRAL_IN) {
-      const float2* __restrict__ in = static_cast<const float2*>(a.in) + (size_t)b * n * N;
-      for (int v = 0; v < nvalid; ++v)
-        for (int c = threadIdx.x; c < N; c += C::P) lds[c * C::TP + v] = in[(size_t)(vec0 + v) * N + c];
+      load_spec_rows<C>(lds, static_cast<const float2*>(a.in) + (size_t)b * n * N, vec0, nvalid);
       __syncthreads();
       b_inverse_all<C>(t);
       __syncthreads();
-      if constexpr (KIND == kAsRowMid) {
-        a_layer_op<C, false, true>(t, a, b, vec, vok, acc);
-      } else if constexpr (KIND == kAsRowBwdMid) {
-        a_layer_op<C, true, true>(t, a, b, vec, vok, acc);
-      } else if constexpr (KIND == kAsRowBwdLast) {
-        a_layer_op<C, true, false>(t, a, b, vec, vok, acc);
-        continue;
-      } else {
-        a_inverse<C>(t);  // kAsRowLast, kAsRowIfft: back to positions (crop on output)
+      read_a(t, j, x);
+      Dft<N1, 1>::run(x);
+      if constexpr (LAYER) {
+        const float2* __restrict__ ai = ACC ? a.act_in + (size_t)b * nn : nullptr;
+        float2* __restrict__ ao = (KIND == kAsRowMid && a.act_out) ? a.act_out + (size_t)b * nn : nullptr;
+        for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int oi, bool in) {
+          if constexpr (KIND == kAsRowMid) {
+            const float2 u = in ? cmul(x[k.value], ld(a.mod, oi)) : c2(0.f, 0.f);
+            if (ao && in) st(ao, oi, u);
+            x[k.value] = u;
+          } else {
+            const float2 ul = in ? ld(ai, oi) : c2(0.f, 0.f);
+            acc[k.value] += ul.x * x[k.value].y - ul.y * x[k.value].x;
+            if constexpr (KIND == kAsRowBwdMid) x[k.value] = in ? cmulc(x[k.value], ld(a.mod, oi)) : c2(0.f, 0.f);
+          }
+        });
+        if constexpr (KIND == kAsRowBwdLast) continue;
       }
     } else {
-      load_tile<C, kRow, KIND == kAsRowBwdFirst>(lds, a, b, vec0, nvalid);
+      if constexpr (KIND == kAsRowBwdFirst) {
+        load_seed<C, kRow>(lds, a, b, vec0, nvalid);
+      } else {
+        const size_t es = a.in_real ? sizeof(float) : sizeof(float2);
+        load_tile<C, kRow>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * es, a.in_real != 0, n, off, vec0,
+                           nvalid);
+      }
       __syncthreads();
-      a_forward<C>(t);
+      read_a(t, j, x);
     }
-    __syncthreads();
 
     if constexpr (FWD_OUT) {
-      if constexpr (SPECTRAL_IN) {
-        // a_layer_op already ran the forward A-step
-      }
+      Dft<N1, -1>::run(x);
+      write_a(t, j, x);
+      __syncthreads();
       b_forward_all<C>(t);
       __syncthreads();
-      float2* __restrict__ out = a.out + (size_t)b * n * N;
-      for (int v = 0; v < nvalid; ++v)
-        for (int c = threadIdx.x; c < N; c += C::P) out[(size_t)(vec0 + v) * N + c] = lds[c * C::TP + v];
-    } else if constexpr (KIND == kAsRowIfft) {
-      float2* __restrict__ out = a.out + (size_t)b * n * n;
-      for_tile_elems<C, kRow>(n, nvalid, [&](int v, int q) {
-        out[(size_t)(vec0 + v) * n + q] = lds[lds_index<C>(q + off, v)];
-      });
-    } else {  // kAsRowLast
-      tile_outputs<C, kRow>(lds, red, a, b, vec0, nvalid);
+      store_spec_rows<C>(lds, a.out + (size_t)b * n * N, vec0, nvalid);
+    } else {
+      write_a(t, j, x);  // positions, cropped on output
+      __syncthreads();
+      if constexpr (KIND == kAsRowIfft) {
+        store_tile<C, kRow>(lds, a.out + (size_t)b * nn, n, off, vec0, nvalid);
+      } else {  // kAsRowLast
+        tile_outputs<C, kRow>(lds, red, a, b, vec0, nvalid, wi.tile);
+      }
     }
   }
-  if constexpr (ACC) write_dphi(t, a, vec, vok, acc);
+  if constexpr (ACC) {
+    float* __restrict__ dp = a.dphi_part + (size_t)wi.group * nn;
+    for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
+      if (in) st(dp, idx, acc[k.value]);
+    });
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -456,23 +627,24 @@ __global__ void __launch_bounds__(C::P, C::WAVES) as_pass(PassArgs a) {
 
 // Separable chirps from the 2-D Fresnel table: row (x) chirp H[0][k] and
 // column (y) chirp H[k][0]*conj(H[0][0]) (so their product carries exp(jkz)
-// once), with the 1/N of each inverse DFT folded in, stored B-item major.
-template <class PL>
+// once), with the 1/N of each inverse DFT folded in, each stored B-item major
+// in the plan of the passes that use it.
+template <class PLR, class PLC>
 __global__ void prep_chirps_kernel(const float2* __restrict__ H, float2* __restrict__ cx, float2* __restrict__ cy) {
-  constexpr int N = PL::N;
+  constexpr int N = PLR::N;
   const float2 h00c = cconj(H[0]);
   const float inv = 1.0f / (float)N;
   for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < N; i += gridDim.x * blockDim.x) {
-    const int k1 = i / PL::N2;
-    const int k2 = i - k1 * PL::N2;
-    const int f = PL::freq(k1, k2);
-    cx[i] = cscale(H[f], inv);
-    cy[i] = cscale(cmul(H[(size_t)f * N], h00c), inv);
+    const int k1 = i / PLR::N2;
+    const int k2 = i - k1 * PLR::N2;
+    cx[i] = cscale(H[PLR::freq(k1, k2)], inv);
+    cy[i] = cscale(cmul(H[(size_t)PLC::freq(k1, k2) * N], h00c), inv);
   }
 }
 
 // Column-permuted 2-D table for the angular-spectrum column pass:
-// Hp[ky][c] = H[ky][kx(c)] / N^2, c the slot of frequency kx.
+// Hp[ky][c] = H[ky][kx(c)] / N^2, c the slot of frequency kx in the row plan
+// (the layout in which row passes store x-spectra).
 template <class PL>
 __global__ void prep_as_table_kernel(const float2* __restrict__ H, float2* __restrict__ Hp) {
   constexpr int N = PL::N;
@@ -493,26 +665,27 @@ __global__ void prep_as_table_kernel(const float2* __restrict__ H, float2* __res
 // Per-size launchers (explicitly instantiated in one translation unit per size)
 // ---------------------------------------------------------------------------
 
-template <int N> struct Shape;
-// T vectors per workgroup, S slots per vector.
-template <> struct Shape<64>   { static constexpr int T = 16, S = 8; };
-template <> struct Shape<100>  { static constexpr int T = 16, S = 4; };
-template <> struct Shape<128>  { static constexpr int T = 16, S = 8; };
-template <> struct Shape<200>  { static constexpr int T = 16, S = 8; };
-template <> struct Shape<256>  { static constexpr int T = 8, S = 16; };
-template <> struct Shape<400>  { static constexpr int T = 8, S = 8; };
-template <> struct Shape<500>  { static constexpr int T = 8, S = 8; };
-template <> struct Shape<512>  { static constexpr int T = 4, S = 16; };
-template <> struct Shape<1000> { static constexpr int T = 4, S = 16; };
-template <> struct Shape<1024> { static constexpr int T = 4, S = 16; };
+// Vectors per workgroup by FFT length (the workgroup has T * N2 threads).
+template <int N> struct TileT;
+template <> struct TileT<64>   { static constexpr int T = 16; };
+template <> struct TileT<100>  { static constexpr int T = 16; };
+template <> struct TileT<128>  { static constexpr int T = 16; };
+template <> struct TileT<200>  { static constexpr int T = 16; };
+template <> struct TileT<256>  { static constexpr int T = 8; };
+template <> struct TileT<400>  { static constexpr int T = 8; };
+template <> struct TileT<512>  { static constexpr int T = 8; };
+template <> struct TileT<1000> { static constexpr int T = 8; };
+template <> struct TileT<1024> { static constexpr int T = 4; };
 
 template <int N>
-using CfgFor = Cfg<typename PlanFor<N>::type, Shape<N>::T, Shape<N>::S>;
+using CfgFor = Cfg<typename PlanFor<N>::type, TileT<N>::T>;
+template <int N>
+using RowCfgFor = Cfg<typename RowPlanFor<N>::type, TileT<N>::T>;
 
 template <int N, int KIND, int AXIS>
 hipError_t launch_fr(const PassArgs& a, hipStream_t st) {
-  using C = CfgFor<N>;
-  const dim3 grid(a.ntiles, (a.batch + a.spg - 1) / a.spg);
+  using C = std::conditional_t<AXIS == kRow, RowCfgFor<N>, CfgFor<N>>;
+  const dim3 grid(work_grid(a.ntiles, (a.batch + a.spg - 1) / a.spg));
   hipLaunchKernelGGL((fresnel_pass<C, KIND, AXIS>), grid, dim3(C::P), 0, st, a);
   return hipGetLastError();
 }
@@ -537,8 +710,8 @@ hipError_t launch_fr_n(PassKind kind, Axis axis, const PassArgs& a, hipStream_t 
 
 template <int N, int KIND>
 hipError_t launch_as(const PassArgs& a, hipStream_t st) {
-  using C = CfgFor<N>;
-  const dim3 grid(a.ntiles, (a.batch + a.spg - 1) / a.spg);
+  using C = std::conditional_t<KIND == kAsCol, CfgFor<N>, RowCfgFor<N>>;
+  const dim3 grid(work_grid(a.ntiles, (a.batch + a.spg - 1) / a.spg));
   hipLaunchKernelGGL((as_pass<C, KIND>), grid, dim3(C::P), 0, st, a);
   return hipGetLastError();
 }
@@ -560,19 +733,20 @@ hipError_t launch_as_n(AsPassKind kind, const PassArgs& a, hipStream_t st) {
 
 template <int N>
 hipError_t prep_chirps_n(const float2* H, float2* cx, float2* cy, hipStream_t st) {
-  hipLaunchKernelGGL((prep_chirps_kernel<typename PlanFor<N>::type>), dim3((N + 255) / 256), dim3(256), 0, st, H, cx, cy);
+  hipLaunchKernelGGL((prep_chirps_kernel<typename RowPlanFor<N>::type, typename PlanFor<N>::type>), dim3((N + 255) / 256),
+                     dim3(256), 0, st, H, cx, cy);
   return hipGetLastError();
 }
 
 template <int N>
 hipError_t prep_as_n(const float2* H, float2* Hp, hipStream_t st) {
   const int blocks = (int)(((size_t)N * N + 255) / 256);
-  hipLaunchKernelGGL((prep_as_table_kernel<typename PlanFor<N>::type>), dim3(blocks < 4096 ? blocks : 4096), dim3(256), 0,
-                     st, H, Hp);
+  hipLaunchKernelGGL((prep_as_table_kernel<typename RowPlanFor<N>::type>), dim3(blocks < 4096 ? blocks : 4096), dim3(256),
+                     0, st, H, Hp);
   return hipGetLastError();
 }
 
 template <int N>
-TileShape shape_n() { return TileShape{Shape<N>::T, Shape<N>::S}; }
+TileShape shape_n() { return TileShape{CfgFor<N>::T, CfgFor<N>::S}; }
 
 }  // namespace lr

@@ -71,17 +71,25 @@ struct Plan2 {
   LR_HD static float2 twiddle(int k1, int j) { return Roots<N>::table.w[k1 * j]; }
 };
 
-// Plans by FFT length.  Sizes without an entry are rejected by the host code.
+// Plans by FFT length.  N1 is the length of the A-step transforms (one A-item
+// per thread), N2 that of the B-step ones.  Sizes without an entry are
+// rejected by the host code.  The Good-Thomas map is used where the factors
+// are coprime (no twiddles).  Row and column passes may use different plans
+// (RowPlanFor); the transfer-function tables are built for each.
 template <int N> struct PlanFor;
 template <> struct PlanFor<64>   { using type = Plan2<8, 8, false>; };
-template <> struct PlanFor<100>  { using type = Plan2<4, 25, true>; };
+template <> struct PlanFor<100>  { using type = Plan2<25, 4, true>; };
 template <> struct PlanFor<128>  { using type = Plan2<16, 8, false>; };
-template <> struct PlanFor<200>  { using type = Plan2<8, 25, true>; };
+template <> struct PlanFor<200>  { using type = Plan2<25, 8, true>; };
 template <> struct PlanFor<256>  { using type = Plan2<16, 16, false>; };
-template <> struct PlanFor<400>  { using type = Plan2<16, 25, true>; };
-template <> struct PlanFor<500>  { using type = Plan2<20, 25, false>; };
-template <> struct PlanFor<512>  { using type = Plan2<16, 32, false>; };
-template <> struct PlanFor<1000> { using type = Plan2<40, 25, false>; };
+template <> struct PlanFor<400>  { using type = Plan2<25, 16, true>; };
+template <> struct PlanFor<512>  { using type = Plan2<32, 16, false>; };
+template <> struct PlanFor<1000> { using type = Plan2<25, 40, false>; };
 template <> struct PlanFor<1024> { using type = Plan2<32, 32, false>; };
+
+template <int N>
+struct RowPlanFor {
+  using type = typename PlanFor<N>::type;
+};
 
 }  // namespace lr

@@ -11,27 +11,29 @@
 
 namespace lr {
 
-template <class PL, int T_, int S_>
+// T vectors per workgroup; slot s = tid / T owns A-item j = s (one per
+// thread, S = N2 slots) and B-items k1 = s, s + S, ...
+template <class PL, int T_>
 struct Cfg {
   using Plan = PL;
   static constexpr int N = PL::N;
   static constexpr int N1 = PL::N1;
   static constexpr int N2 = PL::N2;
   static constexpr int T = T_;
-  static constexpr int S = S_;
-  static constexpr int P = T_ * S_;
+  static constexpr int S = PL::N2;
+  static constexpr int P = T_ * S;
   static constexpr int TP = T_ + 1;
-  static constexpr int IA = (N2 + S_ - 1) / S_;
-  static constexpr int IB = (N1 + S_ - 1) / S_;
-  static constexpr bool A_FULL = (N2 % S_) == 0;
-  static constexpr bool B_FULL = (N1 % S_) == 0;
+  static constexpr int IB = (N1 + S - 1) / S;
+  static constexpr bool B_FULL = (N1 % S) == 0;
   static constexpr int LDS_ELEMS = N * TP;
   static constexpr int LDS_BYTES = LDS_ELEMS * 8 + (P / 64) * 4;
   // Waves per SIMD that shared memory (160 KiB per CU) allows; the kernels
   // ask the compiler to fit their registers to this occupancy.
   static constexpr int WG_PER_CU = (160 * 1024) / LDS_BYTES;
   static constexpr int WAVES_RAW = (WG_PER_CU * (P / 64)) / 4;
-  static constexpr int WAVES = WAVES_RAW < 1 ? 1 : (WAVES_RAW > 8 ? 8 : WAVES_RAW);
+  static constexpr int WAVES = WAVES_RAW < 1 ? 1 : (WAVES_RAW > 4 ? 4 : WAVES_RAW);
+  // kernels that also carry per-element gradient accumulators
+  static constexpr int WAVES_ACC = WAVES > 2 ? 2 : WAVES;
   static_assert(P % 64 == 0, "workgroup must be whole wavefronts");
 };
 
@@ -54,26 +56,6 @@ template <class C>
 __device__ __forceinline__ void write_a(const Tile<C>& t, int j, const float2 (&x)[C::N1]) {
   float2* p = &t.at(j);
   static_for<0, C::N1>([&](auto k) { p[k.value * C::N2 * C::TP] = x[k.value]; });
-}
-
-// Run f(ii, i2) for this thread's A-items; ii is a compile-time constant
-// (std::integral_constant) so per-item register arrays can be indexed by it.
-template <class C, class F>
-__device__ __forceinline__ void for_a_items_static(const Tile<C>& t, F&& f) {
-  static_for<0, C::IA>([&](auto ic) {
-    const int i2 = t.s + C::S * decltype(ic)::value;
-    if (C::A_FULL || i2 < C::N2) f(ic, i2);
-  });
-}
-// Same with a run-time item loop (smaller code, no per-item state).
-template <class C, class F>
-__device__ __forceinline__ void for_a_items(const Tile<C>& t, F&& f) {
-#pragma unroll 1
-  for (int ii = 0; ii < C::IA; ++ii) {
-    const int i2 = t.s + C::S * ii;
-    if (!C::A_FULL && i2 >= C::N2) break;
-    f(i2);
-  }
 }
 
 // ---- B-items -------------------------------------------------------------
@@ -108,26 +90,35 @@ __device__ __forceinline__ void b_inverse(int k1, float2 (&y)[C::N2]) {
   }
 }
 
-// B-step "forward, multiply by a per-frequency table, inverse" used by every
-// propagation: tab is ordered [k1][k2] (B-item major), conj selects conj(tab).
+// The padding column of the shared tile (vector index T, pitch T+1) holds N
+// spare entries: the per-frequency table of the pass lives there, B-item major
+// (slot of entry i = i), so B-steps read it next to their data.
 template <class C>
-__device__ __forceinline__ void b_spectral(const Tile<C>& t, const float2* __restrict__ tab, bool conj_tab) {
-#pragma unroll 1
-  for (int ii = 0; ii < C::IB; ++ii) {
-    const int k1 = t.s + C::S * ii;
-    if (!C::B_FULL && k1 >= C::N1) break;
-    float2 y[C::N2];
-    read_b(t, k1, y);
-    b_forward<C>(k1, y);
-    const float2* tk = tab + k1 * C::N2;
-    if (conj_tab) {
-      static_for<0, C::N2>([&](auto k) { y[k.value] = cmulc(y[k.value], tk[k.value]); });
-    } else {
-      static_for<0, C::N2>([&](auto k) { y[k.value] = cmul(y[k.value], tk[k.value]); });
+__device__ __forceinline__ void stage_table(float2* lds, const float2* __restrict__ tab) {
+  for (int i = threadIdx.x; i < C::N; i += C::P) lds[i * C::TP + C::T] = tab[i];
+}
+
+// B-step "forward, multiply by the staged per-frequency table, inverse" used
+// by every propagation; conj selects conj(table).  The items of a thread are
+// unrolled so their shared-memory reads overlap.
+template <class C>
+__device__ __forceinline__ void b_spectral(const Tile<C>& t, bool conj_tab) {
+  static_for<0, C::IB>([&](auto ic) {
+    const int k1 = t.s + C::S * decltype(ic)::value;
+    if (C::B_FULL || k1 < C::N1) {
+      float2 y[C::N2];
+      read_b(t, k1, y);
+      b_forward<C>(k1, y);
+      const float2* tk = t.lds + (C::N2 * k1) * C::TP + C::T;
+      if (conj_tab) {
+        static_for<0, C::N2>([&](auto k) { y[k.value] = cmulc(y[k.value], tk[k.value * C::TP]); });
+      } else {
+        static_for<0, C::N2>([&](auto k) { y[k.value] = cmul(y[k.value], tk[k.value * C::TP]); });
+      }
+      b_inverse<C>(k1, y);
+      write_b(t, k1, y);
     }
-    b_inverse<C>(k1, y);
-    write_b(t, k1, y);
-  }
+  });
 }
 
 // ---- reductions ------------------------------------------------------------
