@@ -36,7 +36,39 @@ def parse():
     ap.add_argument("--batch", type=int, default=None, help="override the batch size")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-samples", type=int, default=None, help="samples in the oracle timing run")
+    ap.add_argument("--copy-calibration", type=int, default=None, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB three times (the reference "
+                         "kernel whose FETCH_SIZE / WRITE_SIZE counters calibrate HBM traffic)")
     return ap.parse_args()
+
+
+def copy_calibration(mib: int):
+    import torch
+
+    nbytes = mib * 1024 * 1024
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": nbytes, "copies": 3}))
+
+
+def recorded_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary of
+    this workload, or None when there is none or the device sources have
+    changed since the counters were taken."""
+    from paper_2306_11268_amd.build import source_digest
+
+    path = os.path.join(ROOT, "profiles", f"fresnel_passes__{workload}__traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        doc = json.load(fh)
+    if doc.get("source_digest") != source_digest() or kernel not in doc.get("kernels", {}):
+        return None
+    return doc["kernels"][kernel]["hbm_bytes_per_dispatch"]
 
 
 def algorithmic_bytes_per_sample(kind: str, n: int) -> float:
@@ -78,8 +110,8 @@ def oracle_baseline(w, batch, amp, phi, labels):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU only; the batch-sharded design for more "
-                                   "GPUs is described but not launched", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "bench.py measures one GPU only; the batch-sharded design for more "
+                                   "GPUs is documented but not launched", "n_gpus": args.gpus}))
         sys.exit(2)
 
     import numpy as np
@@ -91,6 +123,9 @@ def main():
     if not torch.cuda.is_available():
         print(json.dumps({"error": "no GPU visible"}))
         sys.exit(1)
+    if args.copy_calibration is not None:
+        copy_calibration(args.copy_calibration)
+        return
     lb.load()
     w = wl.WORKLOADS[args.workload]
     if w.kind != "train" or w.grad != "ce":
@@ -149,9 +184,12 @@ def main():
         avg_s = kt[dom]["ms"] / kt[dom]["count"] / 1e3
         bytes_launch = algorithmic_bytes_per_sample(kind, w.n) * batch
         achieved = bytes_launch / avg_s / 1e9
+        traffic = recorded_traffic(w.name, dom) if batch == w.batch else None
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None, "kernel": dom,
-                "avg_launch_us": round(avg_s * 1e6, 2), "algorithmic_bytes_per_launch": int(bytes_launch)}
+                "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic, "kernel": dom,
+                "avg_launch_us": round(avg_s * 1e6, 2), "algorithmic_bytes_per_launch": int(bytes_launch),
+                "traffic_unit": "HBM bytes per launch (FETCH_SIZE, WRITE_SIZE scaled by a copy calibration)",
+                "traffic_gbps": round(traffic / avg_s / 1e9, 1) if traffic else None}
 
     # whole-step algorithmic traffic per sample: forward reads the amplitude (4 n^2), writes every
     # activation and reads it back once (16 n^2 per layer) and keeps the detector regions of U_D

@@ -15,8 +15,7 @@ hot path computes, written from the LightRidge paper (arXiv 2306.11268):
 * a loss on the detector sums and the gradient with respect to every phase
   mask (§2.1: the system is differentiable from detector to source).
 
-Readings taken where the paper is silent or ambiguous (each is listed in
-the design doc with its reason):
+Readings taken where the paper is silent or ambiguous:
 
 * transfer functions are the analytic ones, sampled on the unshifted DFT
   frequency grid f_k = k'/(M*dx), k' = k for k < (M+1)//2 else k - M;

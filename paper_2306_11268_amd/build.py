@@ -35,6 +35,23 @@ COMMON = [
 ]
 
 
+def source_digest() -> str:
+    """SHA-256 over the device sources, the public header and the compile flags.
+
+    Hardware-counter figures recorded for a kernel are only valid for the
+    sources they were taken from; a changed digest marks them stale."""
+    import hashlib
+    h = hashlib.sha256()
+    files = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".hpp")))
+    files.append(os.path.join(os.path.dirname(PKG), "include", "lr.h"))
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    h.update(" ".join(COMMON).encode())
+    return h.hexdigest()[:16]
+
+
 def hipcc() -> str:
     for cand in (os.environ.get("HIPCC"), shutil.which("hipcc"), "/opt/rocm/bin/hipcc"):
         if cand and os.path.exists(cand):
