@@ -123,10 +123,14 @@ int lr_tf_build(double wavelength, double pixel_pitch, double distance, int32_t 
 int64_t lr_workspace_size(const lr_donn* net, int32_t batch, int32_t op);
 
 /* Bytes of the saved-state buffer that lr_donn_forward fills for
- * lr_donn_backward: L activations U_l then U_D, each complex64 [batch][n][n].
- * Activation l (1-based) is stored transposed ([batch][x][y]) when
- * lr_saved_layer_transposed() says so, natural ([batch][y][x]) otherwise;
- * U_D is always natural.  Negative lr_status on invalid arguments. */
+ * lr_donn_backward: the L activations U_l, then one detector-plane field, each
+ * complex64 [batch][n][n].  Activation l (1-based) is stored transposed
+ * ([batch][x][y]) when lr_saved_layer_transposed() says so, natural
+ * ([batch][y][x]) otherwise.  The detector-plane field is internal state: the
+ * Fresnel path keeps the field after the first-axis half of the last hop
+ * (lr_donn_backward finishes that hop itself, on the rows or columns the seed
+ * needs), the angular-spectrum path keeps U_D.  Negative lr_status on invalid
+ * arguments. */
 int64_t lr_saved_size(const lr_donn* net, int32_t batch);
 int32_t lr_saved_layer_transposed(const lr_donn* net, int32_t layer);
 

@@ -192,12 +192,14 @@ class Network:
         return bool(load().lr_saved_layer_transposed(ctypes.byref(self.c), int(layer)))
 
     def saved_activation(self, saved, batch: int, layer: int):
-        """View of U_layer (1-based; layer L+1 is U_D) from a saved buffer, natural [B, n, n]."""
+        """View of U_layer (1-based, layer <= L) from a saved buffer, natural [B, n, n]."""
         torch = _torch()
+        if not 1 <= layer <= self.num_layers:
+            raise ValueError(f"layer must be in 1..{self.num_layers}")
         nn = self.n * self.n
         flat = saved.view(torch.complex64)[: (self.num_layers + 1) * batch * nn]
         t = flat[(layer - 1) * batch * nn: layer * batch * nn].view(batch, self.n, self.n)
-        if layer <= self.num_layers and self.layer_transposed(layer):
+        if self.layer_transposed(layer):
             t = t.transpose(1, 2)
         return t
 

@@ -120,7 +120,8 @@ size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 struct Layout {
   size_t chirp_x = 0, chirp_y = 0, hp = 0, mod = 0, w0 = 0, w1 = 0;
-  size_t sums_part = 0, grad_sums = 0, dphi_part = 0, regions = 0, row_mask = 0, col_mask = 0, total = 0;
+  size_t sums_part = 0, grad_sums = 0, dphi_part = 0, regions = 0, row_mask = 0, col_mask = 0, row_perm = 0,
+         col_perm = 0, total = 0;
   int ntiles_vec = 0;   // tiles over n vectors
   int ntiles_spec = 0;  // tiles over n_fft spectrum columns (angular spectrum)
   int groups = 1;
@@ -160,6 +161,8 @@ Layout make_layout(const lr_donn* net, int batch, int op) {
     L.regions = take(static_cast<size_t>(K) * 8);
     L.row_mask = take(static_cast<size_t>(n) * 8);
     L.col_mask = take(static_cast<size_t>(n) * 8);
+    L.row_perm = take(static_cast<size_t>(n) * 4);
+    L.col_perm = take(static_cast<size_t>(n) * 4);
   }
   if (op == LR_OP_FORWARD && K > 0) L.sums_part = take(static_cast<size_t>(batch) * L.ntiles_vec * K * 4);
   if (op == LR_OP_BACKWARD) {
@@ -245,8 +248,35 @@ int upload_regions(const lr_donn* net, const Layout& L, void* w, hipStream_t st)
   const lr::Regions r = host_regions(net->det);
   return run_timed("set_regions", st, [&] {
     return lr::launch_set_regions(r, net->n, at<int2>(w, L.regions), at<unsigned long long>(w, L.row_mask),
-                                  at<unsigned long long>(w, L.col_mask), st);
+                                  at<unsigned long long>(w, L.col_mask), at<int>(w, L.row_perm),
+                                  at<int>(w, L.col_perm), st);
   });
+}
+
+// Number of rows (axis = row) or columns covered by at least one detector
+// region: the same test the region kernel applies when it orders them first.
+int covered_vectors(const lr_detector& d, int n, Axis ax) {
+  int c = 0;
+  for (int i = 0; i < n; ++i) {
+    bool hit = false;
+    for (int k = 0; k < d.num && !hit; ++k) {
+      const int lo = ax == lr::kRow ? d.y0[k] : d.x0[k];
+      hit = static_cast<unsigned>(i - lo) < static_cast<unsigned>(d.size);
+    }
+    c += hit ? 1 : 0;
+  }
+  return c;
+}
+
+// Restrict a detector-plane pass along `ax` to the vectors the regions
+// cover; with zero_rest, tiles after those write zero vectors over the rest.
+void restrict_to_regions(PassArgs& a, const lr_detector& d, const Layout& L, void* w, Axis ax, int tile_t,
+                         bool zero_rest) {
+  const int n = a.n;
+  a.vperm = at<int>(w, ax == lr::kRow ? L.row_perm : L.col_perm);
+  a.nact = covered_vectors(d, n, ax);
+  a.ntiles_act = ceil_div(a.nact, tile_t);
+  a.ntiles = a.ntiles_act + (zero_rest ? ceil_div(n - a.nact, tile_t) : 0);
 }
 
 void set_detector(PassArgs& a, const lr_detector& d, const Layout& L, void* w) {
@@ -460,6 +490,8 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   if (d_sums) LR_TRY(upload_regions(net, L, d_work, st));
 
   PassArgs a = base_args(net, batch);
+  const int tile_t = lr::tile_shape(N, 0).T;
+  int sum_tiles = L.ntiles_vec;  // tiles that wrote partial detector sums
   if (net->approx == LR_FRESNEL) {
     a.nvec = n;
     a.ntiles = L.ntiles_vec;
@@ -472,32 +504,40 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
     LR_TRY(fr_pass(N, lr::kPropOnce, lr::kRow, a, st));
     a.in_real = 0;
     int cur = 0;
-    // passes 2..L+1: end of hop l, modulation of layer l, start of hop l+1
+    // passes 2..L+1: end of hop l, modulation of layer l, start of hop l+1.
+    // The last of them writes W (the field after the first-axis half of hop
+    // L+1) into the saved state, where the backward pass finds it.
+    float2* w_last = saved ? saved + static_cast<size_t>(Lyr) * batch * nn : nullptr;
     for (int l = 1; l <= Lyr; ++l) {
       const Axis ax = pass_axis(l + 1);
       a.in = w[cur];
-      a.out = w[cur ^ 1];
+      a.out = (l == Lyr && w_last) ? w_last : w[cur ^ 1];
       a.tab = chirp(ax);
       a.mod = ws_mod + static_cast<size_t>(l - 1) * nn;
       a.act_out = saved ? saved + static_cast<size_t>(l - 1) * batch * nn : nullptr;
       LR_TRY(fr_pass(N, lr::kFwdMid, ax, a, st));
       cur ^= 1;
     }
-    // pass L+2: end of hop L+1, detector plane
-    const Axis ax = pass_axis(Lyr + 2);
-    a.in = w[cur];
-    a.out = nullptr;
-    a.tab = chirp(ax);
-    a.mod = nullptr;
-    a.act_out = nullptr;
-    a.intensity = d_intensity;
-    a.field_out = reinterpret_cast<float2*>(d_field_out);
-    a.saved_ud = saved ? saved + static_cast<size_t>(Lyr) * batch * nn : nullptr;
-    if (d_sums) {
-      set_detector(a, net->det, L, d_work);
-      a.sums_part = at<float>(d_work, L.sums_part);
+    // pass L+2: rest of hop L+1, detector plane
+    if (d_sums || d_intensity || d_field_out) {
+      const Axis ax = pass_axis(Lyr + 2);
+      PassArgs d = a;
+      d.in = w_last ? w_last : w[cur];
+      d.out = nullptr;
+      d.tab = chirp(ax);
+      d.mod = nullptr;
+      d.act_out = nullptr;
+      d.intensity = d_intensity;
+      d.field_out = reinterpret_cast<float2*>(d_field_out);
+      if (d_sums) {
+        set_detector(d, net->det, L, d_work);
+        d.sums_part = at<float>(d_work, L.sums_part);
+        // sums only: transform just the rows / columns the regions cover
+        if (!d_intensity && !d_field_out) restrict_to_regions(d, net->det, L, d_work, ax, tile_t, false);
+      }
+      sum_tiles = d.ntiles;
+      LR_TRY(fr_pass(N, lr::kFwdLast, ax, d, st));
     }
-    LR_TRY(fr_pass(N, lr::kFwdLast, ax, a, st));
   } else {
     a.nvec = n;
     a.ntiles = L.ntiles_vec;
@@ -540,7 +580,7 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   }
   if (d_sums) {
     LR_TRY(run_timed("finish_sums", st, [&] {
-      return lr::launch_finish_sums(at<float>(d_work, L.sums_part), batch, L.ntiles_vec, net->det.num, d_sums, st);
+      return lr::launch_finish_sums(at<float>(d_work, L.sums_part), batch, sum_tiles, net->det.num, d_sums, st);
     }));
   }
   return LR_OK;
@@ -606,15 +646,18 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
 
   if (net->approx == LR_FRESNEL) {
     auto chirp = [&](Axis ax) { return at<float2>(d_work, ax == lr::kRow ? L.chirp_x : L.chirp_y); };
-    // adjoint of the last sweep (hop L+1), seeded at the detector plane
+    // rest of hop L+1 from the saved W, seed at the detector plane, adjoint of that half hop
     {
       PassArgs s = a;
       const Axis ax = pass_axis(Lyr + 2);
       s.tab = chirp(ax);
-      s.ud_in = saved + static_cast<size_t>(Lyr) * batch * nn;
+      s.in = saved + static_cast<size_t>(Lyr) * batch * nn;
       s.grad_int = d_grad_intensity;
       s.grad_sums = gsum;
-      if (gsum) set_detector(s, net->det, L, d_work);
+      if (gsum) {
+        set_detector(s, net->det, L, d_work);
+        restrict_to_regions(s, net->det, L, d_work, ax, lr::tile_shape(N, 0).T, true);
+      }
       s.out = w[0];
       LR_TRY(fr_pass(N, lr::kBwdFirst, ax, s, st));
     }

@@ -108,13 +108,19 @@ __global__ void __launch_bounds__(256) reduce_dphi_kernel(const float* __restric
   }
 }
 
-// Detector readout from a field: one workgroup per (sample, region).
-__global__ void set_regions_kernel(Regions reg, int n, int2* dst, unsigned long long* row_mask,
-                                   unsigned long long* col_mask) {
-  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+// Region corners, per-row / per-column coverage masks and the covered-first
+// permutations of rows and columns: covered indices in ascending order, then
+// the uncovered ones.  One workgroup of 1024 threads, thread i handles row i
+// and column i (n <= 1024).
+__global__ void __launch_bounds__(1024) set_regions_kernel(Regions reg, int n, int2* dst,
+                                                           unsigned long long* row_mask,
+                                                           unsigned long long* col_mask, int* row_perm,
+                                                           int* col_perm) {
+  __shared__ int wave_count[2][16];
+  const int i = threadIdx.x;
   if (i < reg.K) dst[i] = make_int2(reg.y0[i], reg.x0[i]);
+  unsigned long long rm = 0, cm = 0;
   if (i < n) {
-    unsigned long long rm = 0, cm = 0;
     for (int k = 0; k < reg.K; ++k) {
       if ((unsigned)(i - reg.y0[k]) < (unsigned)reg.s) rm |= 1ull << k;
       if ((unsigned)(i - reg.x0[k]) < (unsigned)reg.s) cm |= 1ull << k;
@@ -122,8 +128,35 @@ __global__ void set_regions_kernel(Regions reg, int n, int2* dst, unsigned long 
     row_mask[i] = rm;
     col_mask[i] = cm;
   }
+  const bool rc = i < n && rm != 0;
+  const bool cc = i < n && cm != 0;
+  const int lane = i & 63;
+  const int wave = i >> 6;
+  const unsigned long long rb = __ballot(rc);
+  const unsigned long long cb = __ballot(cc);
+  const unsigned long long below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  if (lane == 0) {
+    wave_count[0][wave] = __popcll(rb);
+    wave_count[1][wave] = __popcll(cb);
+  }
+  __syncthreads();
+  int r_rank = __popcll(rb & below), c_rank = __popcll(cb & below), r_total = 0, c_total = 0;
+  for (int w = 0; w < 16; ++w) {
+    if (w < wave) {
+      r_rank += wave_count[0][w];
+      c_rank += wave_count[1][w];
+    }
+    r_total += wave_count[0][w];
+    c_total += wave_count[1][w];
+  }
+  if (i < n) {
+    // r_rank = covered rows before i, so i - r_rank uncovered rows precede it
+    row_perm[rc ? r_rank : r_total + (i - r_rank)] = i;
+    col_perm[cc ? c_rank : c_total + (i - c_rank)] = i;
+  }
 }
 
+// Detector readout from a field: one workgroup per (sample, region).
 __global__ void __launch_bounds__(256) readout_kernel(const float2* __restrict__ field, int n, Regions reg,
                                                       float* __restrict__ sums) {
   __shared__ float red[4];
@@ -271,9 +304,10 @@ hipError_t launch_reduce_dphi(const float* part, int groups, int n, int transpos
 }
 
 hipError_t launch_set_regions(const Regions& r, int n, int2* dst, unsigned long long* row_mask,
-                              unsigned long long* col_mask, hipStream_t st) {
-  const int m = n > kMaxRegions ? n : kMaxRegions;
-  hipLaunchKernelGGL(set_regions_kernel, dim3((m + 255) / 256), dim3(256), 0, st, r, n, dst, row_mask, col_mask);
+                              unsigned long long* col_mask, int* row_perm, int* col_perm, hipStream_t st) {
+  if (n < 1 || n > 1024 || r.K < 0 || r.K > kMaxRegions) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(set_regions_kernel, dim3(1), dim3(1024), 0, st, r, n, dst, row_mask, col_mask, row_perm,
+                     col_perm);
   return hipGetLastError();
 }
 

@@ -15,7 +15,7 @@ enum PassKind : int {
   kPropOnce = 0,   // load -> one 1-D propagation -> store
   kFwdMid = 1,     // load -> prop -> x M_l (store U_l) -> prop -> store
   kFwdLast = 2,    // load -> prop -> detector-plane outputs
-  kBwdFirst = 3,   // seed 2*(dL/dI)*U_D -> adjoint prop -> store
+  kBwdFirst = 3,   // load -> prop (U_D) -> seed 2*(dL/dI)*U_D -> adjoint prop -> store
   kBwdMid = 4,     // load -> adj prop -> dphi_l -> x conj(M_l) -> adj prop -> store
   kBwdLast = 5,    // load -> adj prop -> dphi_1
 };
@@ -58,12 +58,19 @@ struct PassArgs {
   // detector-plane outputs (natural [B][n][n] layouts)
   float* intensity;
   float2* field_out;
-  float2* saved_ud;
+  float2* saved_ud;     // angular-spectrum path only
   float* sums_part;     // [B][ntiles][K]
   // backward seed
   const float* grad_sums;  // [B][K]
   const float* grad_int;   // [B][n][n]
-  const float2* ud_in;     // [B][n][n]
+  const float2* ud_in;     // [B][n][n] (angular-spectrum path)
+  // Detector-plane passes restricted to the vectors the detector regions
+  // cover: vperm lists those nact vectors first (ascending), then the others.
+  // Tiles [0, ntiles_act) transform the covered vectors; a backward seed pass
+  // writes zero vectors over the rest with tiles [ntiles_act, ntiles).
+  const int* vperm;
+  int nact;
+  int ntiles_act;
   // detector regions: K squares of side det_size, corners regions[k] = (y0, x0);
   // row_mask[y] / col_mask[x] have bit k set when region k covers row y / column x
   int K;
@@ -96,10 +103,11 @@ struct Regions {
   int y0[kMaxRegions];
   int x0[kMaxRegions];
 };
-// Region corners (int2 [K]) and per-row / per-column coverage masks (uint64 [n])
-// in device memory.
+// Region corners (int2 [K]), per-row / per-column coverage masks (uint64 [n])
+// and the covered-first permutations of rows and of columns (int [n] each)
+// in device memory.  n <= 1024.
 hipError_t launch_set_regions(const Regions& r, int n, int2* dst, unsigned long long* row_mask,
-                              unsigned long long* col_mask, hipStream_t st);
+                              unsigned long long* col_mask, int* row_perm, int* col_perm, hipStream_t st);
 hipError_t launch_readout(const float2* field, int batch, int n, const Regions& r, float* sums, hipStream_t st);
 
 }  // namespace lr

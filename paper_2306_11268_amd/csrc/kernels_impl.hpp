@@ -153,24 +153,36 @@ __device__ __forceinline__ void tile_walk2(int n, int nvalid, F1&& first, F2&& s
 
 constexpr int kStoreChunk = 8;
 
-// Load a tile of complex (or real) natural-layout rows/columns into shared memory.
-template <class C, int AXIS>
-__device__ __forceinline__ void load_tile(float2* lds, const void* src, bool real, int n, int off, int vec0,
+// Load a tile of complex (or real) natural-layout rows/columns into shared
+// memory.  Tile vector v is field row/column vf(v).
+template <class C, int AXIS, class VF>
+__device__ __forceinline__ void load_tile(float2* lds, const void* src, bool real, int n, int off, VF&& vf,
                                           int nvalid) {
   zero_padding<C>(lds, n, off);
   float2 buf[C::N1];
   if (real) {
     const float* __restrict__ in = static_cast<const float*>(src);
     tile_walk2<C, AXIS, C::N1>(n, nvalid,
-        [&](auto i, int v, int q) { buf[i.value] = c2(ld(in, nat_index<AXIS>(n, vec0 + v, q)), 0.f); },
+        [&](auto i, int v, int q) { buf[i.value] = c2(ld(in, nat_index<AXIS>(n, vf(v), q)), 0.f); },
         [&](auto i, int v, int q) { lds[lds_index<C>(q + off, v)] = buf[i.value]; });
   } else {
     const float2* __restrict__ in = static_cast<const float2*>(src);
     tile_walk2<C, AXIS, C::N1>(n, nvalid,
-        [&](auto i, int v, int q) { buf[i.value] = ld(in, nat_index<AXIS>(n, vec0 + v, q)); },
+        [&](auto i, int v, int q) { buf[i.value] = ld(in, nat_index<AXIS>(n, vf(v), q)); },
         [&](auto i, int v, int q) { lds[lds_index<C>(q + off, v)] = buf[i.value]; });
   }
 }
+
+// Tile vector v is field vector vec0 + v.
+struct Consecutive {
+  int vec0;
+  __device__ __forceinline__ int operator()(int v) const { return vec0 + v; }
+};
+// Tile vector v is field vector map[v] (shared memory).
+struct Mapped {
+  const int* map;
+  __device__ __forceinline__ int operator()(int v) const { return map[v]; }
+};
 
 // Adjoint seed at the detector plane: G_D = 2 * (dL/dI) * U_D, with dL/dI a
 // full map or constant over each detector region (from dL/dS).
@@ -206,20 +218,32 @@ __device__ __forceinline__ void load_seed(float2* lds, const PassArgs& a, int b,
       [&](auto i, int v, int q) { lds[lds_index<C>(q + off, v)] = cscale(buf[i.value], 2.f * g[i.value]); });
 }
 
-template <class C, int AXIS>
-__device__ __forceinline__ void store_tile(const float2* lds, float2* __restrict__ out, int n, int off, int vec0,
+template <class C, int AXIS, class VF>
+__device__ __forceinline__ void store_tile(const float2* lds, float2* __restrict__ out, int n, int off, VF&& vf,
                                            int nvalid) {
   float2 buf[kStoreChunk];
   tile_walk2<C, AXIS, kStoreChunk>(n, nvalid,
       [&](auto i, int v, int q) { buf[i.value] = lds[lds_index<C>(q + off, v)]; },
-      [&](auto i, int v, int q) { st(out, nat_index<AXIS>(n, vec0 + v, q), buf[i.value]); });
+      [&](auto i, int v, int q) { st(out, nat_index<AXIS>(n, vf(v), q), buf[i.value]); });
+}
+
+// Zero vectors vf(0..nvalid) of a natural-layout field.
+template <class C, int AXIS, class VF>
+__device__ __forceinline__ void zero_vectors(float2* __restrict__ out, int n, VF&& vf, int nvalid) {
+  tile_walk2<C, AXIS, kStoreChunk>(n, nvalid, [&](auto, int, int) {},
+      [&](auto, int v, int q) { st(out, nat_index<AXIS>(n, vf(v), q), c2(0.f, 0.f)); });
 }
 
 // Detector-plane outputs from a tile that holds U_D in natural order:
-// |U|^2, U_D copies, and per-(sample, tile, region) partial sums.
-template <class C, int AXIS>
-__device__ __forceinline__ void tile_outputs(const float2* lds, float* red, const PassArgs& a, int b, int vec0,
+// |U|^2, U_D copies, and per-(sample, tile, region) partial sums.  The
+// partial sums are formed in a fixed order: thread pairs (region k, tile
+// vector v) sum their vector's run of |U|^2 inside the region into rsum
+// ([K][T] floats of shared memory), then one thread per region adds the T
+// runs.
+template <class C, int AXIS, class VF>
+__device__ __forceinline__ void tile_outputs(const float2* lds, float* rsum, const PassArgs& a, int b, VF&& vf,
                                              int nvalid, int tile) {
+  using PL = typename C::Plan;
   const int n = a.n;
   const int off = a.off;
   const size_t nn = (size_t)n * n;
@@ -231,7 +255,7 @@ __device__ __forceinline__ void tile_outputs(const float2* lds, float* red, cons
     tile_walk2<C, AXIS, kStoreChunk>(n, nvalid,
         [&](auto i, int v, int q) { buf[i.value] = lds[lds_index<C>(q + off, v)]; },
         [&](auto i, int v, int q) {
-          const int idx = nat_index<AXIS>(n, vec0 + v, q);
+          const int idx = nat_index<AXIS>(n, vf(v), q);
           if (fo) st(fo, idx, buf[i.value]);
           if (sv) st(sv, idx, buf[i.value]);
           if (io) st(io, idx, cabs2(buf[i.value]));
@@ -240,24 +264,29 @@ __device__ __forceinline__ void tile_outputs(const float2* lds, float* red, cons
   if (a.sums_part) {
     const int K = a.K;
     const int s = a.det_size;
-    for (int k = 0; k < K; ++k) {
-      const int2 r = a.regions[k];                 // (y0, x0)
-      const int vlo_g = AXIS == kRow ? r.x : r.y;  // region start along the vector index
-      const int qlo = AXIS == kRow ? r.y : r.x;    // region start along positions
-      const int v_lo = max(vlo_g - vec0, 0);
-      const int v_hi = min(vlo_g + s - vec0, nvalid);
-      float part = 0.f;
-      if (v_hi > v_lo) {
-        const int nv = v_hi - v_lo;
-        float my = 0.f;
-        for (int e = threadIdx.x; e < nv * s; e += C::P) {
-          const int qq = e / nv;
-          const int vv = e - qq * nv;
-          my += cabs2(lds[lds_index<C>(qlo + qq + off, v_lo + vv)]);
+    for (int idx = threadIdx.x; idx < K * C::T; idx += C::P) {
+      const int k = idx / C::T;
+      const int v = idx - k * C::T;
+      float run = 0.f;
+      if (v < nvalid) {
+        const int2 r = a.regions[k];                // (y0, x0)
+        const int vlo = AXIS == kRow ? r.x : r.y;   // region start along the vector index
+        const int qlo = AXIS == kRow ? r.y : r.x;   // region start along positions
+        if ((unsigned)(vf(v) - vlo) < (unsigned)s) {
+          auto w = PL::walk(qlo + off);
+          for (int d = 0; d < s; ++d) {
+            run += cabs2(lds[PL::walk_slot(w) * C::TP + v]);
+            PL::walk_next(w);
+          }
         }
-        part = block_sum<C::P>(my, red);
       }
-      if (threadIdx.x == 0) a.sums_part[((size_t)b * a.ntiles + tile) * K + k] = part;
+      rsum[idx] = run;
+    }
+    __syncthreads();
+    for (int k = threadIdx.x; k < K; k += C::P) {
+      float part = 0.f;
+      for (int v = 0; v < C::T; ++v) part += rsum[k * C::T + v];
+      a.sums_part[((size_t)b * a.ntiles + tile) * K + k] = part;
     }
   }
 }
@@ -304,21 +333,18 @@ __device__ __forceinline__ void store_a_direct(float2* __restrict__ out, int pit
 }
 
 // ---------------------------------------------------------------------------
-// Separable (Fresnel) pass.
+// Separable (Fresnel) passes through the layers.
 // ---------------------------------------------------------------------------
 template <class C, int KIND, int AXIS>
 __global__ void __launch_bounds__(C::P, (KIND == kBwdMid || KIND == kBwdLast) ? C::WAVES_ACC : C::WAVES)
     fresnel_pass(PassArgs a) {
+  static_assert(KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid || KIND == kBwdLast,
+                "detector-plane kinds run in detector_pass");
   __shared__ float2 lds[C::LDS_ELEMS];
-  __shared__ float red[C::P / 64];
-  using PL = typename C::Plan;
   constexpr int N1 = C::N1;
   constexpr bool ACC = (KIND == kBwdMid || KIND == kBwdLast);
   constexpr bool TWO = (KIND == kFwdMid || KIND == kBwdMid);
-  constexpr bool DIRECT_IN = AXIS == kCol && (KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid ||
-                                              KIND == kBwdLast);
-  constexpr bool DIRECT_OUT = AXIS == kCol && (KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid ||
-                                               KIND == kBwdFirst);
+  constexpr bool DIRECT = AXIS == kCol;  // column tiles address their A-items in global memory
   const Tile<C> t{lds, (int)(threadIdx.x % C::T), (int)(threadIdx.x / C::T)};
   const int j = t.s;
 
@@ -344,16 +370,12 @@ __global__ void __launch_bounds__(C::P, (KIND == kBwdMid || KIND == kBwdLast) ? 
   for (int b = b0; b < b1; ++b) {
     float2 x[N1];
     __syncthreads();  // shared memory reuse across samples
-    if constexpr (DIRECT_IN) {
+    if constexpr (DIRECT) {
       load_a_direct<C>(static_cast<const float2*>(a.in) + (size_t)b * nn, n, n, off, vec, vok, x);
     } else {
-      if constexpr (KIND == kBwdFirst) {
-        load_seed<C, AXIS>(lds, a, b, vec0, nvalid);
-      } else {
-        const size_t es = a.in_real ? sizeof(float) : sizeof(float2);
-        load_tile<C, AXIS>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * es, a.in_real != 0, n, off, vec0,
-                           nvalid);
-      }
+      const size_t es = a.in_real ? sizeof(float) : sizeof(float2);
+      load_tile<C, AXIS>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * es, a.in_real != 0, n, off,
+                         Consecutive{vec0}, nvalid);
       __syncthreads();
       read_a(t, j, x);
     }
@@ -409,16 +431,12 @@ __global__ void __launch_bounds__(C::P, (KIND == kBwdMid || KIND == kBwdLast) ? 
       static_for<0, N1>([&](auto k) { acc[k.value] += ul[k.value].x * x[k.value].y - ul[k.value].y * x[k.value].x; });
       continue;
     }
-    if constexpr (DIRECT_OUT) {
+    if constexpr (DIRECT) {
       store_a_direct<C>(a.out + (size_t)b * nn, n, n, off, vec, vok, x);
     } else {
       write_a(t, j, x);
       __syncthreads();
-      if constexpr (KIND == kFwdLast) {
-        tile_outputs<C, AXIS>(lds, red, a, b, vec0, nvalid, wi.tile);
-      } else {
-        store_tile<C, AXIS>(lds, a.out + (size_t)b * nn, n, off, vec0, nvalid);
-      }
+      store_tile<C, AXIS>(lds, a.out + (size_t)b * nn, n, off, Consecutive{vec0}, nvalid);
     }
   }
   if constexpr (ACC) {
@@ -426,6 +444,132 @@ __global__ void __launch_bounds__(C::P, (KIND == kBwdMid || KIND == kBwdLast) ? 
     for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
       if (in) st(dp, idx, acc[k.value]);
     });
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Detector-plane passes of the separable path.  Their input W is the field
+// after the first-axis half of the last hop (it is also what the forward pass
+// keeps for the backward one).
+//   kFwdLast:  W -> rest of the hop -> U_D -> |U_D|^2, U_D, region partial sums
+//   kBwdFirst: W -> rest of the hop -> U_D -> G_D = 2 (dL/dI) U_D -> adjoint of
+//              that half hop -> G
+// A region loss depends on U_D only on the rows (row pass) or columns (column
+// pass) the detector regions cover, and G_D vanishes on the others; with
+// a.vperm only those vectors are transformed, and the seed pass writes zero
+// vectors for the rest.
+// ---------------------------------------------------------------------------
+template <class C, int KIND, int AXIS>
+__global__ void __launch_bounds__(C::P, C::WAVES) detector_pass(PassArgs a) {
+  static_assert(KIND == kFwdLast || KIND == kBwdFirst, "detector-plane kinds only");
+  __shared__ float2 lds[C::LDS_ELEMS];
+  __shared__ float rsum[KIND == kFwdLast ? C::T * kMaxRegions : 1];
+  __shared__ int vmap[C::T];
+  constexpr int N1 = C::N1;
+  const Tile<C> t{lds, (int)(threadIdx.x % C::T), (int)(threadIdx.x / C::T)};
+  const int j = t.s;
+
+  const WorkItem wi = work_item(a.ntiles, (a.batch + a.spg - 1) / a.spg);
+  if (!wi.valid) return;
+  const int n = a.n;
+  const int off = a.off;
+  const size_t nn = (size_t)n * n;
+  const int b0 = wi.group * a.spg;
+  const int b1 = min(a.batch, b0 + a.spg);
+
+  // tile vectors: a run of the covered-first permutation, or consecutive vectors
+  int first;
+  int nvalid;
+  bool zero_tile = false;
+  if (a.vperm) {
+    if (wi.tile < a.ntiles_act) {
+      first = wi.tile * C::T;
+      nvalid = min(C::T, a.nact - first);
+    } else {
+      zero_tile = true;
+      first = a.nact + (wi.tile - a.ntiles_act) * C::T;
+      nvalid = min(C::T, n - first);
+    }
+  } else {
+    first = wi.tile * C::T;
+    nvalid = min(C::T, n - first);
+  }
+  if ((int)threadIdx.x < C::T) {
+    const int v = (int)threadIdx.x;
+    vmap[v] = v < nvalid ? (a.vperm ? a.vperm[first + v] : first + v) : 0;
+  }
+  const Mapped vf{vmap};
+  if (KIND == kBwdFirst && zero_tile) {
+    __syncthreads();
+    for (int b = b0; b < b1; ++b) zero_vectors<C, AXIS>(a.out + (size_t)b * nn, n, vf, nvalid);
+    return;
+  }
+  stage_table<C>(lds, a.tab);
+  __syncthreads();
+  const bool vok = t.v < nvalid;
+  const int vec = vmap[t.v];
+
+  for (int b = b0; b < b1; ++b) {
+    float2 x[N1];
+    __syncthreads();
+    load_tile<C, AXIS>(lds, static_cast<const float2*>(a.in) + (size_t)b * nn, false, n, off, vf, nvalid);
+    __syncthreads();
+    read_a(t, j, x);
+    // rest of the last hop: U_D
+    Dft<N1, -1>::run(x);
+    write_a(t, j, x);
+    __syncthreads();
+    b_spectral(t, false);
+    __syncthreads();
+    read_a(t, j, x);
+    Dft<N1, 1>::run(x);
+
+    if constexpr (KIND == kFwdLast) {
+      write_a(t, j, x);
+      __syncthreads();
+      tile_outputs<C, AXIS>(lds, rsum, a, b, vf, nvalid, wi.tile);
+    } else {
+      // seed G_D = 2 (dL/dI) U_D at this thread's positions (zero outside the aperture)
+      if (a.grad_int) {
+        float2 g[N1];
+        __syncthreads();  // every read of U_D from shared memory is done
+        load_tile<C, AXIS>(lds, a.grad_int + (size_t)b * nn, true, n, off, vf, nvalid);
+        __syncthreads();
+        read_a(t, j, g);
+        static_for<0, N1>([&](auto k) { x[k.value] = cscale(x[k.value], 2.f * g[k.value].x); });
+      } else {
+        // dL/dI is dL/dS_k on region k: sum over the regions covering the pixel
+        const float* __restrict__ gs = a.grad_sums + (size_t)b * a.K;
+        const unsigned long long vmask = vok ? ld(AXIS == kRow ? a.row_mask : a.col_mask, vec) : 0ull;
+        const unsigned long long* __restrict__ qmask = AXIS == kRow ? a.col_mask : a.row_mask;
+        for_a_elems<C>(off, n, 1, 0, vok, [&](auto k, int q, bool in) {
+          float gv = 0.f;
+          if (in && vmask) {
+            unsigned long long mk = vmask & ld(qmask, q);
+            while (mk) {
+              gv += gs[__builtin_ctzll(mk)];
+              mk &= mk - 1;
+            }
+          }
+          x[k.value] = cscale(x[k.value], 2.f * gv);
+        });
+      }
+      // adjoint of the half hop
+      Dft<N1, -1>::run(x);
+      write_a(t, j, x);
+      __syncthreads();
+      b_spectral(t, true);
+      __syncthreads();
+      read_a(t, j, x);
+      Dft<N1, 1>::run(x);
+      if constexpr (AXIS == kCol) {
+        store_a_direct<C>(a.out + (size_t)b * nn, n, n, off, vec, vok, x);
+      } else {
+        write_a(t, j, x);
+        __syncthreads();
+        store_tile<C, AXIS>(lds, a.out + (size_t)b * nn, n, off, vf, nvalid);
+      }
+    }
   }
 }
 
@@ -493,7 +637,9 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
                                             ? C::WAVES_ACC : C::WAVES)
     as_pass(PassArgs a) {
   __shared__ float2 lds[C::LDS_ELEMS];
-  __shared__ float red[C::P / 64];
+  // region partial sums of the detector-plane outputs (row kinds that end in positions)
+  __shared__ float rsum[(KIND == kAsRowLast || KIND == kAsRowBwdLast || KIND == kAsRowIfft)
+                            ? C::T * kMaxRegions : 1];
   using PL = typename C::Plan;
   constexpr int N = C::N;
   constexpr int N1 = C::N1;
@@ -589,8 +735,8 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
         load_seed<C, kRow>(lds, a, b, vec0, nvalid);
       } else {
         const size_t es = a.in_real ? sizeof(float) : sizeof(float2);
-        load_tile<C, kRow>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * es, a.in_real != 0, n, off, vec0,
-                           nvalid);
+        load_tile<C, kRow>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * es, a.in_real != 0, n, off,
+                           Consecutive{vec0}, nvalid);
       }
       __syncthreads();
       read_a(t, j, x);
@@ -607,9 +753,9 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
       write_a(t, j, x);  // positions, cropped on output
       __syncthreads();
       if constexpr (KIND == kAsRowIfft) {
-        store_tile<C, kRow>(lds, a.out + (size_t)b * nn, n, off, vec0, nvalid);
+        store_tile<C, kRow>(lds, a.out + (size_t)b * nn, n, off, Consecutive{vec0}, nvalid);
       } else {  // kAsRowLast
-        tile_outputs<C, kRow>(lds, red, a, b, vec0, nvalid, wi.tile);
+        tile_outputs<C, kRow>(lds, rsum, a, b, Consecutive{vec0}, nvalid, wi.tile);
       }
     }
   }
@@ -686,7 +832,11 @@ template <int N, int KIND, int AXIS>
 hipError_t launch_fr(const PassArgs& a, hipStream_t st) {
   using C = std::conditional_t<AXIS == kRow, RowCfgFor<N>, CfgFor<N>>;
   const dim3 grid(work_grid(a.ntiles, (a.batch + a.spg - 1) / a.spg));
-  hipLaunchKernelGGL((fresnel_pass<C, KIND, AXIS>), grid, dim3(C::P), 0, st, a);
+  if constexpr (KIND == kFwdLast || KIND == kBwdFirst) {
+    hipLaunchKernelGGL((detector_pass<C, KIND, AXIS>), grid, dim3(C::P), 0, st, a);
+  } else {
+    hipLaunchKernelGGL((fresnel_pass<C, KIND, AXIS>), grid, dim3(C::P), 0, st, a);
+  }
   return hipGetLastError();
 }
 

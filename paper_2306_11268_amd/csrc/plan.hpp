@@ -61,6 +61,25 @@ struct Plan2 {
     if (PFA) return ((p % N1) * U1 % N1) * N2 + (p % N2) * U2 % N2;
     return p;
   }
+  // Slot of natural position p advanced one position at a time, without
+  // divisions: under the Good-Thomas map the slot is (s1, s2) =
+  // ((p mod N1) * U1 mod N1, (p mod N2) * U2 mod N2), and p + 1 adds (U1, U2).
+  struct Walk {
+    int s1;
+    int s2;
+  };
+  LR_HD static Walk walk(int p) { return PFA ? Walk{(p % N1) * U1 % N1, (p % N2) * U2 % N2} : Walk{p, 0}; }
+  LR_HD static int walk_slot(const Walk& w) { return PFA ? w.s1 * N2 + w.s2 : w.s1; }
+  LR_HD static void walk_next(Walk& w) {
+    if (PFA) {
+      w.s1 += U1;
+      if (w.s1 >= N1) w.s1 -= N1;
+      w.s2 += U2;
+      if (w.s2 >= N2) w.s2 -= N2;
+    } else {
+      ++w.s1;
+    }
+  }
   // Frequency index of element k2 of B-item k1 and its inverse (slot of frequency f).
   LR_HD static int freq(int k1, int k2) {
     return PFA ? (k1 * E1 + k2 * E2) % N : k1 + N1 * k2;

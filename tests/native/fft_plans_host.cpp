@@ -122,6 +122,14 @@ static bool check_plan_type(std::mt19937& g) {
   for (int k1 = 0; k1 < PL::N1; ++k1) for (int j = 0; j < PL::N2; ++j) cb[PL::b_slot(k1, j)]++;
   bool cover = true;
   for (int p = 0; p < N; ++p) cover &= (ca[p] == 1 && cb[p] == 1 && cp[p] == 1);
+  // the incremental slot walk agrees with slot_of_pos from every start
+  for (int p0 = 0; p0 < N; p0 += 7) {
+    auto w = PL::walk(p0);
+    for (int p = p0; p < N; ++p) {
+      cover &= PL::walk_slot(w) == PL::slot_of_pos(p);
+      PL::walk_next(w);
+    }
+  }
   const bool pass = ef < 2e-6 && ei < 2e-6 && cover;
   std::printf("plan N=%d (%dx%d %s) fwd=%.3e inv=%.3e cover=%d %s\n", N, PL::N1, PL::N2,
               PL::PFA ? "pfa" : "ct", ef, ei, (int)cover, pass ? "ok" : "FAIL");

@@ -1,0 +1,153 @@
+"""Training-step paths of the separable (Fresnel) network against the oracle.
+
+The forward pass here asks for the detector sums only, as a training step
+does: the detector-plane pass then transforms just the rows (or columns)
+covered by detector regions, and the backward seed pass finishes the last
+hop itself from the saved half-hop field.  Tolerances as in
+test_gpu_parity.py: relative L2 1e-4 on sums and loss, 1e-3 on dL/dphi.
+"""
+
+import numpy as np
+import pytest
+
+import oracle.donn as od
+from paper_2306_11268_amd import workloads as wl
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+TOL_FIELD = 1e-4
+TOL_GRAD = 1e-3
+
+
+def rel(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    r = float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-300))
+    print(f"  rel-L2 {r:.3e} over {b.size} values")
+    return r
+
+
+@pytest.fixture(scope="module")
+def lrb():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2306_11268_amd import binding
+    binding.load()
+    return binding
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def odet(d):
+    return od.Detector(d.size, tuple(d.y0), tuple(d.x0))
+
+
+def sums_only_forward(lrb, w, batch, layers, det, gamma=1.0):
+    net = lrb.Network(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n, w.n_fft, layers, gamma,
+                      lrb.Detector(det.size, det.y0, det.x0))
+    amp = wl.amplitudes(w, batch)
+    phi = wl.phases(w)[:layers]
+    saved = net.new_saved(batch)
+    out = lrb.lr_donn_forward(net, dev(amp), dev(phi), saved=saved, sums=True)
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
+    ref = od.donn_forward(amp, phi, h, gamma, odet(det))
+    return net, phi, saved, out, ref, h
+
+
+# L odd: the detector-plane pass is a row pass; L even: a column pass
+@pytest.mark.parametrize("layers", [5, 2, 1])
+def test_cross_entropy_step_sums_only(lrb, layers):
+    w = wl.WORKLOADS[3]
+    b = 7
+    net, phi, saved, out, ref, h = sums_only_forward(lrb, w, b, layers, w.detector)
+    assert out.get("intensity") is None and out.get("field") is None
+    assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
+    labels = wl.labels(w, b)
+    grad, loss = lrb.lr_donn_backward(net, dev(phi), saved, sums=out["sums"], labels=dev(labels))
+    ref_loss, gs = od.softmax_cross_entropy(ref["sums"], labels)
+    ref_grad = od.donn_backward(ref, phi, h, 1.0, odet(w.detector), grad_sums=gs)
+    assert abs(float(loss) - ref_loss) / abs(ref_loss) < TOL_FIELD
+    assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+@pytest.mark.parametrize("layers", [1, 2])
+def test_full_map_backward_after_sums_only_forward(lrb, layers):
+    # the saved half-hop field serves any seed, also a full dL/dI map
+    w = wl.WORKLOADS[3]
+    b = 3
+    net, phi, saved, out, ref, h = sums_only_forward(lrb, w, b, layers, w.detector)
+    gi = np.random.default_rng(17).standard_normal((b, w.n, w.n)).astype(np.float32)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_intensity=dev(gi))
+    ref_grad = od.donn_backward(ref, phi, h, 1.0, grad_intensity=gi)
+    assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+@pytest.mark.parametrize("layers", [1, 2, 3])
+def test_overlapping_regions_at_the_edges(lrb, layers):
+    # overlapping regions, regions touching the plane border, one region inside another
+    w = wl.WORKLOADS[3]
+    det = wl.DetectorLayout(size=30, y0=(0, 15, 170, 100, 105), x0=(0, 20, 170, 0, 5))
+    b = 3
+    net, phi, saved, out, ref, h = sums_only_forward(lrb, w, b, layers, det, gamma=0.9)
+    assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
+    gs = np.random.default_rng(3).standard_normal((b, det.num)).astype(np.float32)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_sums=dev(gs))
+    ref_grad = od.donn_backward(ref, phi, h, 0.9, odet(det), grad_sums=gs)
+    assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+@pytest.mark.parametrize("layers", [2, 3])
+def test_padded_grid_sums_only(lrb, layers):
+    # n = 100 centred in a 128 grid: the pruned passes crop and pad as well
+    w = wl.Workload(91, "test", 532e-9, 36e-6, 0.2, od.FRESNEL, 100, 128, 3, 3, "train",
+                    wl.layout_grid(100, 4, 12), "sums", "uniform")
+    b = 3
+    net, phi, saved, out, ref, h = sums_only_forward(lrb, w, b, layers, w.detector)
+    assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
+    gs = np.random.default_rng(4).standard_normal((b, w.detector.num)).astype(np.float32)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_sums=dev(gs))
+    ref_grad = od.donn_backward(ref, phi, h, 1.0, odet(w.detector), grad_sums=gs)
+    assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+def test_single_region_single_row(lrb):
+    # a 1 x 1 region: one covered row and one covered column
+    w = wl.WORKLOADS[3]
+    det = wl.DetectorLayout(size=1, y0=(123,), x0=(45,))
+    for layers in (1, 2):
+        net, phi, saved, out, ref, h = sums_only_forward(lrb, w, 2, layers, det)
+        assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
+        gs = np.array([[1.0], [-0.5]], dtype=np.float32)
+        grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_sums=dev(gs))
+        ref_grad = od.donn_backward(ref, phi, h, 1.0, odet(det), grad_sums=gs)
+        assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+def test_training_step_at_full_size(lrb):
+    """The benchmarked step itself: 5 layers, 200 x 200, batch 500, sums-only
+    forward, cross-entropy, backward, in the benchmark's launch configuration,
+    compared with the oracle on the whole batch."""
+    w = wl.WORKLOADS[3]
+    b = w.batch
+    net, phi, saved, out, ref, h = sums_only_forward(lrb, w, b, w.layers, w.detector)
+    assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
+    labels = wl.labels(w, b)
+    grad, loss = lrb.lr_donn_backward(net, dev(phi), saved, sums=out["sums"], labels=dev(labels))
+    g1 = host(grad).copy()
+    ref_loss, gs = od.softmax_cross_entropy(ref["sums"], labels)
+    assert abs(float(loss) - ref_loss) / abs(ref_loss) < TOL_FIELD
+    ref_grad = od.donn_backward(ref, phi, h, 1.0, odet(w.detector), grad_sums=gs)
+    assert rel(g1, ref_grad) < TOL_GRAD
+    # bitwise repeatable, and invariant to a global phase of each mask
+    grad2, _ = lrb.lr_donn_backward(net, dev(phi), saved, sums=out["sums"], labels=dev(labels))
+    assert np.array_equal(g1, host(grad2))
+    s = g1.sum(axis=(1, 2))
+    assert np.all(np.abs(s) <= 1e-4 * np.abs(g1).sum(axis=(1, 2)))
