@@ -95,33 +95,96 @@ __device__ __forceinline__ void zero_padding(float2* lds, int n, int off) {
 }
 
 // ---------------------------------------------------------------------------
-// Batched tile walks.  A tile has nvalid vectors of n elements; thread tid
-// handles elements e = tid + i*P, i < N1 (N1 * P = T * N covers the tile).
-//   row tiles:    element e is (v, q) = divmod(e, n) of a contiguous block;
-//   column tiles: element e is (v, q) = (e mod T, e div T).
-// The walk runs in chunks of W elements: first(i, v, q) is called for the
-// whole chunk (issue loads), then second(i, v, q) (consume them).  Loads use
-// one chunk of N1 (every load of the thread in flight before the first wait);
-// stores, which do not wait, use smaller chunks.  Only valid elements are
-// visited.
+// Batched tile walks.  A tile has nvalid vectors of n elements (positions
+// q < n; shared-memory position q + off).  Each visited element is passed to
+// the callbacks as (i, v, q, li): i the compile-time buffer index inside the
+// current chunk, v the tile vector, q the position, li its shared-memory index.
+//
+//   row tiles (whole rows per wave):  wave w moves rows v = w, w + NW, ... and
+//     its lanes cover positions q = lane + 64*m, so every global access of a
+//     wave is one contiguous run of a row and the shared-memory index of each
+//     (lane, m) is a per-lane constant plus v;
+//   column tiles: thread tid handles elements e = tid + i*P, i < N1, with
+//     (v, q) = (e mod T, e div T): every access of a wave covers T consecutive
+//     columns of a few rows.
+//
+// The walk runs in chunks of at most W elements per thread: first() is
+// called for the whole chunk (issue loads), then second() (consume them).
+// Loads use one chunk (every load of the thread in flight before the first
+// wait); stores, which do not wait, use small chunks.  Only valid elements
+// are visited.  WalkShape<C, AXIS, W>::BUF is the buffer length a chunk needs.
 // ---------------------------------------------------------------------------
+template <class C>
+struct RowLanes {
+  static constexpr int NW = C::P / 64;                 // waves per workgroup
+  static constexpr bool OK = C::T % NW == 0;           // rows split evenly over the waves
+  static constexpr int RPW = OK ? C::T / NW : 1;       // rows per wave
+  static constexpr int NCH = (C::N + 63) / 64;         // 64-position runs per row
+};
+
+constexpr int kAll = 1 << 20;
+
+template <class C, int AXIS, int W>
+struct WalkShape {
+  static constexpr bool ROWS = AXIS == kRow && RowLanes<C>::OK;
+  static constexpr int NCH = RowLanes<C>::NCH;
+  static constexpr int RPW = RowLanes<C>::RPW;
+  // rows: chunks of whole rows; columns: chunks of W elements
+  static constexpr int RCH = ROWS ? (W / NCH < 1 ? 1 : (W / NCH > RPW ? RPW : W / NCH)) : 1;
+  static constexpr int CH = ROWS ? RCH * NCH : (W < C::N1 ? W : C::N1);
+  static constexpr int NCHUNK = ROWS ? (RPW + RCH - 1) / RCH : (C::N1 + CH - 1) / CH;
+  static constexpr int BUF = CH;
+};
+
 template <class C, int AXIS, int W, class F1, class F2>
-__device__ __forceinline__ void tile_walk2(int n, int nvalid, F1&& first, F2&& second) {
-  constexpr int NCH = (C::N1 + W - 1) / W;
-  if constexpr (AXIS == kRow) {
+__device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& first, F2&& second) {
+  using WS = WalkShape<C, AXIS, W>;
+  if constexpr (WS::ROWS) {
+    using RL = RowLanes<C>;
+    const int tid = opaque_tid();
+    const int lane = tid & 63;
+    const int wv = tid >> 6;
+    int lofs[RL::NCH];  // shared-memory index of position lane + 64*m in tile vector 0
+    static_for<0, RL::NCH>([&](auto m) {
+      const int q = lane + 64 * decltype(m)::value;
+      lofs[m.value] = q < n ? lds_index<C>(q + off, 0) : 0;
+    });
+    static_for<0, WS::NCHUNK>([&](auto c) {
+      auto visit = [&](auto& f) {
+        static_for<0, WS::RCH>([&](auto rr) {
+          constexpr int r = decltype(c)::value * WS::RCH + decltype(rr)::value;
+          if constexpr (r < RL::RPW) {
+            const int v = wv + RL::NW * r;
+            if (v < nvalid) {
+              static_for<0, RL::NCH>([&](auto m) {
+                const int q = lane + 64 * decltype(m)::value;
+                if (q < n) {
+                  f(std::integral_constant<int, decltype(rr)::value * RL::NCH + decltype(m)::value>{}, v, q,
+                    lofs[m.value] + v);
+                }
+              });
+            }
+          }
+        });
+      };
+      visit(first);
+      visit(second);
+    });
+  } else if constexpr (AXIS == kRow) {
+    // rows that do not split evenly over the waves: flat walk over the tile
     const int total = nvalid * n;
     const int dv = C::P / n;
     const int dq = C::P - dv * n;
-    static_for<0, NCH>([&](auto c) {
-      constexpr int e0 = decltype(c)::value * W * C::P;
+    static_for<0, WS::NCHUNK>([&](auto c) {
+      constexpr int e0 = decltype(c)::value * WS::CH * C::P;
       auto visit = [&](auto& f) {
         const int tid = opaque_tid();
         int v = (tid + e0) / n;
         int q = (tid + e0) - v * n;
-        static_for<0, W>([&](auto i) {
-          constexpr int ii = decltype(c)::value * W + decltype(i)::value;
+        static_for<0, WS::CH>([&](auto i) {
+          constexpr int ii = decltype(c)::value * WS::CH + decltype(i)::value;
           if constexpr (ii < C::N1) {
-            if (tid + ii * C::P < total) f(i, v, q);
+            if (tid + ii * C::P < total) f(i, v, q, lds_index<C>(q + off, v));
             q += dq;
             v += dv;
             if (q >= n) { q -= n; ++v; }
@@ -132,16 +195,16 @@ __device__ __forceinline__ void tile_walk2(int n, int nvalid, F1&& first, F2&& s
       visit(second);
     });
   } else {
-    static_for<0, NCH>([&](auto c) {
+    static_for<0, WS::NCHUNK>([&](auto c) {
       auto visit = [&](auto& f) {
         const int tid = opaque_tid();
-        static_for<0, W>([&](auto i) {
-          constexpr int ii = decltype(c)::value * W + decltype(i)::value;
+        static_for<0, WS::CH>([&](auto i) {
+          constexpr int ii = decltype(c)::value * WS::CH + decltype(i)::value;
           if constexpr (ii < C::N1) {
             const int e = tid + ii * C::P;
             const int q = e / C::T;
             const int v = e - q * C::T;
-            if (q < n && v < nvalid) f(i, v, q);
+            if (q < n && v < nvalid) f(i, v, q, lds_index<C>(q + off, v));
           }
         });
       };
@@ -159,17 +222,19 @@ template <class C, int AXIS, class VF>
 __device__ __forceinline__ void load_tile(float2* lds, const void* src, bool real, int n, int off, VF&& vf,
                                           int nvalid) {
   zero_padding<C>(lds, n, off);
-  float2 buf[C::N1];
+  constexpr int BUF = WalkShape<C, AXIS, kAll>::BUF;
   if (real) {
     const float* __restrict__ in = static_cast<const float*>(src);
-    tile_walk2<C, AXIS, C::N1>(n, nvalid,
-        [&](auto i, int v, int q) { buf[i.value] = c2(ld(in, nat_index<AXIS>(n, vf(v), q)), 0.f); },
-        [&](auto i, int v, int q) { lds[lds_index<C>(q + off, v)] = buf[i.value]; });
+    float buf[BUF];
+    tile_walk2<C, AXIS, kAll>(n, off, nvalid,
+        [&](auto i, int v, int q, int) { buf[i.value] = ld(in, nat_index<AXIS>(n, vf(v), q)); },
+        [&](auto i, int, int, int li) { lds[li] = c2(buf[i.value], 0.f); });
   } else {
     const float2* __restrict__ in = static_cast<const float2*>(src);
-    tile_walk2<C, AXIS, C::N1>(n, nvalid,
-        [&](auto i, int v, int q) { buf[i.value] = ld(in, nat_index<AXIS>(n, vf(v), q)); },
-        [&](auto i, int v, int q) { lds[lds_index<C>(q + off, v)] = buf[i.value]; });
+    float2 buf[BUF];
+    tile_walk2<C, AXIS, kAll>(n, off, nvalid,
+        [&](auto i, int v, int q, int) { buf[i.value] = ld(in, nat_index<AXIS>(n, vf(v), q)); },
+        [&](auto i, int, int, int li) { lds[li] = buf[i.value]; });
   }
 }
 
@@ -195,10 +260,11 @@ __device__ __forceinline__ void load_seed(float2* lds, const PassArgs& a, int b,
   const float2* __restrict__ ud = a.ud_in + (size_t)b * nn;
   const float* __restrict__ gint = a.grad_int ? a.grad_int + (size_t)b * nn : nullptr;
   const float* __restrict__ gsum = a.grad_sums ? a.grad_sums + (size_t)b * a.K : nullptr;
-  float2 buf[C::N1];
-  float g[C::N1];
-  tile_walk2<C, AXIS, C::N1>(n, nvalid,
-      [&](auto i, int v, int q) {
+  constexpr int BUF = WalkShape<C, AXIS, kAll>::BUF;
+  float2 buf[BUF];
+  float g[BUF];
+  tile_walk2<C, AXIS, kAll>(n, off, nvalid,
+      [&](auto i, int v, int q, int) {
         const int y = AXIS == kRow ? vec0 + v : q;
         const int x = AXIS == kRow ? q : vec0 + v;
         float gv = 0.f;
@@ -215,23 +281,23 @@ __device__ __forceinline__ void load_seed(float2* lds, const PassArgs& a, int b,
         g[i.value] = gv;
         buf[i.value] = gv != 0.f ? ld(ud, y * n + x) : c2(0.f, 0.f);
       },
-      [&](auto i, int v, int q) { lds[lds_index<C>(q + off, v)] = cscale(buf[i.value], 2.f * g[i.value]); });
+      [&](auto i, int, int, int li) { lds[li] = cscale(buf[i.value], 2.f * g[i.value]); });
 }
 
 template <class C, int AXIS, class VF>
 __device__ __forceinline__ void store_tile(const float2* lds, float2* __restrict__ out, int n, int off, VF&& vf,
                                            int nvalid) {
-  float2 buf[kStoreChunk];
-  tile_walk2<C, AXIS, kStoreChunk>(n, nvalid,
-      [&](auto i, int v, int q) { buf[i.value] = lds[lds_index<C>(q + off, v)]; },
-      [&](auto i, int v, int q) { st(out, nat_index<AXIS>(n, vf(v), q), buf[i.value]); });
+  float2 buf[WalkShape<C, AXIS, kStoreChunk>::BUF];
+  tile_walk2<C, AXIS, kStoreChunk>(n, off, nvalid,
+      [&](auto i, int, int, int li) { buf[i.value] = lds[li]; },
+      [&](auto i, int v, int q, int) { st(out, nat_index<AXIS>(n, vf(v), q), buf[i.value]); });
 }
 
 // Zero vectors vf(0..nvalid) of a natural-layout field.
 template <class C, int AXIS, class VF>
 __device__ __forceinline__ void zero_vectors(float2* __restrict__ out, int n, VF&& vf, int nvalid) {
-  tile_walk2<C, AXIS, kStoreChunk>(n, nvalid, [&](auto, int, int) {},
-      [&](auto, int v, int q) { st(out, nat_index<AXIS>(n, vf(v), q), c2(0.f, 0.f)); });
+  tile_walk2<C, AXIS, kStoreChunk>(n, 0, nvalid, [&](auto, int, int, int) {},
+      [&](auto, int v, int q, int) { st(out, nat_index<AXIS>(n, vf(v), q), c2(0.f, 0.f)); });
 }
 
 // Detector-plane outputs from a tile that holds U_D in natural order:
@@ -251,10 +317,10 @@ __device__ __forceinline__ void tile_outputs(const float2* lds, float* rsum, con
   float2* sv = a.saved_ud ? a.saved_ud + (size_t)b * nn : nullptr;
   float* io = a.intensity ? a.intensity + (size_t)b * nn : nullptr;
   if (fo || sv || io) {
-    float2 buf[kStoreChunk];
-    tile_walk2<C, AXIS, kStoreChunk>(n, nvalid,
-        [&](auto i, int v, int q) { buf[i.value] = lds[lds_index<C>(q + off, v)]; },
-        [&](auto i, int v, int q) {
+    float2 buf[WalkShape<C, AXIS, kStoreChunk>::BUF];
+    tile_walk2<C, AXIS, kStoreChunk>(n, off, nvalid,
+        [&](auto i, int, int, int li) { buf[i.value] = lds[li]; },
+        [&](auto i, int v, int q, int) {
           const int idx = nat_index<AXIS>(n, vf(v), q);
           if (fo) st(fo, idx, buf[i.value]);
           if (sv) st(sv, idx, buf[i.value]);
