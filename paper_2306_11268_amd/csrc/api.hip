@@ -3,6 +3,7 @@
 // entry point.  Every compute step runs in the HIP kernels of kernels.hip.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdio>
 #include <cstring>
@@ -16,6 +17,12 @@
 
 using lr::Axis;
 using lr::PassArgs;
+
+#define LR_TRY(x)                  \
+  do {                             \
+    const int _r = (x);            \
+    if (_r != LR_OK) return _r;    \
+  } while (0)
 
 namespace {
 
@@ -213,8 +220,32 @@ std::string as_name(int N, int kind) {
   return b;
 }
 
+// Schedule of a separable layer pass (PassArgs::workers / lanes).
+// Accumulating passes run persistently, as many workgroups as fit on the
+// device at once: each keeps one tile and takes a share of the batch for one
+// of `lanes` partial sums (lanes <= max_lanes, the partials the workspace
+// holds).  The other passes take one (tile, sample) item per workgroup.
+int schedule_layer_pass(int N, lr::PassKind kind, Axis ax, int max_lanes, PassArgs& a) {
+  const int slots = lr::fresnel_pass_slots(N, kind, ax);
+  if (slots <= 0) return LR_E_HIP;
+  if (kind == lr::kBwdMid || kind == lr::kBwdLast) {
+    int lanes = std::max(1, slots / std::max(1, a.ntiles));
+    lanes = std::min(lanes, std::max(1, std::min(max_lanes, a.batch)));
+    a.lanes = lanes;
+    a.workers = lanes * a.ntiles;
+  } else {
+    a.lanes = 0;  // one (tile, sample) item per workgroup
+    a.workers = a.ntiles * a.batch;
+  }
+  return LR_OK;
+}
+
+// Launch a separable pass; layer passes without accumulation are scheduled here,
+// accumulating ones by the caller (which needs the number of partials).
 int fr_pass(int N, lr::PassKind kind, Axis ax, const PassArgs& a, hipStream_t st) {
-  return run_timed(fr_name(N, kind, ax), st, [&] { return lr::launch_fresnel_pass(N, kind, ax, a, st); });
+  PassArgs s = a;
+  if (kind == lr::kPropOnce || kind == lr::kFwdMid) LR_TRY(schedule_layer_pass(N, kind, ax, 0, s));
+  return run_timed(fr_name(N, kind, ax), st, [&] { return lr::launch_fresnel_pass(N, kind, ax, s, st); });
 }
 int as_pass(int N, lr::AsPassKind kind, const PassArgs& a, hipStream_t st) {
   return run_timed(as_name(N, kind), st, [&] { return lr::launch_as_pass(N, kind, a, st); });
@@ -312,12 +343,6 @@ int prep_mod(const lr_donn* net, const float* d_phi, const Layout& L, void* w, h
     return lr::launch_prep_mod(d_phi, net->num_layers, net->n, net->gamma, orient, at<float2>(w, L.mod), st);
   });
 }
-
-#define LR_TRY(x)                  \
-  do {                             \
-    const int _r = (x);            \
-    if (_r != LR_OK) return _r;    \
-  } while (0)
 
 }  // namespace
 
@@ -637,9 +662,9 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
   a.conj_mod = 1;
   a.nvec = n;
   a.ntiles = L.ntiles_vec;
-  auto reduce = [&](int l) {
+  auto reduce = [&](int l, int groups) {
     return run_timed("reduce_dphi", st, [&] {
-      return lr::launch_reduce_dphi(part, L.groups, n, layer_transposed(net, l),
+      return lr::launch_reduce_dphi(part, groups, n, layer_transposed(net, l),
                                     d_grad_phi + static_cast<size_t>(l - 1) * nn, st);
     });
   };
@@ -671,14 +696,12 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
       m.mod = ws_mod + static_cast<size_t>(l - 1) * nn;
       m.act_in = saved + static_cast<size_t>(l - 1) * batch * nn;
       m.dphi_part = part;
-      if (l > 1) {
-        m.out = w[cur ^ 1];
-        LR_TRY(fr_pass(N, lr::kBwdMid, ax, m, st));
-        cur ^= 1;
-      } else {
-        LR_TRY(fr_pass(N, lr::kBwdLast, ax, m, st));
-      }
-      LR_TRY(reduce(l));
+      const lr::PassKind kind = l > 1 ? lr::kBwdMid : lr::kBwdLast;
+      LR_TRY(schedule_layer_pass(N, kind, ax, L.groups, m));
+      if (l > 1) m.out = w[cur ^ 1];
+      LR_TRY(fr_pass(N, kind, ax, m, st));
+      if (l > 1) cur ^= 1;
+      LR_TRY(reduce(l, m.lanes));
     }
     return LR_OK;
   }
@@ -716,7 +739,7 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
     } else {
       LR_TRY(as_pass(N, lr::kAsRowBwdLast, r, st));
     }
-    LR_TRY(reduce(l));
+    LR_TRY(reduce(l, L.groups));
   }
   return LR_OK;
 }

@@ -40,7 +40,15 @@ struct PassArgs {
   int batch;
   int nvec;       // vectors along the tile axis
   int spg;        // samples per workgroup (group size of the batch reduction)
-  int ntiles;     // tiles along the vector axis (grid.x)
+  int ntiles;     // tiles along the vector axis
+  // Persistent schedule of the separable layer passes (fresnel_pass): the
+  // first `workers` workgroup ranks work.  Without dphi accumulation, rank r
+  // takes the (tile, sample) items r, r + workers, ... (item i = tile
+  // i % ntiles of sample i / ntiles).  With it, rank r keeps tile r % ntiles
+  // and takes samples r / ntiles + k * lanes, accumulating dphi over them
+  // into partial r / ntiles (workers = lanes * ntiles).
+  int workers;
+  int lanes;
   // main field
   const void* in;
   int in_real;    // input is a real float amplitude
@@ -86,6 +94,8 @@ bool fft_size_supported(int N);
 TileShape tile_shape(int N, int axis);
 
 hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& a, hipStream_t st);
+// Workgroups of a separable pass kernel that fit on the current device at once.
+int fresnel_pass_slots(int N, PassKind kind, Axis axis);
 hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t st);
 
 // Small helper kernels.

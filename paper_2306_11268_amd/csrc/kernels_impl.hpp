@@ -19,6 +19,7 @@
 
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <type_traits>
 
 #include "kernels.hpp"
@@ -238,6 +239,39 @@ __device__ __forceinline__ void load_tile(float2* lds, const void* src, bool rea
   }
 }
 
+// Two-phase tile load for prefetching: issue the global loads of a tile into
+// registers, later write them into shared memory (with the padding zeroed).
+template <class C, int AXIS>
+using TileBuf = float2[WalkShape<C, AXIS, kAll>::BUF];
+
+template <class C, int AXIS, class VF>
+__device__ __forceinline__ void tile_issue(TileBuf<C, AXIS>& buf, const void* src, bool real, int n, VF&& vf,
+                                           int nvalid) {
+  if (real) {
+    const float* __restrict__ in = static_cast<const float*>(src);
+    tile_walk2<C, AXIS, kAll>(n, 0, nvalid,
+        [&](auto i, int v, int q, int) { buf[i.value].x = ld(in, nat_index<AXIS>(n, vf(v), q)); },
+        [](auto, int, int, int) {});
+  } else {
+    const float2* __restrict__ in = static_cast<const float2*>(src);
+    tile_walk2<C, AXIS, kAll>(n, 0, nvalid,
+        [&](auto i, int v, int q, int) { buf[i.value] = ld(in, nat_index<AXIS>(n, vf(v), q)); },
+        [](auto, int, int, int) {});
+  }
+}
+template <class C, int AXIS>
+__device__ __forceinline__ void tile_commit(float2* lds, const TileBuf<C, AXIS>& buf, bool real, int n, int off,
+                                            int nvalid) {
+  zero_padding<C>(lds, n, off);
+  if (real) {
+    tile_walk2<C, AXIS, kAll>(n, off, nvalid, [](auto, int, int, int) {},
+        [&](auto i, int, int, int li) { lds[li] = c2(buf[i.value].x, 0.f); });
+  } else {
+    tile_walk2<C, AXIS, kAll>(n, off, nvalid, [](auto, int, int, int) {},
+        [&](auto i, int, int, int li) { lds[li] = buf[i.value]; });
+  }
+}
+
 // Tile vector v is field vector vec0 + v.
 struct Consecutive {
   int vec0;
@@ -400,9 +434,23 @@ __device__ __forceinline__ void store_a_direct(float2* __restrict__ out, int pit
 
 // ---------------------------------------------------------------------------
 // Separable (Fresnel) passes through the layers.
+//
+// Schedule (PassArgs::workers / lanes): a workgroup walks a sequence of
+// (tile, sample) items; with prefetching it issues the global loads of the
+// next item's field while it still transforms the current one, into
+// registers whose previous contents are dead by then (the modulation, or the
+// current field after its first A-step).  The workgroup ranks are
+// XCD-contiguous, so the workgroups of one XCD work on neighbouring items at
+// the same time.
 // ---------------------------------------------------------------------------
+struct Cursor {
+  int tile;
+  int b;     // sample
+  int item;  // flat item index (without accumulation)
+};
+
 template <class C, int KIND, int AXIS>
-__global__ void __launch_bounds__(C::P, (KIND == kBwdMid || KIND == kBwdLast) ? C::WAVES_ACC : C::WAVES)
+__global__ void __launch_bounds__(C::P, C::WAVES_ACC)
     fresnel_pass(PassArgs a) {
   static_assert(KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid || KIND == kBwdLast,
                 "detector-plane kinds run in detector_pass");
@@ -411,21 +459,51 @@ __global__ void __launch_bounds__(C::P, (KIND == kBwdMid || KIND == kBwdLast) ? 
   constexpr bool ACC = (KIND == kBwdMid || KIND == kBwdLast);
   constexpr bool TWO = (KIND == kFwdMid || KIND == kBwdMid);
   constexpr bool DIRECT = AXIS == kCol;  // column tiles address their A-items in global memory
+  // Accumulating (backward) passes run persistently and prefetch the next
+  // item's field (column tiles: into registers that are free by then; row
+  // tiles, whose staging buffer is larger, load at the top).  The other kinds
+  // get one item per workgroup (workers = items): a finishing workgroup
+  // leaves its stores draining while a fresh one starts loading.
+  constexpr bool PREFETCH = DIRECT && ACC;
   const Tile<C> t{lds, (int)(threadIdx.x % C::T), (int)(threadIdx.x / C::T)};
   const int j = t.s;
 
-  const WorkItem wi = work_item(a.ntiles, (a.batch + a.spg - 1) / a.spg);
-  if (!wi.valid) return;
+  const int G = (int)gridDim.x;
+  const int l = (int)blockIdx.x;
+  const int rank = (l & 7) * (G >> 3) + (l >> 3);
+  if (rank >= a.workers) return;
   const int n = a.n;
   const int off = a.off;
   const size_t nn = (size_t)n * n;
-  const int vec0 = wi.tile * C::T;
-  const int vec = vec0 + t.v;
-  const int nvalid = min(C::T, a.nvec - vec0);
-  const bool vok = t.v < nvalid;
-  const int b0 = wi.group * a.spg;
-  const int b1 = min(a.batch, b0 + a.spg);
+  const int total = a.ntiles * a.batch;
   const bool conj_tab = a.conj_tab != 0;
+  const bool real = a.in_real != 0;
+
+  // item sequence of this workgroup
+  Cursor cur;
+  if constexpr (ACC) {
+    cur = Cursor{rank % a.ntiles, rank / a.ntiles, 0};
+  } else {
+    cur = Cursor{rank % a.ntiles, rank / a.ntiles, rank};
+  }
+  auto advance = [&](const Cursor& c) {
+    if constexpr (ACC) {
+      return Cursor{c.tile, c.b + a.lanes, 0};
+    } else {
+      const int it = c.item + a.workers;
+      return Cursor{it % a.ntiles, it / a.ntiles, it};
+    }
+  };
+  auto has = [&](const Cursor& c) {
+    if constexpr (ACC) {
+      return c.b < a.batch;
+    } else {
+      return c.item < total;
+    }
+  };
+  auto src = [&](int b) -> const char* {
+    return static_cast<const char*>(a.in) + (size_t)b * nn * (real ? sizeof(float) : sizeof(float2));
+  };
 
   float acc[ACC ? N1 : 1];
   if constexpr (ACC) {
@@ -433,20 +511,86 @@ __global__ void __launch_bounds__(C::P, (KIND == kBwdMid || KIND == kBwdLast) ? 
   }
   stage_table<C>(lds, a.tab);  // visible after the first barrier below
 
-  for (int b = b0; b < b1; ++b) {
+  int vec0 = cur.tile * C::T;
+  int vec = vec0 + t.v;
+  int nvalid = min(C::T, a.nvec - vec0);
+  bool vok = t.v < nvalid;
+
+  // Column tiles keep an item's output in registers and store it after the
+  // next item's first A-step: stores count in the same vector-memory counter
+  // as loads, so a store issued right before the wait for the prefetched
+  // field would make that wait cover its completion as well.
+  constexpr bool DEFER = PREFETCH && DIRECT && KIND != kBwdLast;
+  float2 xout[DEFER ? N1 : 1];
+  bool pending = false;
+  int pend_b = 0;
+  int pend_vec = 0;
+  bool pend_vok = false;
+  auto store_pending = [&]() {
+    if constexpr (DEFER) {
+      __builtin_amdgcn_sched_barrier(0);  // after the A-step, not hoisted above the wait for the field
+      if (pending) store_a_direct<C>(a.out + (size_t)pend_b * nn, n, n, off, pend_vec, pend_vok, xout);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+
+  // prefetched input of the current item
+  float2 xin[PREFETCH && DIRECT ? N1 : 1];
+  TileBuf<C, AXIS> buf;
+  bool live = has(cur);
+  if constexpr (PREFETCH) {
+    if (live) {
+      if constexpr (DIRECT) {
+        load_a_direct<C>(static_cast<const float2*>(a.in) + (size_t)cur.b * nn, n, n, off, vec, vok, xin);
+      } else {
+        tile_issue<C, AXIS>(buf, src(cur.b), real, n, Consecutive{vec0}, nvalid);
+      }
+    }
+  }
+
+  while (live) {
+    const Cursor nxt = advance(cur);
+    const bool more = has(nxt);
+    const int nvec0 = nxt.tile * C::T;
+    const int nvalid_n = min(C::T, a.nvec - nvec0);
+    // Issue the next item's loads, once its registers are free.  After the
+    // last item the current one is loaded again (unused), so the buffer is
+    // always overwritten and its previous contents are dead from the copy on.
+    auto prefetch = [&]() {
+      if constexpr (PREFETCH) {
+        __builtin_amdgcn_sched_barrier(0);
+        const int pb = more ? nxt.b : cur.b;
+        const int pv0 = more ? nvec0 : vec0;
+        const int pnv = more ? nvalid_n : nvalid;
+        if constexpr (DIRECT) {
+          load_a_direct<C>(static_cast<const float2*>(a.in) + (size_t)pb * nn, n, n, off, pv0 + t.v, t.v < pnv,
+                           xin);
+        } else {
+          tile_issue<C, AXIS>(buf, src(pb), real, n, Consecutive{pv0}, pnv);
+        }
+      }
+    };
+    const int b = cur.b;
+
     float2 x[N1];
-    __syncthreads();  // shared memory reuse across samples
-    if constexpr (DIRECT) {
+    __syncthreads();  // shared memory reuse across items
+    if constexpr (PREFETCH && DIRECT) {
+      static_for<0, N1>([&](auto k) { x[k.value] = xin[k.value]; });
+    } else if constexpr (PREFETCH) {
+      tile_commit<C, AXIS>(lds, buf, real, n, off, nvalid);
+      __syncthreads();
+      read_a(t, j, x);
+    } else if constexpr (DIRECT) {
       load_a_direct<C>(static_cast<const float2*>(a.in) + (size_t)b * nn, n, n, off, vec, vok, x);
     } else {
-      const size_t es = a.in_real ? sizeof(float) : sizeof(float2);
-      load_tile<C, AXIS>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * es, a.in_real != 0, n, off,
-                         Consecutive{vec0}, nvalid);
+      load_tile<C, AXIS>(lds, src(b), real, n, off, Consecutive{vec0}, nvalid);
       __syncthreads();
       read_a(t, j, x);
     }
     Dft<N1, -1>::run(x);
     write_a(t, j, x);
+    store_pending();  // after the A-step's shared-memory writes, which need the field loads
+    if constexpr (!TWO) prefetch();  // the field registers are free from here on
 
     // per-element layer data, loaded now so it arrives during the B-step:
     // modulation gamma*exp(j*phi_l) and (backward) the saved activation U_l
@@ -484,6 +628,7 @@ __global__ void __launch_bounds__(C::P, (KIND == kBwdMid || KIND == kBwdLast) ? 
           x[k.value] = cmulc(g, m[k.value]);
         });
       }
+      prefetch();  // the modulation (and activation) registers are free from here on
       Dft<N1, -1>::run(x);
       write_a(t, j, x);
       __syncthreads();
@@ -495,18 +640,33 @@ __global__ void __launch_bounds__(C::P, (KIND == kBwdMid || KIND == kBwdLast) ? 
 
     if constexpr (KIND == kBwdLast) {
       static_for<0, N1>([&](auto k) { acc[k.value] += ul[k.value].x * x[k.value].y - ul[k.value].y * x[k.value].x; });
-      continue;
-    }
-    if constexpr (DIRECT) {
+    } else if constexpr (DEFER) {
+      static_for<0, N1>([&](auto k) { xout[k.value] = x[k.value]; });
+      pending = true;
+      pend_b = b;
+      pend_vec = vec;
+      pend_vok = vok;
+    } else if constexpr (DIRECT) {
       store_a_direct<C>(a.out + (size_t)b * nn, n, n, off, vec, vok, x);
     } else {
       write_a(t, j, x);
       __syncthreads();
       store_tile<C, AXIS>(lds, a.out + (size_t)b * nn, n, off, Consecutive{vec0}, nvalid);
     }
+
+    live = more;
+    if (more) {
+      cur = nxt;
+      vec0 = nvec0;
+      vec = vec0 + t.v;
+      nvalid = nvalid_n;
+      vok = t.v < nvalid;
+    }
   }
+  store_pending();
   if constexpr (ACC) {
-    float* __restrict__ dp = a.dphi_part + (size_t)wi.group * nn;
+    // one partial per lane; a lane with no samples contributes zeros
+    float* __restrict__ dp = a.dphi_part + (size_t)(rank / a.ntiles) * nn;
     for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
       if (in) st(dp, idx, acc[k.value]);
     });
@@ -897,13 +1057,71 @@ using RowCfgFor = Cfg<typename RowPlanFor<N>::type, TileT<N>::T>;
 template <int N, int KIND, int AXIS>
 hipError_t launch_fr(const PassArgs& a, hipStream_t st) {
   using C = std::conditional_t<AXIS == kRow, RowCfgFor<N>, CfgFor<N>>;
-  const dim3 grid(work_grid(a.ntiles, (a.batch + a.spg - 1) / a.spg));
   if constexpr (KIND == kFwdLast || KIND == kBwdFirst) {
+    const dim3 grid(work_grid(a.ntiles, (a.batch + a.spg - 1) / a.spg));
     hipLaunchKernelGGL((detector_pass<C, KIND, AXIS>), grid, dim3(C::P), 0, st, a);
   } else {
+    if (a.workers < 1) return hipErrorInvalidValue;
+    const dim3 grid(8 * ((a.workers + 7) / 8));
     hipLaunchKernelGGL((fresnel_pass<C, KIND, AXIS>), grid, dim3(C::P), 0, st, a);
   }
   return hipGetLastError();
+}
+
+// Compute units of the current device (cached per device).
+inline int device_cus() {
+  static int cache[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  if (cache[dev] == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    cache[dev] = cus;
+  }
+  return cache[dev];
+}
+
+// Workgroups of a kernel resident per compute unit: the runtime's occupancy
+// figure, capped by shared memory counted in its allocation granules (512
+// bytes), which the occupancy query does not round to.
+inline int resident_per_cu(const void* kernel, int block) {
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, block, 0) != hipSuccess) return 0;
+  hipFuncAttributes at;
+  if (hipFuncGetAttributes(&at, kernel) != hipSuccess) return 0;
+  int dev = 0;
+  int lds_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&lds_cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) != hipSuccess)
+    return 0;
+  const size_t granule = 512;
+  const size_t lds = (at.sharedSizeBytes + granule - 1) / granule * granule;
+  if (lds > 0) nb = std::min(nb, static_cast<int>(static_cast<size_t>(lds_cu) / lds));
+  return nb;
+}
+
+template <int N, int KIND, int AXIS>
+int slots_fr() {
+  using C = std::conditional_t<AXIS == kRow, RowCfgFor<N>, CfgFor<N>>;
+  static int per_cu = 0;
+  if (per_cu == 0) per_cu = resident_per_cu(reinterpret_cast<const void*>(&fresnel_pass<C, KIND, AXIS>), C::P);
+  return per_cu * device_cus();
+}
+
+template <int N, int KIND>
+int slots_fr_axis(Axis axis) {
+  return axis == kRow ? slots_fr<N, KIND, kRow>() : slots_fr<N, KIND, kCol>();
+}
+
+template <int N>
+int slots_fr_n(PassKind kind, Axis axis) {
+  switch (kind) {
+    case kPropOnce: return slots_fr_axis<N, kPropOnce>(axis);
+    case kFwdMid: return slots_fr_axis<N, kFwdMid>(axis);
+    case kBwdMid: return slots_fr_axis<N, kBwdMid>(axis);
+    case kBwdLast: return slots_fr_axis<N, kBwdLast>(axis);
+    default: return 0;
+  }
 }
 
 template <int N, int KIND>
