@@ -38,6 +38,18 @@ __device__ __forceinline__ void st(T* base, unsigned idx, T v) {
   *reinterpret_cast<T*>(reinterpret_cast<char*>(base) + idx * (unsigned)sizeof(T)) = v;
 }
 
+// Streaming variants for data touched once per pass (saved activations):
+// non-temporal hints keep them from displacing reused lines in the caches.
+__device__ __forceinline__ float2 ld_stream(const float2* base, unsigned idx) {
+  const unsigned long long u = __builtin_nontemporal_load(
+      reinterpret_cast<const unsigned long long*>(reinterpret_cast<const char*>(base) + idx * 8u));
+  return __builtin_bit_cast(float2, u);
+}
+__device__ __forceinline__ void st_stream(float2* base, unsigned idx, float2 v) {
+  __builtin_nontemporal_store(__builtin_bit_cast(unsigned long long, v),
+                              reinterpret_cast<unsigned long long*>(reinterpret_cast<char*>(base) + idx * 8u));
+}
+
 // threadIdx.x behind an empty asm statement: values derived from it are not
 // hoisted out of the per-sample loop (which would keep dozens of index
 // registers alive through the whole kernel); they are recomputed next to
@@ -600,7 +612,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
       const float2* __restrict__ ai = ACC ? a.act_in + (size_t)b * nn : nullptr;
       for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
         if constexpr (TWO) m[k.value] = in ? ld(a.mod, idx) : c2(0.f, 0.f);
-        if constexpr (ACC) ul[k.value] = in ? ld(ai, idx) : c2(0.f, 0.f);
+        if constexpr (ACC) ul[k.value] = in ? ld_stream(ai, idx) : c2(0.f, 0.f);
       });
     }
     __syncthreads();
@@ -618,7 +630,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
         });
         if (ao) {
           for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
-            if (in) st(ao, idx, x[k.value]);
+            if (in) st_stream(ao, idx, x[k.value]);
           });
         }
       } else {
