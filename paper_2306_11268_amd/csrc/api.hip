@@ -227,7 +227,9 @@ std::string as_name(int N, int kind) {
 // holds).  The other passes take one (tile, sample) item per workgroup.
 int schedule_layer_pass(int N, lr::PassKind kind, Axis ax, int max_lanes, PassArgs& a) {
   const int slots = lr::fresnel_pass_slots(N, kind, ax);
-  if (slots <= 0) return LR_E_HIP;
+  const int tile_t = lr::fresnel_pass_tile(N, kind, ax);
+  if (slots <= 0 || tile_t <= 0) return LR_E_HIP;
+  a.ntiles = ceil_div(a.nvec, tile_t);
   if (kind == lr::kBwdMid || kind == lr::kBwdLast) {
     int lanes = std::max(1, slots / std::max(1, a.ntiles));
     lanes = std::min(lanes, std::max(1, std::min(max_lanes, a.batch)));

@@ -9,6 +9,7 @@ namespace lr {
 // Per-size entry points, defined in kern_size.hip (one object per size).
 template <int N> hipError_t launch_fr_n(PassKind, Axis, const PassArgs&, hipStream_t);
 template <int N> int slots_fr_n(PassKind, Axis);
+template <int N> int tile_fr_n(PassKind, Axis);
 template <int N> hipError_t launch_as_n(AsPassKind, const PassArgs&, hipStream_t);
 template <int N> hipError_t prep_chirps_n(const float2*, float2*, float2*, hipStream_t);
 template <int N> hipError_t prep_as_n(const float2*, float2*, hipStream_t);
@@ -226,6 +227,21 @@ hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& 
     case 1000: return launch_fr_n<1000>(kind, axis, a, st);
     case 1024: return launch_fr_n<1024>(kind, axis, a, st);
     default: return hipErrorInvalidValue;
+  }
+}
+
+int fresnel_pass_tile(int N, PassKind kind, Axis axis) {
+  switch (N) {
+    case 64: return tile_fr_n<64>(kind, axis);
+    case 100: return tile_fr_n<100>(kind, axis);
+    case 128: return tile_fr_n<128>(kind, axis);
+    case 200: return tile_fr_n<200>(kind, axis);
+    case 256: return tile_fr_n<256>(kind, axis);
+    case 400: return tile_fr_n<400>(kind, axis);
+    case 512: return tile_fr_n<512>(kind, axis);
+    case 1000: return tile_fr_n<1000>(kind, axis);
+    case 1024: return tile_fr_n<1024>(kind, axis);
+    default: return 0;
   }
 }
 

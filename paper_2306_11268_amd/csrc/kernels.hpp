@@ -94,8 +94,10 @@ bool fft_size_supported(int N);
 TileShape tile_shape(int N, int axis);
 
 hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& a, hipStream_t st);
-// Workgroups of a separable pass kernel that fit on the current device at once.
+// Workgroups of a separable pass kernel that fit on the current device at
+// once, and the vectors each of its workgroups transforms.
 int fresnel_pass_slots(int N, PassKind kind, Axis axis);
+int fresnel_pass_tile(int N, PassKind kind, Axis axis);
 hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t st);
 
 // Small helper kernels.

@@ -1066,13 +1066,28 @@ using CfgFor = Cfg<typename PlanFor<N>::type, TileT<N>::T>;
 template <int N>
 using RowCfgFor = Cfg<typename RowPlanFor<N>::type, TileT<N>::T>;
 
+// Vectors per workgroup of the separable layer passes, by kind and axis where
+// a measured sweep preferred another width than the size default (fields and
+// tables do not depend on it).
+template <int N, int KIND, int AXIS>
+struct LayerTile {
+  static constexpr int T = TileT<N>::T;
+};
+template <> struct LayerTile<200, kFwdMid, kCol> { static constexpr int T = 24; };
+template <> struct LayerTile<200, kBwdLast, kCol> { static constexpr int T = 24; };
+
+template <int N, int KIND, int AXIS>
+using LayerCfg = Cfg<std::conditional_t<AXIS == kRow, typename RowPlanFor<N>::type, typename PlanFor<N>::type>,
+                     LayerTile<N, KIND, AXIS>::T>;
+
 template <int N, int KIND, int AXIS>
 hipError_t launch_fr(const PassArgs& a, hipStream_t st) {
-  using C = std::conditional_t<AXIS == kRow, RowCfgFor<N>, CfgFor<N>>;
   if constexpr (KIND == kFwdLast || KIND == kBwdFirst) {
+    using C = std::conditional_t<AXIS == kRow, RowCfgFor<N>, CfgFor<N>>;
     const dim3 grid(work_grid(a.ntiles, (a.batch + a.spg - 1) / a.spg));
     hipLaunchKernelGGL((detector_pass<C, KIND, AXIS>), grid, dim3(C::P), 0, st, a);
   } else {
+    using C = LayerCfg<N, KIND, AXIS>;
     if (a.workers < 1) return hipErrorInvalidValue;
     const dim3 grid(8 * ((a.workers + 7) / 8));
     hipLaunchKernelGGL((fresnel_pass<C, KIND, AXIS>), grid, dim3(C::P), 0, st, a);
@@ -1114,7 +1129,7 @@ inline int resident_per_cu(const void* kernel, int block) {
 
 template <int N, int KIND, int AXIS>
 int slots_fr() {
-  using C = std::conditional_t<AXIS == kRow, RowCfgFor<N>, CfgFor<N>>;
+  using C = LayerCfg<N, KIND, AXIS>;
   static int per_cu = 0;
   if (per_cu == 0) per_cu = resident_per_cu(reinterpret_cast<const void*>(&fresnel_pass<C, KIND, AXIS>), C::P);
   return per_cu * device_cus();
@@ -1123,6 +1138,23 @@ int slots_fr() {
 template <int N, int KIND>
 int slots_fr_axis(Axis axis) {
   return axis == kRow ? slots_fr<N, KIND, kRow>() : slots_fr<N, KIND, kCol>();
+}
+
+template <int N, int KIND>
+int tile_fr_axis(Axis axis) {
+  return axis == kRow ? LayerTile<N, KIND, kRow>::T : LayerTile<N, KIND, kCol>::T;
+}
+
+// Vectors per workgroup of a separable pass.
+template <int N>
+int tile_fr_n(PassKind kind, Axis axis) {
+  switch (kind) {
+    case kPropOnce: return tile_fr_axis<N, kPropOnce>(axis);
+    case kFwdMid: return tile_fr_axis<N, kFwdMid>(axis);
+    case kBwdMid: return tile_fr_axis<N, kBwdMid>(axis);
+    case kBwdLast: return tile_fr_axis<N, kBwdLast>(axis);
+    default: return TileT<N>::T;  // detector-plane passes
+  }
 }
 
 template <int N>
