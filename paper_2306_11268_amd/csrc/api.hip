@@ -180,7 +180,8 @@ Layout make_layout(const lr_donn* net, int batch, int op) {
     if (spg > batch) spg = batch > 0 ? batch : 1;
     L.spg = spg;
     L.groups = batch > 0 ? ceil_div(batch, spg) : 1;
-    L.dphi_part = take(static_cast<size_t>(L.groups) * nn * 4);
+    // one set of partials per layer, reduced in a single launch at the end
+    L.dphi_part = take(static_cast<size_t>(net->num_layers) * L.groups * nn * 4);
   }
   L.total = off;
   return L;
@@ -275,17 +276,6 @@ lr::Regions host_regions(const lr_detector& d) {
   return r;
 }
 
-// Region corners go to the workspace once per call; the pass kernels read them there.
-int upload_regions(const lr_donn* net, const Layout& L, void* w, hipStream_t st) {
-  if (net->det.num == 0) return LR_OK;
-  const lr::Regions r = host_regions(net->det);
-  return run_timed("set_regions", st, [&] {
-    return lr::launch_set_regions(r, net->n, at<int2>(w, L.regions), at<unsigned long long>(w, L.row_mask),
-                                  at<unsigned long long>(w, L.col_mask), at<int>(w, L.row_perm),
-                                  at<int>(w, L.col_perm), st);
-  });
-}
-
 // Number of rows (axis = row) or columns covered by at least one detector
 // region: the same test the region kernel applies when it orders them first.
 int covered_vectors(const lr_detector& d, int n, Axis ax) {
@@ -327,22 +317,42 @@ int check_work(const lr_donn* net, int batch, int op, void* d_work, size_t work_
   return LR_OK;
 }
 
+// Transfer-function tables of the passes: the separable Fresnel chirps (in
+// natural frequency order; each pass stages them in its own plan order) or the
+// column-permuted copy of H the angular-spectrum passes read.
 int prep_tables(const lr_donn* net, const Layout& L, void* w, hipStream_t st) {
   const float2* H = reinterpret_cast<const float2*>(net->d_H);
   if (net->approx == LR_FRESNEL) {
-    return run_timed("prep_chirps", st, [&] {
-      return lr::launch_prep_chirps(net->n_fft, H, at<float2>(w, L.chirp_x), at<float2>(w, L.chirp_y), st);
+    return run_timed("prep_layers", st, [&] {
+      return lr::launch_prep_layers(nullptr, 0, net->n, 1.0f, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                    nullptr, nullptr, H, net->n_fft, at<float2>(w, L.chirp_x),
+                                    at<float2>(w, L.chirp_y), st);
     });
   }
   return run_timed("prep_as_table", st,
                    [&] { return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), st); });
 }
 
-int prep_mod(const lr_donn* net, const float* d_phi, const Layout& L, void* w, hipStream_t st) {
+// Per-call tables of a forward or backward pass in one launch: the modulation
+// of every layer, the Fresnel chirps, and (when the call reads detector
+// regions) the region tables; the angular-spectrum table takes its own launch.
+int prep_layers(const lr_donn* net, const float* d_phi, bool regions, const Layout& L, void* w, hipStream_t st) {
   int orient[LR_MAX_LAYERS];
   for (int l = 0; l < net->num_layers; ++l) orient[l] = layer_transposed(net, l + 1);
-  return run_timed("prep_mod", st, [&] {
-    return lr::launch_prep_mod(d_phi, net->num_layers, net->n, net->gamma, orient, at<float2>(w, L.mod), st);
+  const bool with_regions = regions && net->det.num > 0;
+  const lr::Regions r = host_regions(net->det);
+  const bool fresnel = net->approx == LR_FRESNEL;
+  const float2* H = reinterpret_cast<const float2*>(net->d_H);
+  if (!fresnel) {
+    LR_TRY(run_timed("prep_as_table", st,
+                     [&] { return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), st); }));
+  }
+  return run_timed("prep_layers", st, [&] {
+    return lr::launch_prep_layers(d_phi, net->num_layers, net->n, net->gamma, orient, at<float2>(w, L.mod),
+                                  with_regions ? &r : nullptr, at<int2>(w, L.regions),
+                                  at<unsigned long long>(w, L.row_mask), at<unsigned long long>(w, L.col_mask),
+                                  at<int>(w, L.row_perm), at<int>(w, L.col_perm), fresnel ? H : nullptr,
+                                  net->n_fft, at<float2>(w, L.chirp_x), at<float2>(w, L.chirp_y), st);
   });
 }
 
@@ -512,9 +522,7 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   float2* ws_mod = at<float2>(d_work, L.mod);
   float2* w[2] = {at<float2>(d_work, L.w0), at<float2>(d_work, L.w1)};
 
-  LR_TRY(prep_tables(net, L, d_work, st));
-  LR_TRY(prep_mod(net, d_phi, L, d_work, st));
-  if (d_sums) LR_TRY(upload_regions(net, L, d_work, st));
+  LR_TRY(prep_layers(net, d_phi, d_sums != nullptr, L, d_work, st));
 
   PassArgs a = base_args(net, batch);
   const int tile_t = lr::tile_shape(N, 0).T;
@@ -635,22 +643,16 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
   LR_TRY(check_work(net, batch, LR_OP_BACKWARD, d_work, work_bytes, &L));
   if (batch == 0) {
     // an empty batch has a zero gradient: a fixed-order sum over no groups
-    for (int l = 1; l <= Lyr; ++l) {
-      LR_TRY(run_timed("reduce_dphi", st, [&] {
-        return lr::launch_reduce_dphi(nullptr, 0, n, 0, d_grad_phi + static_cast<size_t>(l - 1) * nn, st);
-      }));
-    }
-    return LR_OK;
+    int none[LR_MAX_LAYERS] = {};
+    return run_timed("reduce_dphi", st,
+                     [&] { return lr::launch_reduce_dphi(nullptr, 0, none, none, Lyr, n, d_grad_phi, st); });
   }
   const float2* saved = static_cast<const float2*>(d_saved);
   float2* ws_mod = at<float2>(d_work, L.mod);
   float2* w[2] = {at<float2>(d_work, L.w0), at<float2>(d_work, L.w1)};
   float* part = at<float>(d_work, L.dphi_part);
 
-  LR_TRY(prep_tables(net, L, d_work, st));
-  LR_TRY(prep_mod(net, d_phi, L, d_work, st));
-
-  if (d_labels || d_grad_sums) LR_TRY(upload_regions(net, L, d_work, st));
+  LR_TRY(prep_layers(net, d_phi, d_labels || d_grad_sums, L, d_work, st));
   const float* gsum = d_grad_sums;
   if (d_labels) {
     float* g = at<float>(d_work, L.grad_sums);
@@ -664,10 +666,15 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
   a.conj_mod = 1;
   a.nvec = n;
   a.ntiles = L.ntiles_vec;
-  auto reduce = [&](int l, int groups) {
+  // layer l accumulates into its own partials; one launch reduces all layers at the end
+  const size_t layer_stride = static_cast<size_t>(L.groups) * nn;
+  auto part_of = [&](int l) { return part + static_cast<size_t>(l - 1) * layer_stride; };
+  int groups_of[LR_MAX_LAYERS] = {};
+  int orient_of[LR_MAX_LAYERS] = {};
+  for (int l = 1; l <= Lyr; ++l) orient_of[l - 1] = layer_transposed(net, l);
+  auto reduce_all = [&]() {
     return run_timed("reduce_dphi", st, [&] {
-      return lr::launch_reduce_dphi(part, groups, n, layer_transposed(net, l),
-                                    d_grad_phi + static_cast<size_t>(l - 1) * nn, st);
+      return lr::launch_reduce_dphi(part, layer_stride, groups_of, orient_of, Lyr, n, d_grad_phi, st);
     });
   };
 
@@ -697,15 +704,15 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
       m.tab = chirp(ax);
       m.mod = ws_mod + static_cast<size_t>(l - 1) * nn;
       m.act_in = saved + static_cast<size_t>(l - 1) * batch * nn;
-      m.dphi_part = part;
+      m.dphi_part = part_of(l);
       const lr::PassKind kind = l > 1 ? lr::kBwdMid : lr::kBwdLast;
       LR_TRY(schedule_layer_pass(N, kind, ax, L.groups, m));
       if (l > 1) m.out = w[cur ^ 1];
       LR_TRY(fr_pass(N, kind, ax, m, st));
       if (l > 1) cur ^= 1;
-      LR_TRY(reduce(l, m.lanes));
+      groups_of[l - 1] = m.lanes;
     }
-    return LR_OK;
+    return reduce_all();
   }
 
   // angular spectrum
@@ -733,7 +740,7 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
     r.in = w[cur];
     r.mod = ws_mod + static_cast<size_t>(l - 1) * nn;
     r.act_in = saved + static_cast<size_t>(l - 1) * batch * nn;
-    r.dphi_part = part;
+    r.dphi_part = part_of(l);
     if (l > 1) {
       r.out = w[cur ^ 1];
       LR_TRY(as_pass(N, lr::kAsRowBwdMid, r, st));
@@ -741,9 +748,9 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
     } else {
       LR_TRY(as_pass(N, lr::kAsRowBwdLast, r, st));
     }
-    LR_TRY(reduce(l, L.groups));
+    groups_of[l - 1] = L.groups;
   }
-  return LR_OK;
+  return reduce_all();
 }
 
 int lr_kernel_timing(int32_t enable) {

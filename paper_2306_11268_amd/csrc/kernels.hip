@@ -11,7 +11,6 @@ template <int N> hipError_t launch_fr_n(PassKind, Axis, const PassArgs&, hipStre
 template <int N> int slots_fr_n(PassKind, Axis);
 template <int N> int tile_fr_n(PassKind, Axis);
 template <int N> hipError_t launch_as_n(AsPassKind, const PassArgs&, hipStream_t);
-template <int N> hipError_t prep_chirps_n(const float2*, float2*, float2*, hipStream_t);
 template <int N> hipError_t prep_as_n(const float2*, float2*, hipStream_t);
 template <int N> TileShape shape_n();
 
@@ -22,8 +21,8 @@ template <int N> TileShape shape_n();
 struct OrientArg { int o[64]; };
 
 // mod[l][q][vec] = gamma * exp(j*phi_l[y][x]); (y, x) = (q, vec) or (vec, q) when transposed.
-__global__ void prep_mod_kernel(const float* __restrict__ phi, int layers, int n, float gamma, OrientArg orient,
-                                float2* __restrict__ mod) {
+__device__ __forceinline__ void prep_mod_body(const float* __restrict__ phi, int layers, int n, float gamma,
+                                              const OrientArg& orient, float2* __restrict__ mod) {
   const size_t nn = (size_t)n * n;
   const size_t total = nn * layers;
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
@@ -49,13 +48,13 @@ __global__ void finish_sums_kernel(const float* __restrict__ part, int batch, in
 }
 
 // Softmax cross-entropy over the detector sums, averaged over the batch.
-// One workgroup; sample b is handled by thread b % 256 in a fixed order.
-__global__ void __launch_bounds__(256) ce_loss_kernel(const float* __restrict__ sums, const int32_t* __restrict__ labels,
+// One workgroup; sample b is handled by thread b % 1024 in a fixed order.
+__global__ void __launch_bounds__(1024) ce_loss_kernel(const float* __restrict__ sums, const int32_t* __restrict__ labels,
                                                       int batch, int K, float* __restrict__ grad, float* __restrict__ loss) {
-  __shared__ float red[4];
+  __shared__ float red[16];
   float my = 0.f;
   const float invb = 1.0f / (float)batch;
-  for (int b = threadIdx.x; b < batch; b += 256) {
+  for (int b = threadIdx.x; b < batch; b += 1024) {
     const float* s = sums + (size_t)b * K;
     float mx = s[0];
     for (int k = 1; k < K; ++k) mx = fmaxf(mx, s[k]);
@@ -70,17 +69,26 @@ __global__ void __launch_bounds__(256) ce_loss_kernel(const float* __restrict__ 
     }
     my += valid ? (lz + mx - s[tl]) : __builtin_nanf("");
   }
-  const float tot = block_sum<256>(my, red);
+  const float tot = block_sum<1024>(my, red);
   if (threadIdx.x == 0 && loss) *loss = tot * invb;
 }
 
-// dphi[y][x] = sum over groups of part[g][q][vec], oriented (transposed: q = x).
-// A workgroup covers 64 consecutive elements with 4 slices of 64 threads;
-// slice s sums groups s, s+4, s+8, ... in order and the four partial sums are
-// added in slice order, so the result does not depend on scheduling.
-__global__ void __launch_bounds__(256) reduce_dphi_kernel(const float* __restrict__ part, int groups, int n,
-                                                          int transposed, float* __restrict__ out) {
+// dphi_l[y][x] = sum over groups of part_l[g][q][vec], oriented (transposed:
+// q = x), for every layer l = blockIdx.y in one launch; part_l starts at
+// part + l * layer_stride.  A workgroup covers 64 consecutive elements with 4
+// slices of 64 threads; slice s sums groups s, s+4, s+8, ... in order and the
+// four partial sums are added in slice order, so the result does not depend
+// on scheduling.  A layer with no groups gets zeros.
+struct ReduceArg {
+  int groups[64];
+  int transposed[64];
+};
+__global__ void __launch_bounds__(256) reduce_dphi_kernel(const float* __restrict__ part, size_t layer_stride,
+                                                          ReduceArg arg, int n, float* __restrict__ out) {
   __shared__ float red[4][64];
+  const int l = blockIdx.y;
+  const int groups = arg.groups[l];
+  const float* __restrict__ pl = part + (size_t)l * layer_stride;
   const size_t nn = (size_t)n * n;
   const int lane = threadIdx.x & 63;
   const int slice = threadIdx.x >> 6;
@@ -89,16 +97,16 @@ __global__ void __launch_bounds__(256) reduce_dphi_kernel(const float* __restric
   if (i < nn) {
     int g = slice;
     for (; g + 12 < groups; g += 16) {
-      const float a0 = part[(size_t)g * nn + i];
-      const float a1 = part[(size_t)(g + 4) * nn + i];
-      const float a2 = part[(size_t)(g + 8) * nn + i];
-      const float a3 = part[(size_t)(g + 12) * nn + i];
+      const float a0 = pl[(size_t)g * nn + i];
+      const float a1 = pl[(size_t)(g + 4) * nn + i];
+      const float a2 = pl[(size_t)(g + 8) * nn + i];
+      const float a3 = pl[(size_t)(g + 12) * nn + i];
       s += a0;
       s += a1;
       s += a2;
       s += a3;
     }
-    for (; g < groups; g += 4) s += part[(size_t)g * nn + i];
+    for (; g < groups; g += 4) s += pl[(size_t)g * nn + i];
   }
   red[slice][lane] = s;
   __syncthreads();
@@ -106,19 +114,16 @@ __global__ void __launch_bounds__(256) reduce_dphi_kernel(const float* __restric
     const float r = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
     const int q = (int)(i / n);
     const int v = (int)(i - (size_t)q * n);
-    out[transposed ? (size_t)v * n + q : i] = r;
+    out[(size_t)l * nn + (arg.transposed[l] ? (size_t)v * n + q : i)] = r;
   }
 }
 
 // Region corners, per-row / per-column coverage masks and the covered-first
 // permutations of rows and columns: covered indices in ascending order, then
-// the uncovered ones.  One workgroup of 1024 threads, thread i handles row i
-// and column i (n <= 1024).
-__global__ void __launch_bounds__(1024) set_regions_kernel(Regions reg, int n, int2* dst,
-                                                           unsigned long long* row_mask,
-                                                           unsigned long long* col_mask, int* row_perm,
-                                                           int* col_perm) {
-  __shared__ int wave_count[2][16];
+// the uncovered ones.  Run by one workgroup of 1024 threads, thread i handles
+// row i and column i (n <= 1024).
+__device__ void set_regions_body(const Regions& reg, int n, int2* dst, unsigned long long* row_mask,
+                                 unsigned long long* col_mask, int* row_perm, int* col_perm, int (*wave_count)[16]) {
   const int i = threadIdx.x;
   if (i < reg.K) dst[i] = make_int2(reg.y0[i], reg.x0[i]);
   unsigned long long rm = 0, cm = 0;
@@ -156,6 +161,35 @@ __global__ void __launch_bounds__(1024) set_regions_kernel(Regions reg, int n, i
     row_perm[rc ? r_rank : r_total + (i - r_rank)] = i;
     col_perm[cc ? c_rank : c_total + (i - c_rank)] = i;
   }
+}
+
+// Separable Fresnel chirps in natural frequency order from the 2-D table H
+// (N x N): x chirp H[0][f], y chirp H[f][0] * conj(H[0][0]) (so the two
+// carry exp(jkz) once), each with the 1/N of the inverse DFT folded in.
+__device__ __forceinline__ void prep_chirps_body(const float2* __restrict__ H, int N, float2* __restrict__ cx,
+                                                 float2* __restrict__ cy) {
+  const float inv = 1.0f / (float)N;
+  const float2 h00c = c2(H[0].x, -H[0].y);
+  for (int f = blockIdx.x * blockDim.x + threadIdx.x; f < N; f += gridDim.x * blockDim.x) {
+    cx[f] = cscale(H[f], inv);
+    cy[f] = cscale(cmul(H[(size_t)f * N], h00c), inv);
+  }
+}
+
+// Per-call tables in one launch: the modulation of every layer (all
+// workgroups), the separable chirps when H is given, and, when the call reads
+// detector regions, the region tables (workgroup 0).  Workgroups of 1024
+// threads.
+__global__ void __launch_bounds__(1024) prep_layers_kernel(const float* __restrict__ phi, int layers, int n, float gamma,
+                                                           OrientArg orient, float2* __restrict__ mod, Regions reg,
+                                                           int2* dst, unsigned long long* row_mask,
+                                                           unsigned long long* col_mask, int* row_perm, int* col_perm,
+                                                           const float2* __restrict__ H, int nfft,
+                                                           float2* __restrict__ cx, float2* __restrict__ cy) {
+  __shared__ int wave_count[2][16];
+  if (blockIdx.x == 0 && dst) set_regions_body(reg, n, dst, row_mask, col_mask, row_perm, col_perm, wave_count);
+  if (H) prep_chirps_body(H, nfft, cx, cy);
+  if (phi) prep_mod_body(phi, layers, n, gamma, orient, mod);
 }
 
 // Detector readout from a field: one workgroup per (sample, region).
@@ -275,20 +309,6 @@ hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t
   }
 }
 
-hipError_t launch_prep_chirps(int N, const float2* H, float2* cx, float2* cy, hipStream_t st) {
-  switch (N) {
-    case 64: return prep_chirps_n<64>(H, cx, cy, st);
-    case 100: return prep_chirps_n<100>(H, cx, cy, st);
-    case 128: return prep_chirps_n<128>(H, cx, cy, st);
-    case 200: return prep_chirps_n<200>(H, cx, cy, st);
-    case 256: return prep_chirps_n<256>(H, cx, cy, st);
-    case 400: return prep_chirps_n<400>(H, cx, cy, st);
-    case 512: return prep_chirps_n<512>(H, cx, cy, st);
-    case 1000: return prep_chirps_n<1000>(H, cx, cy, st);
-    case 1024: return prep_chirps_n<1024>(H, cx, cy, st);
-    default: return hipErrorInvalidValue;
-  }
-}
 
 hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, hipStream_t st) {
   switch (N) {
@@ -305,14 +325,24 @@ hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, hipStream_t 
   }
 }
 
-hipError_t launch_prep_mod(const float* phi, int layers, int n, float gamma, const int* orient_host, float2* mod,
-                           hipStream_t st) {
+hipError_t launch_prep_layers(const float* phi, int layers, int n, float gamma, const int* orient_host, float2* mod,
+                              const Regions* regions, int2* dst, unsigned long long* row_mask,
+                              unsigned long long* col_mask, int* row_perm, int* col_perm, const float2* H, int nfft,
+                              float2* chirp_x, float2* chirp_y, hipStream_t st) {
+  if (n < 1 || n > 1024 || layers < 0 || layers > 64 || (H && (nfft < n || !chirp_x || !chirp_y)))
+    return hipErrorInvalidValue;
+  if (regions && (regions->K < 1 || regions->K > kMaxRegions)) return hipErrorInvalidValue;
   OrientArg o{};
-  for (int l = 0; l < layers && l < 64; ++l) o.o[l] = orient_host[l];
+  for (int l = 0; l < layers; ++l) o.o[l] = orient_host[l];
+  Regions r{};
+  if (regions) r = *regions;
   const size_t total = (size_t)n * n * layers;
-  int blocks = (int)((total + 255) / 256);
-  if (blocks > 8192) blocks = 8192;
-  hipLaunchKernelGGL(prep_mod_kernel, dim3(blocks), dim3(256), 0, st, phi, layers, n, gamma, o, mod);
+  int blocks = (int)((total + 1023) / 1024);
+  if (blocks > 2048) blocks = 2048;
+  if (blocks < 1) blocks = 1;
+  hipLaunchKernelGGL(prep_layers_kernel, dim3(blocks), dim3(1024), 0, st, layers > 0 ? phi : nullptr, layers, n,
+                     gamma, o, mod, r, regions ? dst : nullptr, row_mask, col_mask, row_perm, col_perm, H, nfft,
+                     chirp_x, chirp_y);
   return hipGetLastError();
 }
 
@@ -324,24 +354,24 @@ hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, f
 
 hipError_t launch_ce_loss(const float* sums, const int32_t* labels, int batch, int K, float* grad, float* loss,
                           hipStream_t st) {
-  hipLaunchKernelGGL(ce_loss_kernel, dim3(1), dim3(256), 0, st, sums, labels, batch, K, grad, loss);
+  hipLaunchKernelGGL(ce_loss_kernel, dim3(1), dim3(1024), 0, st, sums, labels, batch, K, grad, loss);
   return hipGetLastError();
 }
 
-hipError_t launch_reduce_dphi(const float* part, int groups, int n, int transposed, float* out, hipStream_t st) {
+hipError_t launch_reduce_dphi(const float* part, size_t layer_stride, const int* groups, const int* transposed,
+                              int layers, int n, float* out, hipStream_t st) {
+  if (layers < 1 || layers > 64) return hipErrorInvalidValue;
+  ReduceArg arg{};
+  for (int l = 0; l < layers; ++l) {
+    arg.groups[l] = groups[l];
+    arg.transposed[l] = transposed[l];
+  }
   const size_t nn = (size_t)n * n;
   const int blocks = (int)((nn + 63) / 64);
-  hipLaunchKernelGGL(reduce_dphi_kernel, dim3(blocks), dim3(256), 0, st, part, groups, n, transposed, out);
+  hipLaunchKernelGGL(reduce_dphi_kernel, dim3(blocks, layers), dim3(256), 0, st, part, layer_stride, arg, n, out);
   return hipGetLastError();
 }
 
-hipError_t launch_set_regions(const Regions& r, int n, int2* dst, unsigned long long* row_mask,
-                              unsigned long long* col_mask, int* row_perm, int* col_perm, hipStream_t st) {
-  if (n < 1 || n > 1024 || r.K < 0 || r.K > kMaxRegions) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(set_regions_kernel, dim3(1), dim3(1024), 0, st, r, n, dst, row_mask, col_mask, row_perm,
-                     col_perm);
-  return hipGetLastError();
-}
 
 hipError_t launch_readout(const float2* field, int batch, int n, const Regions& r, float* sums, hipStream_t st) {
   hipLaunchKernelGGL(readout_kernel, dim3(r.K, batch), dim3(256), 0, st, field, n, r, sums);

@@ -90,6 +90,15 @@ struct PassArgs {
 
 struct TileShape { int T; int S; };
 
+// Detector regions passed by value: K squares of side s with corners (y0, x0).
+struct Regions {
+  int K;
+  int s;
+  int y0[kMaxRegions];
+  int x0[kMaxRegions];
+};
+
+
 bool fft_size_supported(int N);
 TileShape tile_shape(int N, int axis);
 
@@ -101,25 +110,26 @@ int fresnel_pass_tile(int N, PassKind kind, Axis axis);
 hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t st);
 
 // Small helper kernels.
-hipError_t launch_prep_chirps(int N, const float2* H, float2* chirp_row, float2* chirp_col, hipStream_t st);
 hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, hipStream_t st);
-hipError_t launch_prep_mod(const float* phi, int layers, int n, float gamma, const int* orient_host,
-                           float2* mod, hipStream_t st);
 hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, float* sums, hipStream_t st);
 hipError_t launch_ce_loss(const float* sums, const int32_t* labels, int batch, int K, float* grad_sums,
                           float* loss, hipStream_t st);
-hipError_t launch_reduce_dphi(const float* part, int groups, int n, int transposed, float* out, hipStream_t st);
-struct Regions {
-  int K;
-  int s;
-  int y0[kMaxRegions];
-  int x0[kMaxRegions];
-};
-// Region corners (int2 [K]), per-row / per-column coverage masks (uint64 [n])
-// and the covered-first permutations of rows and of columns (int [n] each)
-// in device memory.  n <= 1024.
-hipError_t launch_set_regions(const Regions& r, int n, int2* dst, unsigned long long* row_mask,
-                              unsigned long long* col_mask, int* row_perm, int* col_perm, hipStream_t st);
+// dphi of `layers` layers in one launch: layer l sums groups[l] partials
+// (oriented [q][vec], transposed[l] != 0: q = x) starting at
+// part + l * layer_stride floats into out + l * n * n.
+hipError_t launch_reduce_dphi(const float* part, size_t layer_stride, const int* groups, const int* transposed,
+                              int layers, int n, float* out, hipStream_t st);
+// Per-call tables in one launch: mod[l] = gamma * exp(j*phi_l) oriented per
+// layer (orient_host[l] != 0: transposed; none when layers = 0); when regions
+// is not NULL, the region corners (int2 [K]), per-row / per-column coverage
+// masks (uint64 [n]) and covered-first permutations of rows and columns
+// (int [n]); when H is not NULL, the separable Fresnel chirps of the nfft grid
+// in natural frequency order (chirp_x[f] = H[0][f] / nfft, chirp_y[f] =
+// H[f][0] * conj(H[0][0]) / nfft).  n <= 1024.
+hipError_t launch_prep_layers(const float* phi, int layers, int n, float gamma, const int* orient_host, float2* mod,
+                              const Regions* regions, int2* dst, unsigned long long* row_mask,
+                              unsigned long long* col_mask, int* row_perm, int* col_perm, const float2* H, int nfft,
+                              float2* chirp_x, float2* chirp_y, hipStream_t st);
 hipError_t launch_readout(const float2* field, int batch, int n, const Regions& r, float* sums, hipStream_t st);
 
 }  // namespace lr

@@ -521,7 +521,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
   if constexpr (ACC) {
     static_for<0, N1>([&](auto k) { acc[k.value] = 0.f; });
   }
-  stage_table<C>(lds, a.tab);  // visible after the first barrier below
+  stage_table_by_freq<C>(lds, a.tab);  // visible after the first barrier below
 
   int vec0 = cur.tile * C::T;
   int vec = vec0 + t.v;
@@ -742,7 +742,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES) detector_pass(PassArgs a) {
     for (int b = b0; b < b1; ++b) zero_vectors<C, AXIS>(a.out + (size_t)b * nn, n, vf, nvalid);
     return;
   }
-  stage_table<C>(lds, a.tab);
+  stage_table_by_freq<C>(lds, a.tab);
   __syncthreads();
   const bool vok = t.v < nvalid;
   const int vec = vmap[t.v];
@@ -1009,23 +1009,6 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
 // Helper kernels
 // ---------------------------------------------------------------------------
 
-// Separable chirps from the 2-D Fresnel table: row (x) chirp H[0][k] and
-// column (y) chirp H[k][0]*conj(H[0][0]) (so their product carries exp(jkz)
-// once), with the 1/N of each inverse DFT folded in, each stored B-item major
-// in the plan of the passes that use it.
-template <class PLR, class PLC>
-__global__ void prep_chirps_kernel(const float2* __restrict__ H, float2* __restrict__ cx, float2* __restrict__ cy) {
-  constexpr int N = PLR::N;
-  const float2 h00c = cconj(H[0]);
-  const float inv = 1.0f / (float)N;
-  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < N; i += gridDim.x * blockDim.x) {
-    const int k1 = i / PLR::N2;
-    const int k2 = i - k1 * PLR::N2;
-    cx[i] = cscale(H[PLR::freq(k1, k2)], inv);
-    cy[i] = cscale(cmul(H[(size_t)PLC::freq(k1, k2) * N], h00c), inv);
-  }
-}
-
 // Column-permuted 2-D table for the angular-spectrum column pass:
 // Hp[ky][c] = H[ky][kx(c)] / N^2, c the slot of frequency kx in the row plan
 // (the layout in which row passes store x-spectra).
@@ -1207,13 +1190,6 @@ hipError_t launch_as_n(AsPassKind kind, const PassArgs& a, hipStream_t st) {
     case kAsRowIfft: return launch_as<N, kAsRowIfft>(a, st);
   }
   return hipErrorInvalidValue;
-}
-
-template <int N>
-hipError_t prep_chirps_n(const float2* H, float2* cx, float2* cy, hipStream_t st) {
-  hipLaunchKernelGGL((prep_chirps_kernel<typename RowPlanFor<N>::type, typename PlanFor<N>::type>), dim3((N + 255) / 256),
-                     dim3(256), 0, st, H, cx, cy);
-  return hipGetLastError();
 }
 
 template <int N>

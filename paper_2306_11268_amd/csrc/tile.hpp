@@ -98,6 +98,18 @@ __device__ __forceinline__ void stage_table(float2* lds, const float2* __restric
   for (int i = threadIdx.x; i < C::N; i += C::P) lds[i * C::TP + C::T] = tab[i];
 }
 
+// Stage a per-frequency table given in natural frequency order (entry f for
+// frequency index f) in the plan's B-item order: entry i of the padding
+// column is frequency freq(i / N2, i % N2).
+template <class C>
+__device__ __forceinline__ void stage_table_by_freq(float2* lds, const float2* __restrict__ tab) {
+  using PL = typename C::Plan;
+  for (int i = threadIdx.x; i < C::N; i += C::P) {
+    const int k1 = i / C::N2;
+    lds[i * C::TP + C::T] = tab[PL::freq(k1, i - k1 * C::N2)];
+  }
+}
+
 // B-step "forward, multiply by the staged per-frequency table, inverse" used
 // by every propagation; conj selects conj(table).  The items of a thread are
 // unrolled so their shared-memory reads overlap.
