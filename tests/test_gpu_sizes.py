@@ -1,0 +1,95 @@
+"""Every supported FFT size on the GPU against the oracle.
+
+One hop (Fresnel and angular spectrum, forward and adjoint, unpadded and
+padded with ragged tiles) at every n_fft the library accepts, and a small
+training step (sums-only forward, upstream dL/dS, backward) at every size up
+to 512 with the detector-plane pass both along rows (L = 1) and columns
+(L = 2).  Tolerances: relative L2 1e-4 on fields and sums, 1e-3 on dL/dphi.
+"""
+
+import numpy as np
+import pytest
+
+import oracle.donn as od
+from paper_2306_11268_amd import workloads as wl
+
+torch = pytest.importorskip("torch")
+
+pytestmark = pytest.mark.gpu
+
+TOL_FIELD = 1e-4
+TOL_GRAD = 1e-3
+SIZES = (64, 100, 128, 200, 256, 400, 512, 1000, 1024)
+
+
+def rel(a, b):
+    a = np.asarray(a, dtype=np.complex128)
+    b = np.asarray(b, dtype=np.complex128)
+    r = float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-300))
+    print(f"  rel-L2 {r:.3e} over {b.size} values")
+    return r
+
+
+@pytest.fixture(scope="module")
+def lrb():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2306_11268_amd import binding
+    binding.load()
+    return binding
+
+
+def dev(x):
+    return torch.from_numpy(np.ascontiguousarray(x)).cuda()
+
+
+def host(t):
+    return t.detach().cpu().numpy()
+
+
+def crand(seed, shape):
+    g = np.random.default_rng(seed)
+    return (g.standard_normal(shape) + 1j * g.standard_normal(shape)).astype(np.complex64)
+
+
+def padded(m):
+    # an aperture smaller than the grid by an even margin, not a multiple of the tile widths
+    return m - 2 * max(1, m // 10 + 1)
+
+
+@pytest.mark.parametrize("m", SIZES)
+@pytest.mark.parametrize("approx", [od.FRESNEL, od.ANGULAR_SPECTRUM])
+@pytest.mark.parametrize("pad", [False, True])
+def test_one_hop_every_size(lrb, m, approx, pad):
+    n = padded(m) if pad else m
+    lam, dx, z = (532e-9, 36e-6, 0.3) if approx == od.FRESNEL else (1550e-9, 8e-6, 0.05)
+    b = 2 if m <= 512 else 1
+    u = crand(m + n + approx, (b, n, n))
+    net = lrb.Network(lam, dx, z, approx, n, m, 1)
+    h = od.transfer_function(lam, dx, z, approx, m)
+    for adjoint in (False, True):
+        out = host(lrb.lr_propagate(net, dev(u), adjoint=adjoint))
+        ref = od.propagate(u.astype(np.complex128), h, adjoint=adjoint)
+        assert rel(out, ref) < TOL_FIELD
+
+
+@pytest.mark.parametrize("m", [s for s in SIZES if s <= 512])
+@pytest.mark.parametrize("layers", [1, 2])
+def test_training_step_every_size(lrb, m, layers):
+    n = m if m % 128 else padded(m)  # pad the power-of-two grids, keep the others full
+    det = wl.layout_grid(n, 4, max(2, n // 10))
+    w = wl.Workload(92, "test", 532e-9, 36e-6, 0.3, od.FRESNEL, n, m, layers, 2, "train", det, "sums", "uniform")
+    net = lrb.Network(w.wavelength, w.pixel_pitch, w.distance, w.approx, n, m, layers, 0.95,
+                      lrb.Detector(det.size, det.y0, det.x0))
+    amp = wl.amplitudes(w, 2)
+    phi = wl.phases(w)
+    saved = net.new_saved(2)
+    out = lrb.lr_donn_forward(net, dev(amp), dev(phi), saved=saved, sums=True)
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, m)
+    odet = od.Detector(det.size, tuple(det.y0), tuple(det.x0))
+    ref = od.donn_forward(amp, phi, h, 0.95, odet)
+    assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
+    gs = np.random.default_rng(m + layers).standard_normal((2, det.num)).astype(np.float32)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_sums=dev(gs))
+    ref_grad = od.donn_backward(ref, phi, h, 0.95, odet, grad_sums=gs)
+    assert rel(host(grad), ref_grad) < TOL_GRAD
