@@ -282,3 +282,26 @@ def donn_backward(fwd: dict, phi: np.ndarray, h: np.ndarray, gamma: float = 1.0,
         if layer > 0:
             g = propagate(g, h, adjoint=True)
     return dphi
+
+
+# ---------------------------------------------------------------------------
+# Optimiser of the training step (§5.1: the prototypes' phase masks are
+# trained with Adam, learning rate 0.5, batch 500).
+# ---------------------------------------------------------------------------
+
+def adam_update(phi: np.ndarray, grad: np.ndarray, m: np.ndarray, v: np.ndarray, step: int,
+                lr: float = 0.5, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8):
+    """One Adam step (Kingma and Ba, 2014, Algorithm 1) on the phase masks.
+
+    step is the 1-based step count t.  Returns (phi', m', v'), float64:
+      m' = beta1 m + (1 - beta1) g,  v' = beta2 v + (1 - beta2) g^2,
+      phi' = phi - lr * (m' / (1 - beta1^t)) / (sqrt(v' / (1 - beta2^t)) + eps).
+    """
+    if step < 1:
+        raise ValueError("step counts from 1")
+    g = np.asarray(grad, dtype=np.float64)
+    m1 = beta1 * np.asarray(m, dtype=np.float64) + (1.0 - beta1) * g
+    v1 = beta2 * np.asarray(v, dtype=np.float64) + (1.0 - beta2) * g * g
+    mhat = m1 / (1.0 - beta1 ** step)
+    vhat = v1 / (1.0 - beta2 ** step)
+    return np.asarray(phi, dtype=np.float64) - lr * mhat / (np.sqrt(vhat) + eps), m1, v1

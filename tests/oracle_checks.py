@@ -242,6 +242,64 @@ def ce_known_values():
     return max(e1, e2, e3, e4)
 
 
+def mse_known_values():
+    """Equal sums give p = 1/K: loss (K-1)/K for any label, dL/dS_j =
+    2/(B K) (1/K - t_j) (the softmax-Jacobian term vanishes); a dominant
+    correct class gives a loss near 0."""
+    b, k = 3, 10
+    labels = np.array([0, 4, 9])
+    loss, grad = od.mse_softmax_loss(np.full((b, k), 2.5), labels)
+    t = np.zeros((b, k))
+    t[np.arange(b), labels] = 1.0
+    e1 = abs(loss - (k - 1) / k)
+    e2 = np.abs(grad - 2.0 / (b * k) * (1.0 / k - t)).max()
+    s = np.zeros((b, k))
+    s[np.arange(b), labels] = 60.0
+    e3 = od.mse_softmax_loss(s, labels)[0]
+    return max(e1, e2, e3)
+
+
+def adam_first_step():
+    """With m = v = 0 the first bias-corrected step is lr * g / (|g| + eps)."""
+    g = np.random.default_rng(21).normal(0, 3, (4, 5))
+    phi = np.random.default_rng(22).uniform(0, 6, (4, 5))
+    lr, eps = 0.5, 1e-8
+    p1, m1, v1 = od.adam_update(phi, g, np.zeros_like(g), np.zeros_like(g), 1, lr=lr, eps=eps)
+    return np.abs(p1 - (phi - lr * g / (np.abs(g) + eps))).max()
+
+
+def adam_constant_gradient():
+    """A constant gradient keeps m-hat = g and v-hat = g^2 at every step, so
+    every step moves phi by lr * g / (|g| + eps)."""
+    g = np.array([[2.0, -0.5, 1e-3]])
+    phi = np.zeros_like(g)
+    m = np.zeros_like(g)
+    v = np.zeros_like(g)
+    err = 0.0
+    for t in range(1, 40):
+        before = phi
+        phi, m, v = od.adam_update(phi, g, m, v, t, lr=0.1, eps=1e-8)
+        err = max(err, np.abs((before - phi) - 0.1 * g / (np.abs(g) + 1e-8)).max())
+    return err
+
+
+def adam_vs_torch():
+    """Three steps with changing gradients agree with torch.optim.Adam (float64, CPU)."""
+    import torch
+    g = np.random.default_rng(23)
+    phi0 = g.uniform(0, 6, (3, 4))
+    grads = [g.normal(0, 1, (3, 4)) for _ in range(3)]
+    p = torch.tensor(phi0.copy(), dtype=torch.float64, requires_grad=True)
+    opt = torch.optim.Adam([p], lr=0.5, betas=(0.9, 0.999), eps=1e-8)
+    phi, m, v = phi0, np.zeros_like(phi0), np.zeros_like(phi0)
+    for t, gr in enumerate(grads, start=1):
+        opt.zero_grad()
+        p.grad = torch.tensor(gr, dtype=torch.float64)
+        opt.step()
+        phi, m, v = od.adam_update(phi, gr, m, v, t, lr=0.5)
+    return np.abs(p.detach().numpy() - phi).max()
+
+
 def loss_fd(loss_fn):
     g = np.random.default_rng(13)
     s = g.normal(0, 2, (4, 6))

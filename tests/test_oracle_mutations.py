@@ -14,7 +14,7 @@ import oracle_checks as c
 _orig = {name: getattr(od, name) for name in (
     "dft_matrix", "idft2", "transfer_function", "frequencies", "propagate",
     "modulate", "detector_readout", "region_scatter", "softmax_cross_entropy",
-    "donn_forward", "donn_backward")}
+    "mse_softmax_loss", "donn_forward", "donn_backward", "adam_update")}
 
 
 def _dft_sign_flipped(m, inverse=False):
@@ -102,6 +102,45 @@ def _make_backward(variant):
     return bwd
 
 
+def _mse_no_softmax_jacobian(sums, labels):
+    # gradient taken with respect to p instead of S
+    s = np.asarray(sums, dtype=np.float64)
+    loss, _ = _orig["mse_softmax_loss"](s, labels)
+    e = np.exp(s - s.max(axis=1, keepdims=True))
+    p = e / e.sum(axis=1, keepdims=True)
+    t = np.zeros_like(p)
+    t[np.arange(s.shape[0]), np.asarray(labels)] = 1.0
+    return loss, 2.0 * (p - t) / s.shape[0]
+
+
+def _mse_not_squared(sums, labels):
+    s = np.asarray(sums, dtype=np.float64)
+    e = np.exp(s - s.max(axis=1, keepdims=True))
+    p = e / e.sum(axis=1, keepdims=True)
+    t = np.zeros_like(p)
+    t[np.arange(s.shape[0]), np.asarray(labels)] = 1.0
+    _, grad = _orig["mse_softmax_loss"](s, labels)
+    return float(np.mean(np.sqrt(((p - t) ** 2).sum(axis=1)))), grad
+
+
+def _adam_no_bias_correction(phi, grad, m, v, step, lr=0.5, beta1=0.9, beta2=0.999, eps=1e-8):
+    g = np.asarray(grad, dtype=np.float64)
+    m1 = beta1 * m + (1 - beta1) * g
+    v1 = beta2 * v + (1 - beta2) * g * g
+    return phi - lr * m1 / (np.sqrt(v1) + eps), m1, v1
+
+
+def _adam_eps_inside_sqrt(phi, grad, m, v, step, lr=0.5, beta1=0.9, beta2=0.999, eps=1e-8):
+    g = np.asarray(grad, dtype=np.float64)
+    m1 = beta1 * m + (1 - beta1) * g
+    v1 = beta2 * v + (1 - beta2) * g * g
+    return phi - lr * (m1 / (1 - beta1 ** step)) / np.sqrt(v1 / (1 - beta2 ** step) + 1e-4), m1, v1
+
+
+def _adam_betas_swapped(phi, grad, m, v, step, lr=0.5, beta1=0.9, beta2=0.999, eps=1e-8):
+    return _orig["adam_update"](phi, grad, m, v, step, lr, beta2, beta1, eps)
+
+
 def _fails_grad(**kw):
     return c.grad_fd(**kw)[0] > 1e-3
 
@@ -119,6 +158,12 @@ MUTANTS = [
     ("scatter_transposed", "region_scatter", _scatter_transposed, lambda: _fails_grad(mode="ce")),
     ("ce_grad_sum_not_mean", "softmax_cross_entropy", _ce_grad_not_averaged,
      lambda: c.loss_fd(od.softmax_cross_entropy) > 1e-3),
+    ("mse_no_softmax_jacobian", "mse_softmax_loss", _mse_no_softmax_jacobian,
+     lambda: c.loss_fd(od.mse_softmax_loss) > 1e-3),
+    ("mse_norm_not_squared", "mse_softmax_loss", _mse_not_squared, lambda: c.mse_known_values() > 1e-3),
+    ("adam_no_bias_correction", "adam_update", _adam_no_bias_correction, lambda: c.adam_first_step() > 1e-3),
+    ("adam_eps_inside_sqrt", "adam_update", _adam_eps_inside_sqrt, lambda: c.adam_constant_gradient() > 1e-3),
+    ("adam_betas_swapped", "adam_update", _adam_betas_swapped, lambda: c.adam_vs_torch() > 1e-3),
     ("missing_last_hop", "donn_forward", _forward_missing_last_hop, lambda: c.donn_zero_phase_gaussian() > 1e-3),
     ("bwd_no_factor_two", "donn_backward", _make_backward("no_factor_two"), lambda: _fails_grad(mode="map")),
     ("bwd_sign", "donn_backward", _make_backward("sign"), lambda: _fails_grad(mode="ce")),

@@ -84,6 +84,23 @@ def test_cross_entropy_known_values():
     assert c.ce_known_values() < 1e-14
 
 
+def test_mse_loss_known_values():
+    assert c.mse_known_values() < 1e-14
+
+
+def test_adam_first_step_closed_form():
+    assert c.adam_first_step() < 1e-14
+
+
+def test_adam_constant_gradient_constant_step():
+    assert c.adam_constant_gradient() < 1e-12
+
+
+def test_adam_matches_torch_optimizer():
+    pytest.importorskip("torch")
+    assert c.adam_vs_torch() < 1e-12
+
+
 @pytest.mark.parametrize("fn", [od.softmax_cross_entropy, od.mse_softmax_loss])
 def test_loss_gradients_by_finite_differences(fn):
     assert c.loss_fd(fn) < 1e-7
