@@ -177,6 +177,38 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
                      const float* d_grad_intensity, float* d_loss, float* d_grad_phi,
                      void* d_work, size_t work_bytes, void* stream);
 
+/* Losses of the detector sums (§2.1: the class whose region collects the most
+ * light is the prediction; §5.1: the prototypes are trained with an MSE loss
+ * on one-hot labels). */
+enum lr_loss_kind {
+  LR_LOSS_SOFTMAX_CE = 0,   /* -log softmax(S)_t */
+  LR_LOSS_SOFTMAX_MSE = 1   /* ||softmax(S) - onehot(t)||^2, summed over classes */
+};
+
+/* Loss of a batch of detector sums, averaged over the batch, and its
+ * gradient dL/dS for lr_donn_backward's d_grad_sums.
+ *   d_sums       float32 [batch][classes] (the region sums of lr_donn_forward)
+ *   d_labels     int32 [batch], class indices in [0, classes); a label out of
+ *                range makes the loss NaN
+ *   d_loss       nullable float32 scalar
+ *   d_grad_sums  nullable float32 [batch][classes], must not alias d_sums
+ * At least one of d_loss, d_grad_sums.  The batch mean is summed in a fixed
+ * order.  Errors: LR_E_ARG (unknown kind), LR_E_SIZE (batch < 0, classes not
+ * in 1..LR_MAX_REGIONS), LR_E_NULL, LR_E_ALIAS. */
+int lr_loss(int32_t kind, const float* d_sums, const int32_t* d_labels, int32_t batch, int32_t classes,
+            float* d_loss, float* d_grad_sums, void* stream);
+
+/* One Adam step on the phase masks (§5.1 trains them with Adam, learning
+ * rate 0.5), element-wise over count floats, in place:
+ *   m = beta1 m + (1 - beta1) g,  v = beta2 v + (1 - beta2) g^2,
+ *   phi -= lr * (m / (1 - beta1^step)) / (sqrt(v / (1 - beta2^step)) + eps).
+ * d_phi, d_m, d_v are updated; d_m and d_v start at zero before step 1.
+ * step counts from 1.  No two pointers may be equal.  Errors: LR_E_SIZE
+ * (count < 0, step < 1), LR_E_ARG (lr or eps not finite, eps < 0, beta not in
+ * [0, 1)), LR_E_NULL, LR_E_ALIAS. */
+int lr_adam_update(float* d_phi, const float* d_grad, float* d_m, float* d_v, int64_t count, int32_t step,
+                   float lr, float beta1, float beta2, float eps, void* stream);
+
 /* Human-readable name of an lr_status. */
 const char* lr_status_string(int status);
 

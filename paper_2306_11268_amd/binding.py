@@ -20,10 +20,13 @@ LR_ANGULAR_SPECTRUM = 1
 LR_OP_PROPAGATE = 0
 LR_OP_FORWARD = 1
 LR_OP_BACKWARD = 2
+LR_LOSS_SOFTMAX_CE = 0
+LR_LOSS_SOFTMAX_MSE = 1
 
 EXPORTS = (
     "lr_tf_build", "lr_workspace_size", "lr_saved_size", "lr_saved_layer_transposed",
     "lr_propagate", "lr_detector_readout", "lr_donn_forward", "lr_donn_backward",
+    "lr_loss", "lr_adam_update",
     "lr_status_string", "lr_kernel_timing", "lr_kernel_timing_report", "lr_version",
 )
 
@@ -69,6 +72,8 @@ def load() -> ctypes.CDLL:
     lib.lr_detector_readout.argtypes = [P, c_int32, c_int32, POINTER(LrDetector), P, P]
     lib.lr_donn_forward.argtypes = [POINTER(LrDonn), c_int32, P, P, P, P, P, P, P, c_size_t, P]
     lib.lr_donn_backward.argtypes = [POINTER(LrDonn), c_int32, P, P, P, P, P, P, P, P, P, c_size_t, P]
+    lib.lr_loss.argtypes = [c_int32, P, P, c_int32, c_int32, P, P, P]
+    lib.lr_adam_update.argtypes = [P, P, P, P, c_int64, c_int32, c_float, c_float, c_float, c_float, P]
     lib.lr_status_string.argtypes = [ctypes.c_int]
     lib.lr_status_string.restype = c_char_p
     lib.lr_kernel_timing.argtypes = [c_int32]
@@ -291,6 +296,32 @@ def lr_donn_backward(net: Network, phi, saved, sums=None, labels=None, grad_sums
         _ptr(loss, torch.float32, None, "loss"), _ptr(out_grad_phi, torch.float32, (L, n, n), "grad_phi"),
         _ptr(w), w.numel(), _stream(dev)), "lr_donn_backward")
     return out_grad_phi, loss
+
+
+def lr_loss(sums, labels, kind: int = LR_LOSS_SOFTMAX_CE, out_grad_sums=None, want_loss: bool = True):
+    """Loss of detector sums [B, K] with int32 labels [B] (batch mean) and dL/dS [B, K]."""
+    torch = _torch()
+    b, k = int(sums.shape[0]), int(sums.shape[1])
+    if out_grad_sums is None:
+        out_grad_sums = torch.empty((b, k), dtype=torch.float32, device=sums.device)
+    loss = torch.empty((), dtype=torch.float32, device=sums.device) if want_loss else None
+    _check(load().lr_loss(int(kind), _ptr(sums, torch.float32, (b, k), "sums"),
+                          _ptr(labels, torch.int32, (b,), "labels"), b, k, _ptr(loss, torch.float32, None, "loss"),
+                          _ptr(out_grad_sums, torch.float32, (b, k), "grad_sums"), _stream(sums.device)), "lr_loss")
+    return loss, out_grad_sums
+
+
+def lr_adam_update(phi, grad, m, v, step: int, lr: float = 0.5, beta1: float = 0.9, beta2: float = 0.999,
+                   eps: float = 1e-8):
+    """One in-place Adam step on phi (and its moments m, v), all float32 of one shape."""
+    torch = _torch()
+    shape = tuple(phi.shape)
+    count = int(phi.numel())
+    _check(load().lr_adam_update(_ptr(phi, torch.float32, shape, "phi"), _ptr(grad, torch.float32, shape, "grad"),
+                                 _ptr(m, torch.float32, shape, "m"), _ptr(v, torch.float32, shape, "v"), count,
+                                 int(step), float(lr), float(beta1), float(beta2), float(eps),
+                                 _stream(phi.device)), "lr_adam_update")
+    return phi
 
 
 def kernel_timing(enable: bool) -> None:

@@ -657,7 +657,7 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
   if (d_labels) {
     float* g = at<float>(d_work, L.grad_sums);
     LR_TRY(run_timed("ce_loss", st,
-                     [&] { return lr::launch_ce_loss(d_sums, d_labels, batch, net->det.num, g, d_loss, st); }));
+                     [&] { return lr::launch_loss(0, d_sums, d_labels, batch, net->det.num, g, d_loss, st); }));
     gsum = g;
   }
 
@@ -751,6 +751,42 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
     groups_of[l - 1] = L.groups;
   }
   return reduce_all();
+}
+
+int lr_loss(int32_t kind, const float* d_sums, const int32_t* d_labels, int32_t batch, int32_t classes,
+            float* d_loss, float* d_grad_sums, void* stream) {
+  if (kind != LR_LOSS_SOFTMAX_CE && kind != LR_LOSS_SOFTMAX_MSE) return LR_E_ARG;
+  if (batch < 0 || classes < 1 || classes > LR_MAX_REGIONS) return LR_E_SIZE;
+  if (!d_loss && !d_grad_sums) return LR_E_NULL;
+  if (batch == 0) return LR_OK;
+  if (!d_sums || !d_labels) return LR_E_NULL;
+  if (static_cast<const void*>(d_grad_sums) == static_cast<const void*>(d_sums)) return LR_E_ALIAS;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return run_timed(kind == LR_LOSS_SOFTMAX_CE ? "ce_loss" : "mse_loss", st, [&] {
+    return lr::launch_loss(kind, d_sums, d_labels, batch, classes, d_grad_sums, d_loss, st);
+  });
+}
+
+int lr_adam_update(float* d_phi, const float* d_grad, float* d_m, float* d_v, int64_t count, int32_t step, float lr,
+                   float beta1, float beta2, float eps, void* stream) {
+  if (count < 0 || step < 1) return LR_E_SIZE;
+  if (!std::isfinite(lr) || !(beta1 >= 0.f && beta1 < 1.f) || !(beta2 >= 0.f && beta2 < 1.f) ||
+      !(eps >= 0.f) || !std::isfinite(eps))
+    return LR_E_ARG;
+  if (count == 0) return LR_OK;
+  if (!d_phi || !d_grad || !d_m || !d_v) return LR_E_NULL;
+  const void* p[4] = {d_phi, d_grad, d_m, d_v};
+  for (int i = 0; i < 4; ++i)
+    for (int k = i + 1; k < 4; ++k)
+      if (p[i] == p[k]) return LR_E_ALIAS;
+  const double bc1 = 1.0 - std::pow(static_cast<double>(beta1), step);
+  const double bc2 = 1.0 - std::pow(static_cast<double>(beta2), step);
+  if (!(bc1 > 0.0) || !(bc2 > 0.0)) return LR_E_ARG;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return run_timed("adam", st, [&] {
+    return lr::launch_adam(d_phi, d_grad, d_m, d_v, static_cast<long long>(count), lr, beta1, beta2, eps,
+                           static_cast<float>(bc1), static_cast<float>(bc2), st);
+  });
 }
 
 int lr_kernel_timing(int32_t enable) {

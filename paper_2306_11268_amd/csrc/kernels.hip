@@ -47,10 +47,15 @@ __global__ void finish_sums_kernel(const float* __restrict__ part, int batch, in
   sums[i] = s;
 }
 
-// Softmax cross-entropy over the detector sums, averaged over the batch.
-// One workgroup; sample b is handled by thread b % 1024 in a fixed order.
-__global__ void __launch_bounds__(1024) ce_loss_kernel(const float* __restrict__ sums, const int32_t* __restrict__ labels,
-                                                      int batch, int K, float* __restrict__ grad, float* __restrict__ loss) {
+// Loss of the detector sums, averaged over the batch, and its gradient
+// dL/dS.  kind 0: softmax cross-entropy, -log p_t.  kind 1: the paper's
+// ||softmax(S) - onehot(t)||^2, whose gradient goes through the softmax
+// Jacobian: dL/dS_j = p_j (d_j - sum_i d_i p_i), d = 2 (p - t) / B.
+// One workgroup; sample b is handled by thread b % 1024 and the per-thread
+// losses are summed in a fixed order.  An out-of-range label makes the loss NaN.
+__global__ void __launch_bounds__(1024) loss_kernel(int kind, const float* __restrict__ sums,
+                                                    const int32_t* __restrict__ labels, int batch, int K,
+                                                    float* __restrict__ grad, float* __restrict__ loss) {
   __shared__ float red[16];
   float my = 0.f;
   const float invb = 1.0f / (float)batch;
@@ -62,15 +67,50 @@ __global__ void __launch_bounds__(1024) ce_loss_kernel(const float* __restrict__
     for (int k = 0; k < K; ++k) z += expf(s[k] - mx);
     const float lz = logf(z);
     const int tl = labels[b];
-    const bool valid = (unsigned)tl < (unsigned)K;  // an out-of-range label makes the loss NaN
-    for (int k = 0; k < K; ++k) {
-      const float p = expf(s[k] - mx - lz);
-      grad[(size_t)b * K + k] = (p - (k == tl ? 1.f : 0.f)) * invb;
+    const bool valid = (unsigned)tl < (unsigned)K;
+    float lb;
+    if (kind == 0) {
+      lb = lz + mx - (valid ? s[tl] : 0.f);
+      if (grad) {
+        for (int k = 0; k < K; ++k) grad[(size_t)b * K + k] = (expf(s[k] - mx - lz) - (k == tl ? 1.f : 0.f)) * invb;
+      }
+    } else {
+      lb = 0.f;
+      float c = 0.f;  // sum_i d_i p_i
+      for (int k = 0; k < K; ++k) {
+        const float p = expf(s[k] - mx - lz);
+        const float r = p - (k == tl ? 1.f : 0.f);
+        lb += r * r;
+        c += 2.f * r * invb * p;
+      }
+      if (grad) {
+        for (int k = 0; k < K; ++k) {
+          const float p = expf(s[k] - mx - lz);
+          const float d = 2.f * (p - (k == tl ? 1.f : 0.f)) * invb;
+          grad[(size_t)b * K + k] = p * (d - c);
+        }
+      }
     }
-    my += valid ? (lz + mx - s[tl]) : __builtin_nanf("");
+    my += valid ? lb : __builtin_nanf("");
   }
   const float tot = block_sum<1024>(my, red);
   if (threadIdx.x == 0 && loss) *loss = tot * invb;
+}
+
+// One Adam step on every element: m = b1 m + (1-b1) g, v = b2 v + (1-b2) g^2,
+// phi -= lr * (m / bc1) / (sqrt(v / bc2) + eps), bc = 1 - beta^t.
+__global__ void adam_kernel(float* __restrict__ phi, const float* __restrict__ g, float* __restrict__ m,
+                            float* __restrict__ v, long long count, float lr, float b1, float b2, float eps,
+                            float bc1, float bc2) {
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < count;
+       i += (long long)gridDim.x * blockDim.x) {
+    const float gi = g[i];
+    const float mi = b1 * m[i] + (1.f - b1) * gi;
+    const float vi = b2 * v[i] + (1.f - b2) * gi * gi;
+    m[i] = mi;
+    v[i] = vi;
+    phi[i] -= lr * (mi / bc1) / (sqrtf(vi / bc2) + eps);
+  }
 }
 
 // dphi_l[y][x] = sum over groups of part_l[g][q][vec], oriented (transposed:
@@ -352,9 +392,19 @@ hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, f
   return hipGetLastError();
 }
 
-hipError_t launch_ce_loss(const float* sums, const int32_t* labels, int batch, int K, float* grad, float* loss,
-                          hipStream_t st) {
-  hipLaunchKernelGGL(ce_loss_kernel, dim3(1), dim3(1024), 0, st, sums, labels, batch, K, grad, loss);
+hipError_t launch_loss(int kind, const float* sums, const int32_t* labels, int batch, int K, float* grad, float* loss,
+                       hipStream_t st) {
+  hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(1024), 0, st, kind, sums, labels, batch, K, grad, loss);
+  return hipGetLastError();
+}
+
+hipError_t launch_adam(float* phi, const float* g, float* m, float* v, long long count, float lr, float b1, float b2,
+                       float eps, float bc1, float bc2, hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  long long blocks = (count + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  hipLaunchKernelGGL(adam_kernel, dim3((unsigned)blocks), dim3(256), 0, st, phi, g, m, v, count, lr, b1, b2, eps, bc1,
+                     bc2);
   return hipGetLastError();
 }
 

@@ -112,8 +112,14 @@ hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t
 // Small helper kernels.
 hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, hipStream_t st);
 hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, float* sums, hipStream_t st);
-hipError_t launch_ce_loss(const float* sums, const int32_t* labels, int batch, int K, float* grad_sums,
-                          float* loss, hipStream_t st);
+// Loss of the detector sums (kind 0: softmax cross-entropy, 1: squared norm
+// of softmax minus one-hot), mean over the batch, and dL/dS; grad and loss
+// are nullable.
+hipError_t launch_loss(int kind, const float* sums, const int32_t* labels, int batch, int K, float* grad_sums,
+                       float* loss, hipStream_t st);
+// One Adam step over count elements (bc1, bc2: bias corrections 1 - beta^t).
+hipError_t launch_adam(float* phi, const float* g, float* m, float* v, long long count, float lr, float b1, float b2,
+                       float eps, float bc1, float bc2, hipStream_t st);
 // dphi of `layers` layers in one launch: layer l sums groups[l] partials
 // (oriented [q][vec], transposed[l] != 0: q = x) starting at
 // part + l * layer_stride floats into out + l * n * n.

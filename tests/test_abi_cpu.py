@@ -21,7 +21,7 @@ def declared_functions():
     return sorted(set(re.findall(r"\b(lr_[a-z0-9_]+)\s*\(", text)))
 
 
-def test_header_declares_the_five_entry_points():
+def test_header_declares_the_entry_points():
     fns = declared_functions()
     for f in ("lr_tf_build", "lr_propagate", "lr_donn_forward", "lr_donn_backward", "lr_detector_readout"):
         assert f in fns
@@ -118,6 +118,31 @@ def test_entry_points_reject_bad_arguments_without_touching_the_gpu():
                                 None) == 3
     assert lib.lr_donn_backward(ref, 2, dummy, None, None, None, None, dummy, None, dummy, dummy, 1 << 30,
                                 None) == 1
+    # loss: kind, sizes, outputs, aliasing
+    assert lib.lr_loss(2, dummy, dummy, 4, 10, dummy, P(0x3000), None) == 3
+    assert lib.lr_loss(0, dummy, dummy, -1, 10, dummy, P(0x3000), None) == 2
+    assert lib.lr_loss(1, dummy, dummy, 4, 65, dummy, P(0x3000), None) == 2
+    assert lib.lr_loss(0, dummy, dummy, 4, 10, None, None, None) == 1
+    assert lib.lr_loss(0, None, dummy, 4, 10, dummy, None, None) == 1
+    assert lib.lr_loss(0, dummy, P(0x3000), 4, 10, None, dummy, None) == 7
+    assert lib.lr_loss(0, None, None, 0, 10, dummy, None, None) == 0
+    # Adam: step, hyper-parameters, pointers, aliasing
+    f = ctypes.c_float
+    assert lib.lr_adam_update(dummy, P(0x3000), P(0x4000), P(0x5000), 8, 0, f(0.5), f(0.9), f(0.999), f(1e-8),
+                              None) == 2
+    assert lib.lr_adam_update(dummy, P(0x3000), P(0x4000), P(0x5000), -1, 1, f(0.5), f(0.9), f(0.999), f(1e-8),
+                              None) == 2
+    assert lib.lr_adam_update(dummy, P(0x3000), P(0x4000), P(0x5000), 8, 1, f(0.5), f(1.0), f(0.999), f(1e-8),
+                              None) == 3
+    assert lib.lr_adam_update(dummy, P(0x3000), P(0x4000), P(0x5000), 8, 1, f(float("nan")), f(0.9), f(0.999),
+                              f(1e-8), None) == 3
+    assert lib.lr_adam_update(dummy, P(0x3000), P(0x4000), P(0x5000), 8, 1, f(0.5), f(0.9), f(0.999), f(-1.0),
+                              None) == 3
+    assert lib.lr_adam_update(None, P(0x3000), P(0x4000), P(0x5000), 8, 1, f(0.5), f(0.9), f(0.999), f(1e-8),
+                              None) == 1
+    assert lib.lr_adam_update(dummy, P(0x3000), dummy, P(0x5000), 8, 1, f(0.5), f(0.9), f(0.999), f(1e-8),
+                              None) == 7
+    assert lib.lr_adam_update(None, None, None, None, 0, 1, f(0.5), f(0.9), f(0.999), f(1e-8), None) == 0
     # detector readout
     det = lb.LrDetector(1, 300, None, None)
     assert lib.lr_detector_readout(dummy, 2, 200, ctypes.byref(det), dummy, None) in (1, 3)

@@ -151,3 +151,75 @@ def test_training_step_at_full_size(lrb):
     assert np.array_equal(g1, host(grad2))
     s = g1.sum(axis=(1, 2))
     assert np.all(np.abs(s) <= 1e-4 * np.abs(g1).sum(axis=(1, 2)))
+
+
+# ---------------------------------------------------------------------------
+# losses and the optimiser step (§2.1, §5.1)
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("kind,fn", [(0, od.softmax_cross_entropy), (1, od.mse_softmax_loss)])
+def test_loss_modes(lrb, kind, fn):
+    g = np.random.default_rng(31)
+    sums = g.normal(0.0, 3.0, (500, 10)).astype(np.float32)
+    labels = g.integers(0, 10, 500).astype(np.int32)
+    loss, grad = lrb.lr_loss(dev(sums), dev(labels), kind=kind)
+    ref_loss, ref_grad = fn(sums, labels)
+    assert abs(float(loss) - ref_loss) / abs(ref_loss) < 1e-5
+    assert rel(host(grad), ref_grad) < 1e-5
+
+
+def test_mse_training_step(lrb):
+    # the prototypes' loss (§5.1): squared norm of softmax(S) - onehot(t)
+    w = wl.WORKLOADS[3]
+    b = 6
+    net, phi, saved, out, ref, h = sums_only_forward(lrb, w, b, w.layers, w.detector)
+    labels = wl.labels(w, b)
+    loss, gs = lrb.lr_loss(out["sums"], dev(labels), kind=lrb.LR_LOSS_SOFTMAX_MSE)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_sums=gs)
+    ref_loss, ref_gs = od.mse_softmax_loss(ref["sums"], labels)
+    ref_grad = od.donn_backward(ref, phi, h, 1.0, odet(w.detector), grad_sums=ref_gs)
+    assert abs(float(loss) - ref_loss) / abs(ref_loss) < TOL_FIELD
+    assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+# the library receives its hyper-parameters as float32; the oracle gets the same values
+ADAM_F32 = dict(lr=float(np.float32(0.5)), beta1=float(np.float32(0.9)), beta2=float(np.float32(0.999)),
+                eps=float(np.float32(1e-8)))
+
+
+def test_adam_steps(lrb):
+    g = np.random.default_rng(32)
+    phi0 = g.uniform(0.0, 2 * np.pi, (5, 200, 200)).astype(np.float32)
+    grads = [g.normal(0.0, 1e-3, (5, 200, 200)).astype(np.float32) for _ in range(4)]
+    phi = dev(phi0.copy())
+    m = torch.zeros_like(phi)
+    v = torch.zeros_like(phi)
+    ref = (phi0.astype(np.float64), np.zeros(phi0.shape), np.zeros(phi0.shape))
+    for t, gr in enumerate(grads, start=1):
+        lrb.lr_adam_update(phi, dev(gr), m, v, t, **ADAM_F32)
+        ref = od.adam_update(ref[0], gr, ref[1], ref[2], t, **ADAM_F32)
+    assert rel(host(phi), ref[0]) < 1e-6
+    assert rel(host(m), ref[1]) < 1e-5
+    assert rel(host(v), ref[2]) < 1e-5
+
+
+def test_training_iteration_at_full_size(lrb):
+    """One iteration of the prototypes' training (§5.1) on the benchmark
+    workload: sums-only forward, MSE loss, backward, Adam with learning rate
+    0.5.  The gradient is checked against the oracle's, and the step against
+    the oracle's Adam applied to the same float32 gradient."""
+    w = wl.WORKLOADS[3]
+    b = w.batch
+    net, phi, saved, out, ref, h = sums_only_forward(lrb, w, b, w.layers, w.detector)
+    labels = wl.labels(w, b)
+    _, gs = lrb.lr_loss(out["sums"], dev(labels), kind=lrb.LR_LOSS_SOFTMAX_MSE, want_loss=False)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_sums=gs)
+    _, ref_gs = od.mse_softmax_loss(ref["sums"], labels)
+    assert rel(host(grad), od.donn_backward(ref, phi, h, 1.0, odet(w.detector), grad_sums=ref_gs)) < TOL_GRAD
+    g32 = host(grad)
+    phi_dev = dev(phi.copy())
+    m = torch.zeros_like(phi_dev)
+    v = torch.zeros_like(phi_dev)
+    lrb.lr_adam_update(phi_dev, grad, m, v, 1, **ADAM_F32)
+    ref_phi, _, _ = od.adam_update(phi, g32, np.zeros(phi.shape), np.zeros(phi.shape), 1, **ADAM_F32)
+    assert rel(host(phi_dev), ref_phi) < 1e-6
