@@ -34,10 +34,10 @@ AXES = ("row", "col")
 
 def label(name: str) -> str:
     """Short label of a demangled kernel name."""
-    m = re.search(r"fresnel_pass<.*?Plan2<(\d+), (\d+).*, (\d+), (\d+)>\(", name)
+    m = re.search(r"(fresnel|detector)_pass<.*?Plan2<(\d+), (\d+).*, (\d+), (\d+)>\(", name)
     if m:
-        n = int(m.group(1)) * int(m.group(2))
-        return f"fresnel_pass_{FR_KINDS[int(m.group(3))]}_{AXES[int(m.group(4))]}_N{n}"
+        n = int(m.group(2)) * int(m.group(3))
+        return f"fresnel_pass_{FR_KINDS[int(m.group(4))]}_{AXES[int(m.group(5))]}_N{n}"
     m = re.search(r"as_pass<.*?Plan2<(\d+), (\d+).*, (\d+)>\(", name)
     if m:
         n = int(m.group(1)) * int(m.group(2))
