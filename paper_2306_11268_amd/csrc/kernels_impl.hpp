@@ -471,12 +471,13 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
   constexpr bool ACC = (KIND == kBwdMid || KIND == kBwdLast);
   constexpr bool TWO = (KIND == kFwdMid || KIND == kBwdMid);
   constexpr bool DIRECT = AXIS == kCol;  // column tiles address their A-items in global memory
-  // Accumulating (backward) passes run persistently and prefetch the next
-  // item's field (column tiles: into registers that are free by then; row
-  // tiles, whose staging buffer is larger, load at the top).  The other kinds
-  // get one item per workgroup (workers = items): a finishing workgroup
-  // leaves its stores draining while a fresh one starts loading.
-  constexpr bool PREFETCH = DIRECT && ACC;
+  // Accumulating (backward) passes run persistently; the other kinds get one
+  // item per workgroup (workers = items), so a finishing workgroup leaves its
+  // stores draining while a fresh one starts loading.  The last adjoint
+  // column pass, which has registers to spare (no modulation, no output),
+  // prefetches the next item's field; in the others the extra buffer would
+  // spill.
+  constexpr bool PREFETCH = DIRECT && KIND == kBwdLast;
   const Tile<C> t{lds, (int)(threadIdx.x % C::T), (int)(threadIdx.x / C::T)};
   const int j = t.s;
 
