@@ -123,16 +123,13 @@ int lr_tf_build(double wavelength, double pixel_pitch, double distance, int32_t 
 int64_t lr_workspace_size(const lr_donn* net, int32_t batch, int32_t op);
 
 /* Bytes of the saved-state buffer that lr_donn_forward fills for
- * lr_donn_backward: the L activations U_l, then one detector-plane field, each
- * complex64 [batch][n][n].  Activation l (1-based) is stored transposed
- * ([batch][x][y]) when lr_saved_layer_transposed() says so, natural
- * ([batch][y][x]) otherwise.  The detector-plane field is internal state: the
- * Fresnel path keeps the field after the first-axis half of the last hop
- * (lr_donn_backward finishes that hop itself, on the rows or columns the seed
- * needs), the angular-spectrum path keeps U_D.  Negative lr_status on invalid
- * arguments. */
+ * lr_donn_backward: L+1 complex64 fields of [batch][n][n].  Their content is
+ * internal state of the two calls, valid only for the same network, batch
+ * and phase masks.  (The Fresnel path keeps the field each of its separable
+ * passes wrote, from which the backward pass recomputes the activations
+ * U_l; the angular-spectrum path keeps U_1..U_L and U_D.)  Negative
+ * lr_status on invalid arguments. */
 int64_t lr_saved_size(const lr_donn* net, int32_t batch);
-int32_t lr_saved_layer_transposed(const lr_donn* net, int32_t layer);
 
 /* One hop of `batch` fields (§3.1.1): d_out = P_z(d_in), or its Hilbert
  * adjoint P_z^H (the same pad/crop with conj(H), i.e. back-propagation) when

@@ -24,7 +24,7 @@ LR_LOSS_SOFTMAX_CE = 0
 LR_LOSS_SOFTMAX_MSE = 1
 
 EXPORTS = (
-    "lr_tf_build", "lr_workspace_size", "lr_saved_size", "lr_saved_layer_transposed",
+    "lr_tf_build", "lr_workspace_size", "lr_saved_size",
     "lr_propagate", "lr_detector_readout", "lr_donn_forward", "lr_donn_backward",
     "lr_loss", "lr_adam_update",
     "lr_status_string", "lr_kernel_timing", "lr_kernel_timing_report", "lr_version",
@@ -66,8 +66,6 @@ def load() -> ctypes.CDLL:
     lib.lr_workspace_size.restype = c_int64
     lib.lr_saved_size.argtypes = [POINTER(LrDonn), c_int32]
     lib.lr_saved_size.restype = c_int64
-    lib.lr_saved_layer_transposed.argtypes = [POINTER(LrDonn), c_int32]
-    lib.lr_saved_layer_transposed.restype = c_int32
     lib.lr_propagate.argtypes = [POINTER(LrDonn), c_int32, P, P, c_int32, P, c_size_t, P]
     lib.lr_detector_readout.argtypes = [P, c_int32, c_int32, POINTER(LrDetector), P, P]
     lib.lr_donn_forward.argtypes = [POINTER(LrDonn), c_int32, P, P, P, P, P, P, P, c_size_t, P]
@@ -192,21 +190,6 @@ class Network:
     def new_saved(self, batch: int):
         torch = _torch()
         return torch.empty(max(self.saved_size(batch), 1), dtype=torch.uint8, device=self.device)
-
-    def layer_transposed(self, layer: int) -> bool:
-        return bool(load().lr_saved_layer_transposed(ctypes.byref(self.c), int(layer)))
-
-    def saved_activation(self, saved, batch: int, layer: int):
-        """View of U_layer (1-based, layer <= L) from a saved buffer, natural [B, n, n]."""
-        torch = _torch()
-        if not 1 <= layer <= self.num_layers:
-            raise ValueError(f"layer must be in 1..{self.num_layers}")
-        nn = self.n * self.n
-        flat = saved.view(torch.complex64)[: (self.num_layers + 1) * batch * nn]
-        t = flat[(layer - 1) * batch * nn: layer * batch * nn].view(batch, self.n, self.n)
-        if self.layer_transposed(layer):
-            t = t.transpose(1, 2)
-        return t
 
 
 # ---------------------------------------------------------------------------

@@ -225,7 +225,9 @@ std::string as_name(int N, int kind) {
 // Accumulating passes run persistently, as many workgroups as fit on the
 // device at once: each keeps one tile and takes a share of the batch for one
 // of `lanes` partial sums (lanes <= max_lanes, the partials the workspace
-// holds).  The other passes take one (tile, sample) item per workgroup.
+// holds).  The other passes take one (tile, sample) item per workgroup: the
+// hardware dispatcher then balances them, which measured faster than a
+// persistent schedule with prefetching for them.
 int schedule_layer_pass(int N, lr::PassKind kind, Axis ax, int max_lanes, PassArgs& a) {
   const int slots = lr::fresnel_pass_slots(N, kind, ax);
   const int tile_t = lr::fresnel_pass_tile(N, kind, ax);
@@ -237,7 +239,7 @@ int schedule_layer_pass(int N, lr::PassKind kind, Axis ax, int max_lanes, PassAr
     a.lanes = lanes;
     a.workers = lanes * a.ntiles;
   } else {
-    a.lanes = 0;  // one (tile, sample) item per workgroup
+    a.lanes = 0;
     a.workers = a.ntiles * a.batch;
   }
   return LR_OK;
@@ -440,11 +442,6 @@ int64_t lr_saved_size(const lr_donn* net, int32_t batch) {
   return static_cast<int64_t>(net->num_layers + 1) * batch * net->n * net->n * 8;
 }
 
-int32_t lr_saved_layer_transposed(const lr_donn* net, int32_t layer) {
-  if (!net || layer < 1 || layer > net->num_layers) return -LR_E_ARG;
-  return layer_transposed(net, layer);
-}
-
 int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* d_out, int32_t adjoint,
                  void* d_work, size_t work_bytes, void* stream) {
   LR_TRY(validate_net(net, false));
@@ -531,37 +528,33 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
     a.nvec = n;
     a.ntiles = L.ntiles_vec;
     auto chirp = [&](Axis ax) { return at<float2>(d_work, ax == lr::kRow ? L.chirp_x : L.chirp_y); };
-    // pass 1: first sweep of hop 1 along x
+    // Pass p writes W_p: slot p of the saved state when there is one (the
+    // backward pass reads W_0 .. W_L there), else the two work fields in turn.
+    auto w_out = [&](int p) { return saved ? saved + static_cast<size_t>(p) * batch * nn : w[p & 1]; };
+    // pass 0: first sweep of hop 1 along x
     a.in = d_amp;
     a.in_real = 1;
-    a.out = w[0];
+    a.out = w_out(0);
     a.tab = chirp(lr::kRow);
     LR_TRY(fr_pass(N, lr::kPropOnce, lr::kRow, a, st));
     a.in_real = 0;
-    int cur = 0;
-    // passes 2..L+1: end of hop l, modulation of layer l, start of hop l+1.
-    // The last of them writes W (the field after the first-axis half of hop
-    // L+1) into the saved state, where the backward pass finds it.
-    float2* w_last = saved ? saved + static_cast<size_t>(Lyr) * batch * nn : nullptr;
+    // passes 1..L: end of hop l, modulation of layer l, start of hop l+1
     for (int l = 1; l <= Lyr; ++l) {
       const Axis ax = pass_axis(l + 1);
-      a.in = w[cur];
-      a.out = (l == Lyr && w_last) ? w_last : w[cur ^ 1];
+      a.in = a.out;
+      a.out = w_out(l);
       a.tab = chirp(ax);
       a.mod = ws_mod + static_cast<size_t>(l - 1) * nn;
-      a.act_out = saved ? saved + static_cast<size_t>(l - 1) * batch * nn : nullptr;
       LR_TRY(fr_pass(N, lr::kFwdMid, ax, a, st));
-      cur ^= 1;
     }
-    // pass L+2: rest of hop L+1, detector plane
+    // pass L+1: rest of hop L+1, detector plane
     if (d_sums || d_intensity || d_field_out) {
       const Axis ax = pass_axis(Lyr + 2);
       PassArgs d = a;
-      d.in = w_last ? w_last : w[cur];
+      d.in = a.out;
       d.out = nullptr;
       d.tab = chirp(ax);
       d.mod = nullptr;
-      d.act_out = nullptr;
       d.intensity = d_intensity;
       d.field_out = reinterpret_cast<float2*>(d_field_out);
       if (d_sums) {
@@ -680,7 +673,7 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
 
   if (net->approx == LR_FRESNEL) {
     auto chirp = [&](Axis ax) { return at<float2>(d_work, ax == lr::kRow ? L.chirp_x : L.chirp_y); };
-    // rest of hop L+1 from the saved W, seed at the detector plane, adjoint of that half hop
+    // rest of hop L+1 from the saved W_L, seed at the detector plane, adjoint of that half hop
     {
       PassArgs s = a;
       const Axis ax = pass_axis(Lyr + 2);
@@ -703,7 +696,7 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
       m.in = w[cur];
       m.tab = chirp(ax);
       m.mod = ws_mod + static_cast<size_t>(l - 1) * nn;
-      m.act_in = saved + static_cast<size_t>(l - 1) * batch * nn;
+      m.act_in = saved + static_cast<size_t>(l - 1) * batch * nn;  // W_{l-1}, input of layer l's forward pass
       m.dphi_part = part_of(l);
       const lr::PassKind kind = l > 1 ? lr::kBwdMid : lr::kBwdLast;
       LR_TRY(schedule_layer_pass(N, kind, ax, L.groups, m));

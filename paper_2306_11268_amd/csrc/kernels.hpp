@@ -13,11 +13,11 @@ enum Axis : int { kRow = 0, kCol = 1 };
 // What one pass of the separable (Fresnel) path does along its axis.
 enum PassKind : int {
   kPropOnce = 0,   // load -> one 1-D propagation -> store
-  kFwdMid = 1,     // load -> prop -> x M_l (store U_l) -> prop -> store
+  kFwdMid = 1,     // load W_{l-1} -> prop -> x M_l -> prop -> store W_l
   kFwdLast = 2,    // load -> prop -> detector-plane outputs
   kBwdFirst = 3,   // load -> prop (U_D) -> seed 2*(dL/dI)*U_D -> adjoint prop -> store
-  kBwdMid = 4,     // load -> adj prop -> dphi_l -> x conj(M_l) -> adj prop -> store
-  kBwdLast = 5,    // load -> adj prop -> dphi_1
+  kBwdMid = 4,     // load W_{l-1} -> prop (A_l); load G -> adj prop -> dphi_l -> x conj(M_l) -> adj prop -> store
+  kBwdLast = 5,    // load W_0 -> prop (A_1); load G -> adj prop -> dphi_1
 };
 
 // Passes of the non-separable (angular-spectrum) path.  Fields between
@@ -60,8 +60,8 @@ struct PassArgs {
   // modulation gamma*exp(j*phi_l), oriented [q][vec]
   const float2* mod;
   int conj_mod;
-  float2* act_out;      // oriented [B][n][n]
-  const float2* act_in; // oriented [B][n][n]
+  float2* act_out;      // angular-spectrum path: U_l, oriented [B][n][n]
+  const float2* act_in; // angular-spectrum path: U_l, oriented; separable path: W_{l-1}, natural [B][n][n]
   float* dphi_part;     // oriented [groups][n][n]
   // detector-plane outputs (natural [B][n][n] layouts)
   float* intensity;

@@ -50,6 +50,27 @@ __device__ __forceinline__ void st_stream(float2* base, unsigned idx, float2 v) 
                               reinterpret_cast<unsigned long long*>(reinterpret_cast<char*>(base) + idx * 8u));
 }
 
+// Raw buffer access.  A buffer resource bounds every access to [0, bytes):
+// a load at an out-of-range offset returns zero and a store there is
+// dropped, so masked elements take the offset kOutOfRange instead of a
+// branch, and runs of loads and stores stay in one basic block.  The base
+// must be uniform over the wave.
+constexpr unsigned kOutOfRange = 0x80000000u;
+using Rsrc = __amdgpu_buffer_rsrc_t;
+typedef int lr_v2i __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ Rsrc make_rsrc(const void* base, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float2 bload(Rsrc r, unsigned off) {
+  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
+}
+__device__ __forceinline__ void bstore(Rsrc r, unsigned off, float2 v) {
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(lr_v2i, v), r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void bstore_f(Rsrc r, unsigned off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, (int)off, 0, 0);
+}
+
 // threadIdx.x behind an empty asm statement: values derived from it are not
 // hoisted out of the per-sample loop (which would keep dozens of index
 // registers alive through the whole kernel); they are recomputed next to
@@ -429,38 +450,51 @@ __device__ __forceinline__ void for_a_elems(int off, int n, int pitch, int vec, 
   });
 }
 
+// (in / out: n rows of pitch elements, wave-uniform)
 template <class C>
 __device__ __forceinline__ void load_a_direct(const float2* __restrict__ in, int pitch, int n, int off, int vec,
                                               bool vok, float2 (&x)[C::N1]) {
+  const Rsrc r = make_rsrc(in, (unsigned)(n * pitch) * 8u);
   for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
-    x[k.value] = valid ? ld(in, idx) : c2(0.f, 0.f);
+    x[k.value] = bload(r, valid ? (unsigned)idx * 8u : kOutOfRange);
   });
 }
 template <class C>
 __device__ __forceinline__ void store_a_direct(float2* __restrict__ out, int pitch, int n, int off, int vec,
                                                bool vok, const float2 (&x)[C::N1]) {
+  const Rsrc r = make_rsrc(out, (unsigned)(n * pitch) * 8u);
   for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
-    if (valid) st(out, idx, x[k.value]);
+    bstore(r, valid ? (unsigned)idx * 8u : kOutOfRange, x[k.value]);
   });
+}
+// Per-layer [q][vec] table of n x n entries at this thread's A-item.
+template <class C>
+__device__ __forceinline__ void load_a_table(const float2* __restrict__ tab, int n, int off, int vec, bool vok,
+                                             float2 (&m)[C::N1]) {
+  load_a_direct<C>(tab, n, n, off, vec, vok, m);
 }
 
 // ---------------------------------------------------------------------------
 // Separable (Fresnel) passes through the layers.
 //
-// Schedule (PassArgs::workers / lanes): a workgroup walks a sequence of
-// (tile, sample) items; with prefetching it issues the global loads of the
-// next item's field while it still transforms the current one, into
-// registers whose previous contents are dead by then (the modulation, or the
-// current field after its first A-step).  The workgroup ranks are
-// XCD-contiguous, so the workgroups of one XCD work on neighbouring items at
-// the same time.
+// What the forward pass keeps for the backward one is the field each of its
+// passes writes: W_0 after the first half hop, and W_l after the pass of
+// layer l (end of hop l, modulation, first-axis half of hop l+1).  The
+// adjoint pass of layer l runs along the same axis as the forward pass that
+// made W_l from W_{l-1}, so it recomputes the arriving field
+// A_l = (half hop)(W_{l-1}) with one more 1-D propagation instead of reading
+// a stored activation.  A forward layer pass therefore moves 16 bytes per
+// pixel (one field read, one written) instead of 24, at the price of a third
+// propagation in the adjoint pass.  The recomputation repeats the forward
+// arithmetic, so it is exact with and without aperture padding.
+//
+// Schedule (PassArgs::workers / lanes): workgroup rank r takes the (tile,
+// sample) items r, r + workers, ...  Forward kinds get one item per
+// workgroup; accumulating kinds run persistently with workers = lanes *
+// ntiles, so a workgroup keeps one tile and strides through the batch.  The
+// ranks are XCD-contiguous: the workgroups of one XCD work on neighbouring
+// items at the same time.
 // ---------------------------------------------------------------------------
-struct Cursor {
-  int tile;
-  int b;     // sample
-  int item;  // flat item index (without accumulation)
-};
-
 template <class C, int KIND, int AXIS>
 __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
     fresnel_pass(PassArgs a) {
@@ -469,15 +503,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
   __shared__ float2 lds[C::LDS_ELEMS];
   constexpr int N1 = C::N1;
   constexpr bool ACC = (KIND == kBwdMid || KIND == kBwdLast);
-  constexpr bool TWO = (KIND == kFwdMid || KIND == kBwdMid);
   constexpr bool DIRECT = AXIS == kCol;  // column tiles address their A-items in global memory
-  // Accumulating (backward) passes run persistently; the other kinds get one
-  // item per workgroup (workers = items), so a finishing workgroup leaves its
-  // stores draining while a fresh one starts loading.  The last adjoint
-  // column pass, which has registers to spare (no modulation, no output),
-  // prefetches the next item's field; in the others the extra buffer would
-  // spill.
-  constexpr bool PREFETCH = DIRECT && KIND == kBwdLast;
   const Tile<C> t{lds, (int)(threadIdx.x % C::T), (int)(threadIdx.x / C::T)};
   const int j = t.s;
 
@@ -492,196 +518,147 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
   const bool conj_tab = a.conj_tab != 0;
   const bool real = a.in_real != 0;
 
-  // item sequence of this workgroup
-  Cursor cur;
-  if constexpr (ACC) {
-    cur = Cursor{rank % a.ntiles, rank / a.ntiles, 0};
-  } else {
-    cur = Cursor{rank % a.ntiles, rank / a.ntiles, rank};
-  }
-  auto advance = [&](const Cursor& c) {
-    if constexpr (ACC) {
-      return Cursor{c.tile, c.b + a.lanes, 0};
-    } else {
-      const int it = c.item + a.workers;
-      return Cursor{it % a.ntiles, it / a.ntiles, it};
-    }
-  };
-  auto has = [&](const Cursor& c) {
-    if constexpr (ACC) {
-      return c.b < a.batch;
-    } else {
-      return c.item < total;
-    }
-  };
-  auto src = [&](int b) -> const char* {
-    return static_cast<const char*>(a.in) + (size_t)b * nn * (real ? sizeof(float) : sizeof(float2));
-  };
-
   float acc[ACC ? N1 : 1];
   if constexpr (ACC) {
     static_for<0, N1>([&](auto k) { acc[k.value] = 0.f; });
   }
   stage_table_by_freq<C>(lds, a.tab);  // visible after the first barrier below
 
-  int vec0 = cur.tile * C::T;
-  int vec = vec0 + t.v;
-  int nvalid = min(C::T, a.nvec - vec0);
-  bool vok = t.v < nvalid;
+  // One 1-D propagation of the A-items in v, in place: A-step, B-step with
+  // the staged table (conjugated when cj), inverse A-step.  mid() runs
+  // between the shared-memory writes and the B-step (loads issued there
+  // arrive during it).
+  auto prop = [&](float2(&v)[N1], bool cj, auto&& mid) {
+    Dft<N1, -1>::run(v);
+    write_a(t, j, v);
+    mid();
+    __syncthreads();
+    b_spectral(t, cj);
+    __syncthreads();
+    read_a(t, j, v);
+    Dft<N1, 1>::run(v);
+  };
+  auto nothing = [] {};
 
-  // Column tiles keep an item's output in registers and store it after the
-  // next item's first A-step: stores count in the same vector-memory counter
-  // as loads, so a store issued right before the wait for the prefetched
-  // field would make that wait cover its completion as well.
-  constexpr bool DEFER = PREFETCH && DIRECT && KIND != kBwdLast;
-  float2 xout[DEFER ? N1 : 1];
-  bool pending = false;
-  int pend_b = 0;
-  int pend_vec = 0;
-  bool pend_vok = false;
-  auto store_pending = [&]() {
-    if constexpr (DEFER) {
-      __builtin_amdgcn_sched_barrier(0);  // after the A-step, not hoisted above the wait for the field
-      if (pending) store_a_direct<C>(a.out + (size_t)pend_b * nn, n, n, off, pend_vec, pend_vok, xout);
-      __builtin_amdgcn_sched_barrier(0);
+  // Adjoint column kinds load one input of their next item into pf as soon
+  // as registers are free for it, so it arrives while the current item is
+  // still being transformed: kBwdMid loads W_{l-1} during its last
+  // propagation (after the dphi update), kBwdLast, which has no third
+  // propagation, transforms G first and loads the next G while W_0
+  // propagates.  After the last item the current one is loaded again,
+  // unused: an unconditional load keeps the live ranges simple.  (The
+  // forward kinds, one item per workgroup, rely on the other resident
+  // workgroups instead.)
+  constexpr bool PREFETCH = DIRECT && ACC;
+  constexpr bool G_FIRST = DIRECT && KIND == kBwdLast;
+  float2 pf[PREFETCH ? N1 : 1];
+  auto issue_next = [&](int item) {
+    if constexpr (PREFETCH) {
+      const int v0 = (item % a.ntiles) * C::T;
+      const float2* src = G_FIRST ? static_cast<const float2*>(a.in) : a.act_in;
+      load_a_direct<C>(src + (size_t)(item / a.ntiles) * nn, n, n, off, v0 + t.v, t.v < min(C::T, a.nvec - v0), pf);
     }
   };
+  if (rank < total) issue_next(rank);
 
-  // prefetched input of the current item
-  float2 xin[PREFETCH && DIRECT ? N1 : 1];
-  TileBuf<C, AXIS> buf;
-  bool live = has(cur);
-  if constexpr (PREFETCH) {
-    if (live) {
-      if constexpr (DIRECT) {
-        load_a_direct<C>(static_cast<const float2*>(a.in) + (size_t)cur.b * nn, n, n, off, vec, vok, xin);
-      } else {
-        tile_issue<C, AXIS>(buf, src(cur.b), real, n, Consecutive{vec0}, nvalid);
-      }
-    }
-  }
-
-  while (live) {
-    const Cursor nxt = advance(cur);
-    const bool more = has(nxt);
-    const int nvec0 = nxt.tile * C::T;
-    const int nvalid_n = min(C::T, a.nvec - nvec0);
-    // Issue the next item's loads, once its registers are free.  After the
-    // last item the current one is loaded again (unused), so the buffer is
-    // always overwritten and its previous contents are dead from the copy on.
-    auto prefetch = [&]() {
+  for (int it = rank; it < total; it += a.workers) {
+    const int tile = it % a.ntiles;
+    const int b = it / a.ntiles;
+    const int vec0 = tile * C::T;
+    const int vec = vec0 + t.v;
+    const int nvalid = min(C::T, a.nvec - vec0);
+    const bool vok = t.v < nvalid;
+    const float2* __restrict__ fin = static_cast<const float2*>(a.in) + (size_t)b * nn;
+    auto prefetch = [&] {
       if constexpr (PREFETCH) {
-        __builtin_amdgcn_sched_barrier(0);
-        const int pb = more ? nxt.b : cur.b;
-        const int pv0 = more ? nvec0 : vec0;
-        const int pnv = more ? nvalid_n : nvalid;
-        if constexpr (DIRECT) {
-          load_a_direct<C>(static_cast<const float2*>(a.in) + (size_t)pb * nn, n, n, off, pv0 + t.v, t.v < pnv,
-                           xin);
-        } else {
-          tile_issue<C, AXIS>(buf, src(pb), real, n, Consecutive{pv0}, pnv);
-        }
+        __builtin_amdgcn_sched_barrier(0);  // not hoisted above the last use of the registers it reuses
+        issue_next(it + a.workers < total ? it + a.workers : it);
       }
     };
-    const int b = cur.b;
 
     float2 x[N1];
-    __syncthreads();  // shared memory reuse across items
-    if constexpr (PREFETCH && DIRECT) {
-      static_for<0, N1>([&](auto k) { x[k.value] = xin[k.value]; });
-    } else if constexpr (PREFETCH) {
-      tile_commit<C, AXIS>(lds, buf, real, n, off, nvalid);
-      __syncthreads();
-      read_a(t, j, x);
-    } else if constexpr (DIRECT) {
-      load_a_direct<C>(static_cast<const float2*>(a.in) + (size_t)b * nn, n, n, off, vec, vok, x);
-    } else {
-      load_tile<C, AXIS>(lds, src(b), real, n, off, Consecutive{vec0}, nvalid);
-      __syncthreads();
-      read_a(t, j, x);
-    }
-    Dft<N1, -1>::run(x);
-    write_a(t, j, x);
-    store_pending();  // after the A-step's shared-memory writes, which need the field loads
-    if constexpr (!TWO) prefetch();  // the field registers are free from here on
-
-    // per-element layer data, loaded now so it arrives during the B-step:
-    // modulation gamma*exp(j*phi_l) and (backward) the saved activation U_l
-    float2 m[TWO ? N1 : 1];
-    float2 ul[ACC ? N1 : 1];
-    if constexpr (TWO || ACC) {
-      const float2* __restrict__ ai = ACC ? a.act_in + (size_t)b * nn : nullptr;
-      for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
-        if constexpr (TWO) m[k.value] = in ? ld(a.mod, idx) : c2(0.f, 0.f);
-        if constexpr (ACC) ul[k.value] = in ? ld_stream(ai, idx) : c2(0.f, 0.f);
-      });
-    }
-    __syncthreads();
-    b_spectral(t, conj_tab);
-    __syncthreads();
-    read_a(t, j, x);
-    Dft<N1, 1>::run(x);
-
-    if constexpr (TWO) {
-      if constexpr (KIND == kFwdMid) {
-        float2* __restrict__ ao = a.act_out ? a.act_out + (size_t)b * nn : nullptr;
-        static_for<0, N1>([&](auto k) {
-          const float2 u = cmul(x[k.value], m[k.value]);  // zero outside the aperture (crop)
-          x[k.value] = u;
-        });
-        if (ao) {
-          for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
-            if (in) st_stream(ao, idx, x[k.value]);
-          });
-        }
+    if constexpr (G_FIRST) {
+      // G_1 = adjoint of the first-axis half of hop 2, while W_0 is in flight
+      float2 ar[N1];
+      static_for<0, N1>([&](auto k) { x[k.value] = pf[k.value]; });
+      load_a_direct<C>(a.act_in + (size_t)b * nn, n, n, off, vec, vok, ar);
+      float2 m[N1];
+      prop(x, true, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+      static_for<0, N1>([&](auto k) { x[k.value] = cmulc(x[k.value], m[k.value]); });
+      // A_1, then dphi_1 += Im(conj(A_1) conj(M_1) G_1)
+      prop(ar, false, prefetch);
+      static_for<0, N1>([&](auto k) { acc[k.value] += ar[k.value].x * x[k.value].y - ar[k.value].y * x[k.value].x; });
+    } else if constexpr (ACC) {
+      // A_l from the saved input of the forward pass, while G (the gradient
+      // with respect to W_l) is in flight
+      float2 ar[N1];
+      if constexpr (DIRECT) {
+        static_for<0, N1>([&](auto k) { ar[k.value] = pf[k.value]; });
+        load_a_direct<C>(fin, n, n, off, vec, vok, x);
+        prop(ar, false, nothing);
       } else {
-        static_for<0, N1>([&](auto k) {
-          const float2 g = x[k.value];
-          acc[k.value] += ul[k.value].x * g.y - ul[k.value].y * g.x;  // Im(conj(U_l) * G)
-          x[k.value] = cmulc(g, m[k.value]);
-        });
+        __syncthreads();  // shared memory reuse across items
+        load_tile<C, AXIS>(lds, a.act_in + (size_t)b * nn, false, n, off, Consecutive{vec0}, nvalid);
+        __syncthreads();
+        read_a(t, j, ar);
+        prop(ar, false, nothing);
+        __syncthreads();
+        load_tile<C, AXIS>(lds, fin, false, n, off, Consecutive{vec0}, nvalid);
+        __syncthreads();
+        read_a(t, j, x);
       }
-      prefetch();  // the modulation (and activation) registers are free from here on
-      Dft<N1, -1>::run(x);
-      write_a(t, j, x);
-      __syncthreads();
-      b_spectral(t, conj_tab);
-      __syncthreads();
-      read_a(t, j, x);
-      Dft<N1, 1>::run(x);
-    }
-
-    if constexpr (KIND == kBwdLast) {
-      static_for<0, N1>([&](auto k) { acc[k.value] += ul[k.value].x * x[k.value].y - ul[k.value].y * x[k.value].x; });
-    } else if constexpr (DEFER) {
-      static_for<0, N1>([&](auto k) { xout[k.value] = x[k.value]; });
-      pending = true;
-      pend_b = b;
-      pend_vec = vec;
-      pend_vok = vok;
-    } else if constexpr (DIRECT) {
-      store_a_direct<C>(a.out + (size_t)b * nn, n, n, off, vec, vok, x);
+      // G_l = adjoint of the first-axis half of hop l+1; the modulation is
+      // loaded during its B-step
+      float2 m[N1];
+      prop(x, true, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+      // conj(M_l) G_l (zero outside the aperture) and dphi_l += Im(conj(U_l) G_l) = Im(conj(A_l) conj(M_l) G_l)
+      static_for<0, N1>([&](auto k) {
+        const float2 h = cmulc(x[k.value], m[k.value]);
+        acc[k.value] += ar[k.value].x * h.y - ar[k.value].y * h.x;
+        x[k.value] = h;
+      });
+      if constexpr (KIND == kBwdMid) {
+        prop(x, true, prefetch);
+      } else {
+        prefetch();
+      }
     } else {
-      write_a(t, j, x);
-      __syncthreads();
-      store_tile<C, AXIS>(lds, a.out + (size_t)b * nn, n, off, Consecutive{vec0}, nvalid);
+      if constexpr (DIRECT) {
+        load_a_direct<C>(fin, n, n, off, vec, vok, x);
+      } else {
+        __syncthreads();  // shared memory reuse across items
+        load_tile<C, AXIS>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * (real ? 4 : 8), real, n, off,
+                           Consecutive{vec0}, nvalid);
+        __syncthreads();
+        read_a(t, j, x);
+      }
+      if constexpr (KIND == kFwdMid) {
+        float2 m[N1];
+        prop(x, conj_tab, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+        // U_l = M_l A_l, zero outside the aperture (crop)
+        static_for<0, N1>([&](auto k) { x[k.value] = cmul(x[k.value], m[k.value]); });
+      }
+      prop(x, conj_tab, prefetch);
     }
 
-    live = more;
-    if (more) {
-      cur = nxt;
-      vec0 = nvec0;
-      vec = vec0 + t.v;
-      nvalid = nvalid_n;
-      vok = t.v < nvalid;
+    if constexpr (KIND != kBwdLast) {
+      if constexpr (DIRECT) {
+        store_a_direct<C>(a.out + (size_t)b * nn, n, n, off, vec, vok, x);
+      } else {
+        write_a(t, j, x);
+        __syncthreads();
+        store_tile<C, AXIS>(lds, a.out + (size_t)b * nn, n, off, Consecutive{vec0}, nvalid);
+      }
     }
   }
-  store_pending();
   if constexpr (ACC) {
-    // one partial per lane; a lane with no samples contributes zeros
-    float* __restrict__ dp = a.dphi_part + (size_t)(rank / a.ntiles) * nn;
+    // one partial per lane (the tile is fixed); a lane with no samples contributes zeros
+    const int vec0 = (rank % a.ntiles) * C::T;
+    const int vec = vec0 + t.v;
+    const bool vok = t.v < min(C::T, a.nvec - vec0);
+    const Rsrc dp = make_rsrc(a.dphi_part + (size_t)(rank / a.ntiles) * nn, (unsigned)nn * 4u);
     for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
-      if (in) st(dp, idx, acc[k.value]);
+      bstore_f(dp, in ? (unsigned)idx * 4u : kOutOfRange, acc[k.value]);
     });
   }
 }
@@ -1058,7 +1035,6 @@ struct LayerTile {
   static constexpr int T = TileT<N>::T;
 };
 template <> struct LayerTile<200, kFwdMid, kCol> { static constexpr int T = 24; };
-template <> struct LayerTile<200, kBwdLast, kCol> { static constexpr int T = 24; };
 
 template <int N, int KIND, int AXIS>
 using LayerCfg = Cfg<std::conditional_t<AXIS == kRow, typename RowPlanFor<N>::type, typename PlanFor<N>::type>,

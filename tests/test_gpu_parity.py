@@ -161,9 +161,6 @@ def test_forward_n200_strokes(lrb, layers, gamma):
     assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
     assert rel(host(out["field"]), ref["field"]) < TOL_FIELD
     assert rel(host(out["intensity"]), ref["intensity"]) < TOL_FIELD
-    for layer in range(1, layers + 1):
-        act = host(net.saved_activation(saved, 6, layer))
-        assert rel(act, ref["acts"][layer - 1]) < TOL_FIELD
 
 
 def test_forward_angular_spectrum_padded(lrb):
