@@ -130,23 +130,29 @@ __device__ __forceinline__ void zero_padding(float2* lds, int n, int off) {
 
 // ---------------------------------------------------------------------------
 // Batched tile walks.  A tile has nvalid vectors of n elements (positions
-// q < n; shared-memory position q + off).  Each visited element is passed to
-// the callbacks as (i, v, q, li): i the compile-time buffer index inside the
-// current chunk, v the tile vector, q the position, li its shared-memory index.
+// q < n; shared-memory position q + off).  The callbacks receive
+// (i, v, q, li, ok): i the compile-time buffer index inside the current
+// chunk, v the tile vector, q the position, li its shared-memory index and
+// ok whether (v, q) is an element of the tile.
 //
 //   row tiles (whole rows per wave):  wave w moves rows v = w, w + NW, ... and
 //     its lanes cover positions q = lane + 64*m, so every global access of a
 //     wave is one contiguous run of a row and the shared-memory index of each
-//     (lane, m) is a per-lane constant plus v;
-//   column tiles: thread tid handles elements e = tid + i*P, i < N1, with
-//     (v, q) = (e mod T, e div T): every access of a wave covers T consecutive
-//     columns of a few rows.
+//     (lane, m) is a per-lane constant plus v.  Every (row, run) slot is
+//     visited, without branches: for slots outside the tile ok is false, li
+//     is the spare shared-memory row (position q >= n) or an unused vector of
+//     the tile (v >= nvalid), and global accesses take kOutOfRange;
+//   other tiles (column tiles, rows that do not split evenly over the
+//     waves): only elements of the tile are visited (ok is true); column
+//     thread tid handles elements e = tid + i*P, i < N1, with
+//     (v, q) = (e mod T, e div T): every access of a wave covers T
+//     consecutive columns of a few rows.
 //
 // The walk runs in chunks of at most W elements per thread: first() is
 // called for the whole chunk (issue loads), then second() (consume them).
 // Loads use one chunk (every load of the thread in flight before the first
-// wait); stores, which do not wait, use small chunks.  Only valid elements
-// are visited.  WalkShape<C, AXIS, W>::BUF is the buffer length a chunk needs.
+// wait); stores, which do not wait, use small chunks.
+// WalkShape<C, AXIS, W>::BUF is the buffer length a chunk needs.
 // ---------------------------------------------------------------------------
 template <class C>
 struct RowLanes {
@@ -179,9 +185,11 @@ __device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& firs
     const int lane = tid & 63;
     const int wv = tid >> 6;
     int lofs[RL::NCH];  // shared-memory index of position lane + 64*m in tile vector 0
+    bool qok[RL::NCH];
     static_for<0, RL::NCH>([&](auto m) {
       const int q = lane + 64 * decltype(m)::value;
-      lofs[m.value] = q < n ? lds_index<C>(q + off, 0) : 0;
+      qok[m.value] = q < n;
+      lofs[m.value] = q < n ? lds_index<C>(q + off, 0) : C::SPARE;
     });
     static_for<0, WS::NCHUNK>([&](auto c) {
       auto visit = [&](auto& f) {
@@ -189,15 +197,12 @@ __device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& firs
           constexpr int r = decltype(c)::value * WS::RCH + decltype(rr)::value;
           if constexpr (r < RL::RPW) {
             const int v = wv + RL::NW * r;
-            if (v < nvalid) {
-              static_for<0, RL::NCH>([&](auto m) {
-                const int q = lane + 64 * decltype(m)::value;
-                if (q < n) {
-                  f(std::integral_constant<int, decltype(rr)::value * RL::NCH + decltype(m)::value>{}, v, q,
-                    lofs[m.value] + v);
-                }
-              });
-            }
+            const bool vok = v < nvalid;
+            static_for<0, RL::NCH>([&](auto m) {
+              const int q = lane + 64 * decltype(m)::value;
+              f(std::integral_constant<int, decltype(rr)::value * RL::NCH + decltype(m)::value>{}, v, q,
+                lofs[m.value] + v, vok && qok[m.value]);
+            });
           }
         });
       };
@@ -218,7 +223,7 @@ __device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& firs
         static_for<0, WS::CH>([&](auto i) {
           constexpr int ii = decltype(c)::value * WS::CH + decltype(i)::value;
           if constexpr (ii < C::N1) {
-            if (tid + ii * C::P < total) f(i, v, q, lds_index<C>(q + off, v));
+            if (tid + ii * C::P < total) f(i, v, q, lds_index<C>(q + off, v), true);
             q += dq;
             v += dv;
             if (q >= n) { q -= n; ++v; }
@@ -238,7 +243,7 @@ __device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& firs
             const int e = tid + ii * C::P;
             const int q = e / C::T;
             const int v = e - q * C::T;
-            if (q < n && v < nvalid) f(i, v, q, lds_index<C>(q + off, v));
+            if (q < n && v < nvalid) f(i, v, q, lds_index<C>(q + off, v), true);
           }
         });
       };
@@ -250,25 +255,35 @@ __device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& firs
 
 constexpr int kStoreChunk = 8;
 
-// Load a tile of complex (or real) natural-layout rows/columns into shared
-// memory.  Tile vector v is field row/column vf(v).
+// Byte offset of element (vector vf(v), position q) of an n x n field, or
+// kOutOfRange outside the tile.
+template <int AXIS, int BYTES>
+__device__ __forceinline__ unsigned elem_off(bool ok, int n, int vec, int q) {
+  return ok ? (unsigned)nat_index<AXIS>(n, vec, q) * (unsigned)BYTES : kOutOfRange;
+}
+
+// Load a tile of complex (or real) natural-layout rows/columns of an n x n
+// field (src, wave-uniform) into shared memory.  Tile vector v is field
+// row/column vf(v).
 template <class C, int AXIS, class VF>
 __device__ __forceinline__ void load_tile(float2* lds, const void* src, bool real, int n, int off, VF&& vf,
                                           int nvalid) {
   zero_padding<C>(lds, n, off);
   constexpr int BUF = WalkShape<C, AXIS, kAll>::BUF;
   if (real) {
+    // (real input: loads masked per lane; 4-byte buffer loads over the whole
+    // row runs measured slower here)
     const float* __restrict__ in = static_cast<const float*>(src);
     float buf[BUF];
     tile_walk2<C, AXIS, kAll>(n, off, nvalid,
-        [&](auto i, int v, int q, int) { buf[i.value] = ld(in, nat_index<AXIS>(n, vf(v), q)); },
-        [&](auto i, int, int, int li) { lds[li] = c2(buf[i.value], 0.f); });
+        [&](auto i, int v, int q, int, bool ok) { buf[i.value] = ok ? ld(in, nat_index<AXIS>(n, vf(v), q)) : 0.f; },
+        [&](auto i, int, int, int li, bool) { lds[li] = c2(buf[i.value], 0.f); });
   } else {
-    const float2* __restrict__ in = static_cast<const float2*>(src);
+    const Rsrc r = make_rsrc(src, (unsigned)(n * n) * 8u);
     float2 buf[BUF];
     tile_walk2<C, AXIS, kAll>(n, off, nvalid,
-        [&](auto i, int v, int q, int) { buf[i.value] = ld(in, nat_index<AXIS>(n, vf(v), q)); },
-        [&](auto i, int, int, int li) { lds[li] = buf[i.value]; });
+        [&](auto i, int v, int q, int, bool ok) { buf[i.value] = bload(r, elem_off<AXIS, 8>(ok, n, vf(v), q)); },
+        [&](auto i, int, int, int li, bool) { lds[li] = buf[i.value]; });
   }
 }
 
@@ -283,13 +298,13 @@ __device__ __forceinline__ void tile_issue(TileBuf<C, AXIS>& buf, const void* sr
   if (real) {
     const float* __restrict__ in = static_cast<const float*>(src);
     tile_walk2<C, AXIS, kAll>(n, 0, nvalid,
-        [&](auto i, int v, int q, int) { buf[i.value].x = ld(in, nat_index<AXIS>(n, vf(v), q)); },
-        [](auto, int, int, int) {});
+        [&](auto i, int v, int q, int, bool ok) { buf[i.value].x = ok ? ld(in, nat_index<AXIS>(n, vf(v), q)) : 0.f; },
+        [](auto, int, int, int, bool) {});
   } else {
-    const float2* __restrict__ in = static_cast<const float2*>(src);
+    const Rsrc r = make_rsrc(src, (unsigned)(n * n) * 8u);
     tile_walk2<C, AXIS, kAll>(n, 0, nvalid,
-        [&](auto i, int v, int q, int) { buf[i.value] = ld(in, nat_index<AXIS>(n, vf(v), q)); },
-        [](auto, int, int, int) {});
+        [&](auto i, int v, int q, int, bool ok) { buf[i.value] = bload(r, elem_off<AXIS, 8>(ok, n, vf(v), q)); },
+        [](auto, int, int, int, bool) {});
   }
 }
 template <class C, int AXIS>
@@ -297,11 +312,11 @@ __device__ __forceinline__ void tile_commit(float2* lds, const TileBuf<C, AXIS>&
                                             int nvalid) {
   zero_padding<C>(lds, n, off);
   if (real) {
-    tile_walk2<C, AXIS, kAll>(n, off, nvalid, [](auto, int, int, int) {},
-        [&](auto i, int, int, int li) { lds[li] = c2(buf[i.value].x, 0.f); });
+    tile_walk2<C, AXIS, kAll>(n, off, nvalid, [](auto, int, int, int, bool) {},
+        [&](auto i, int, int, int li, bool) { lds[li] = c2(buf[i.value].x, 0.f); });
   } else {
-    tile_walk2<C, AXIS, kAll>(n, off, nvalid, [](auto, int, int, int) {},
-        [&](auto i, int, int, int li) { lds[li] = buf[i.value]; });
+    tile_walk2<C, AXIS, kAll>(n, off, nvalid, [](auto, int, int, int, bool) {},
+        [&](auto i, int, int, int li, bool) { lds[li] = buf[i.value]; });
   }
 }
 
@@ -310,7 +325,7 @@ struct Consecutive {
   int vec0;
   __device__ __forceinline__ int operator()(int v) const { return vec0 + v; }
 };
-// Tile vector v is field vector map[v] (shared memory).
+// Tile vector v is field vector map[v] (shared memory, T entries).
 struct Mapped {
   const int* map;
   __device__ __forceinline__ int operator()(int v) const { return map[v]; }
@@ -331,40 +346,48 @@ __device__ __forceinline__ void load_seed(float2* lds, const PassArgs& a, int b,
   float2 buf[BUF];
   float g[BUF];
   tile_walk2<C, AXIS, kAll>(n, off, nvalid,
-      [&](auto i, int v, int q, int) {
-        const int y = AXIS == kRow ? vec0 + v : q;
-        const int x = AXIS == kRow ? q : vec0 + v;
+      [&](auto i, int v, int q, int, bool ok) {
         float gv = 0.f;
-        if (gint) {
-          gv = ld(gint, y * n + x);
-        } else {
-          // dL/dI is dL/dS_k on region k: sum over the regions covering (y, x)
-          unsigned long long mask = ld(a.row_mask, y) & ld(a.col_mask, x);
-          while (mask) {
-            gv += gsum[__builtin_ctzll(mask)];
-            mask &= mask - 1;
+        float2 u = c2(0.f, 0.f);
+        if (ok) {
+          const int y = AXIS == kRow ? vec0 + v : q;
+          const int x = AXIS == kRow ? q : vec0 + v;
+          if (gint) {
+            gv = ld(gint, y * n + x);
+          } else {
+            // dL/dI is dL/dS_k on region k: sum over the regions covering (y, x)
+            unsigned long long mask = ld(a.row_mask, y) & ld(a.col_mask, x);
+            while (mask) {
+              gv += gsum[__builtin_ctzll(mask)];
+              mask &= mask - 1;
+            }
           }
+          if (gv != 0.f) u = ld(ud, y * n + x);
         }
         g[i.value] = gv;
-        buf[i.value] = gv != 0.f ? ld(ud, y * n + x) : c2(0.f, 0.f);
+        buf[i.value] = u;
       },
-      [&](auto i, int, int, int li) { lds[li] = cscale(buf[i.value], 2.f * g[i.value]); });
+      [&](auto i, int, int, int li, bool) { lds[li] = cscale(buf[i.value], 2.f * g[i.value]); });
 }
 
+// Store a tile from shared memory into natural-layout rows/columns of an
+// n x n field (out, wave-uniform).
 template <class C, int AXIS, class VF>
 __device__ __forceinline__ void store_tile(const float2* lds, float2* __restrict__ out, int n, int off, VF&& vf,
                                            int nvalid) {
+  const Rsrc r = make_rsrc(out, (unsigned)(n * n) * 8u);
   float2 buf[WalkShape<C, AXIS, kStoreChunk>::BUF];
   tile_walk2<C, AXIS, kStoreChunk>(n, off, nvalid,
-      [&](auto i, int, int, int li) { buf[i.value] = lds[li]; },
-      [&](auto i, int v, int q, int) { st(out, nat_index<AXIS>(n, vf(v), q), buf[i.value]); });
+      [&](auto i, int, int, int li, bool) { buf[i.value] = lds[li]; },
+      [&](auto i, int v, int q, int, bool ok) { bstore(r, elem_off<AXIS, 8>(ok, n, vf(v), q), buf[i.value]); });
 }
 
-// Zero vectors vf(0..nvalid) of a natural-layout field.
+// Zero vectors vf(0..nvalid) of a natural-layout n x n field.
 template <class C, int AXIS, class VF>
 __device__ __forceinline__ void zero_vectors(float2* __restrict__ out, int n, VF&& vf, int nvalid) {
-  tile_walk2<C, AXIS, kStoreChunk>(n, 0, nvalid, [&](auto, int, int, int) {},
-      [&](auto, int v, int q, int) { st(out, nat_index<AXIS>(n, vf(v), q), c2(0.f, 0.f)); });
+  const Rsrc r = make_rsrc(out, (unsigned)(n * n) * 8u);
+  tile_walk2<C, AXIS, kStoreChunk>(n, 0, nvalid, [&](auto, int, int, int, bool) {},
+      [&](auto, int v, int q, int, bool ok) { bstore(r, elem_off<AXIS, 8>(ok, n, vf(v), q), c2(0.f, 0.f)); });
 }
 
 // Detector-plane outputs from a tile that holds U_D in natural order:
@@ -386,12 +409,14 @@ __device__ __forceinline__ void tile_outputs(const float2* lds, float* rsum, con
   if (fo || sv || io) {
     float2 buf[WalkShape<C, AXIS, kStoreChunk>::BUF];
     tile_walk2<C, AXIS, kStoreChunk>(n, off, nvalid,
-        [&](auto i, int, int, int li) { buf[i.value] = lds[li]; },
-        [&](auto i, int v, int q, int) {
-          const int idx = nat_index<AXIS>(n, vf(v), q);
-          if (fo) st(fo, idx, buf[i.value]);
-          if (sv) st(sv, idx, buf[i.value]);
-          if (io) st(io, idx, cabs2(buf[i.value]));
+        [&](auto i, int, int, int li, bool) { buf[i.value] = lds[li]; },
+        [&](auto i, int v, int q, int, bool ok) {
+          if (ok) {
+            const int idx = nat_index<AXIS>(n, vf(v), q);
+            if (fo) st(fo, idx, buf[i.value]);
+            if (sv) st(sv, idx, buf[i.value]);
+            if (io) st(io, idx, cabs2(buf[i.value]));
+          }
         });
   }
   if (a.sums_part) {
@@ -549,14 +574,20 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
   // unused: an unconditional load keeps the live ranges simple.  (The
   // forward kinds, one item per workgroup, rely on the other resident
   // workgroups instead.)
-  constexpr bool PREFETCH = DIRECT && ACC;
+  constexpr bool PREFETCH = ACC && (DIRECT || KIND == kBwdMid);
   constexpr bool G_FIRST = DIRECT && KIND == kBwdLast;
-  float2 pf[PREFETCH ? N1 : 1];
+  float2 pf[PREFETCH && DIRECT ? N1 : 1];
+  TileBuf<C, AXIS> pft;  // row tiles
   auto issue_next = [&](int item) {
     if constexpr (PREFETCH) {
       const int v0 = (item % a.ntiles) * C::T;
+      const int nv = min(C::T, a.nvec - v0);
       const float2* src = G_FIRST ? static_cast<const float2*>(a.in) : a.act_in;
-      load_a_direct<C>(src + (size_t)(item / a.ntiles) * nn, n, n, off, v0 + t.v, t.v < min(C::T, a.nvec - v0), pf);
+      if constexpr (DIRECT) {
+        load_a_direct<C>(src + (size_t)(item / a.ntiles) * nn, n, n, off, v0 + t.v, t.v < nv, pf);
+      } else {
+        tile_issue<C, AXIS>(pft, src + (size_t)(item / a.ntiles) * nn, false, n, Consecutive{v0}, nv);
+      }
     }
   };
   if (rank < total) issue_next(rank);
@@ -598,7 +629,11 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
         prop(ar, false, nothing);
       } else {
         __syncthreads();  // shared memory reuse across items
-        load_tile<C, AXIS>(lds, a.act_in + (size_t)b * nn, false, n, off, Consecutive{vec0}, nvalid);
+        if constexpr (PREFETCH) {
+          tile_commit<C, AXIS>(lds, pft, false, n, off, nvalid);
+        } else {
+          load_tile<C, AXIS>(lds, a.act_in + (size_t)b * nn, false, n, off, Consecutive{vec0}, nvalid);
+        }
         __syncthreads();
         read_a(t, j, ar);
         prop(ar, false, nothing);
@@ -617,8 +652,10 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
         acc[k.value] += ar[k.value].x * h.y - ar[k.value].y * h.x;
         x[k.value] = h;
       });
-      if constexpr (KIND == kBwdMid) {
+      if constexpr (KIND == kBwdMid && DIRECT) {
         prop(x, true, prefetch);
+      } else if constexpr (KIND == kBwdMid) {
+        prop(x, true, nothing);
       } else {
         prefetch();
       }
@@ -648,6 +685,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
         write_a(t, j, x);
         __syncthreads();
         store_tile<C, AXIS>(lds, a.out + (size_t)b * nn, n, off, Consecutive{vec0}, nvalid);
+        if constexpr (ACC) prefetch();
       }
     }
   }
@@ -1035,6 +1073,9 @@ struct LayerTile {
   static constexpr int T = TileT<N>::T;
 };
 template <> struct LayerTile<200, kFwdMid, kCol> { static constexpr int T = 24; };
+template <> struct LayerTile<200, kPropOnce, kRow> { static constexpr int T = 8; };
+template <> struct LayerTile<200, kFwdMid, kRow> { static constexpr int T = 8; };
+template <> struct LayerTile<200, kBwdMid, kRow> { static constexpr int T = 8; };
 
 template <int N, int KIND, int AXIS>
 using LayerCfg = Cfg<std::conditional_t<AXIS == kRow, typename RowPlanFor<N>::type, typename PlanFor<N>::type>,

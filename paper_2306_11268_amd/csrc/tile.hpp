@@ -25,7 +25,10 @@ struct Cfg {
   static constexpr int TP = T_ + 1;
   static constexpr int IB = (N1 + S - 1) / S;
   static constexpr bool B_FULL = (N1 % S) == 0;
-  static constexpr int LDS_ELEMS = N * TP;
+  // N slots of T+1 entries, then a spare slot that absorbs the shared-memory
+  // writes of walk positions outside the tile
+  static constexpr int SPARE = N * TP;
+  static constexpr int LDS_ELEMS = (N + 1) * TP;
   static constexpr int LDS_BYTES = LDS_ELEMS * 8 + (P / 64) * 4;
   // Waves per SIMD that shared memory (160 KiB per CU) allows; the kernels
   // ask the compiler to fit their registers to this occupancy.
