@@ -673,6 +673,7 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
 
   if (net->approx == LR_FRESNEL) {
     auto chirp = [&](Axis ax) { return at<float2>(d_work, ax == lr::kRow ? L.chirp_x : L.chirp_y); };
+    const unsigned long long* live_rows = nullptr;  // rows of the seed's output the first layer pass reads
     // rest of hop L+1 from the saved W_L, seed at the detector plane, adjoint of that half hop
     {
       PassArgs s = a;
@@ -683,7 +684,11 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
       s.grad_sums = gsum;
       if (gsum) {
         set_detector(s, net->det, L, d_work);
-        restrict_to_regions(s, net->det, L, d_work, ax, lr::tile_shape(N, 0).T, true);
+        // The seed vanishes off the covered rows (columns).  A row seed pass
+        // leaves the other rows unwritten, and the next (column) pass skips
+        // them; a column seed pass writes zero columns for the row pass after it.
+        restrict_to_regions(s, net->det, L, d_work, ax, lr::tile_shape(N, 0).T, ax == lr::kCol);
+        if (ax == lr::kRow) live_rows = at<unsigned long long>(d_work, L.row_mask);
       }
       s.out = w[0];
       LR_TRY(fr_pass(N, lr::kBwdFirst, ax, s, st));
@@ -698,6 +703,7 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
       m.mod = ws_mod + static_cast<size_t>(l - 1) * nn;
       m.act_in = saved + static_cast<size_t>(l - 1) * batch * nn;  // W_{l-1}, input of layer l's forward pass
       m.dphi_part = part_of(l);
+      m.live = l == Lyr ? live_rows : nullptr;
       const lr::PassKind kind = l > 1 ? lr::kBwdMid : lr::kBwdLast;
       LR_TRY(schedule_layer_pass(N, kind, ax, L.groups, m));
       if (l > 1) m.out = w[cur ^ 1];

@@ -62,6 +62,10 @@ struct PassArgs {
   int conj_mod;
   float2* act_out;      // angular-spectrum path: U_l, oriented [B][n][n]
   const float2* act_in; // angular-spectrum path: U_l, oriented; separable path: W_{l-1}, natural [B][n][n]
+  // Adjoint column passes: when not NULL, the input field (G) is zero on the
+  // rows y with live[y] == 0 (rows that no detector region covers, which the
+  // detector-plane seed pass does not write); those rows are not read.
+  const unsigned long long* live;
   float* dphi_part;     // oriented [groups][n][n]
   // detector-plane outputs (natural [B][n][n] layouts)
   float* intensity;

@@ -492,6 +492,16 @@ __device__ __forceinline__ void store_a_direct(float2* __restrict__ out, int pit
     bstore(r, valid ? (unsigned)idx * 8u : kOutOfRange, x[k.value]);
   });
 }
+// As load_a_direct, reading only the elements k with bit k of mask set (the
+// others are zero).
+template <class C>
+__device__ __forceinline__ void load_a_direct_masked(const float2* __restrict__ in, int pitch, int n, int off,
+                                                     int vec, bool vok, unsigned mask, float2 (&x)[C::N1]) {
+  const Rsrc r = make_rsrc(in, (unsigned)(n * pitch) * 8u);
+  for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
+    x[k.value] = bload(r, valid && ((mask >> k.value) & 1u) ? (unsigned)idx * 8u : kOutOfRange);
+  });
+}
 // Per-layer [q][vec] table of n x n entries at this thread's A-item.
 template <class C>
 __device__ __forceinline__ void load_a_table(const float2* __restrict__ tab, int n, int off, int vec, bool vok,
@@ -570,27 +580,39 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
   // still being transformed: kBwdMid loads W_{l-1} during its last
   // propagation (after the dphi update), kBwdLast, which has no third
   // propagation, transforms G first and loads the next G while W_0
-  // propagates.  After the last item the current one is loaded again,
-  // unused: an unconditional load keeps the live ranges simple.  (The
-  // forward kinds, one item per workgroup, rely on the other resident
-  // workgroups instead.)
+  // propagates.  After the last item the loads are still issued (which
+  // keeps the live ranges simple), at out-of-range offsets: they move no
+  // data.  (The forward kinds, one item per workgroup, rely on the other
+  // resident workgroups instead: prefetching within chunks of items measured
+  // slower for them.)
+  // elements of this thread's A-item at which G can be nonzero (column passes)
+  unsigned gmask = ~0u;
+  if constexpr (ACC && DIRECT) {
+    if (a.live) {
+      gmask = 0u;
+      for_a_elems<C>(off, n, 1, 0, true, [&](auto k, int q, bool in) {
+        if (in && ld(a.live, q) != 0ull) gmask |= 1u << k.value;
+      });
+    }
+  }
   constexpr bool PREFETCH = ACC && (DIRECT || KIND == kBwdMid);
   constexpr bool G_FIRST = DIRECT && KIND == kBwdLast;
   float2 pf[PREFETCH && DIRECT ? N1 : 1];
   TileBuf<C, AXIS> pft;  // row tiles
-  auto issue_next = [&](int item) {
+  auto issue_next = [&](int item, bool live) {
     if constexpr (PREFETCH) {
       const int v0 = (item % a.ntiles) * C::T;
-      const int nv = min(C::T, a.nvec - v0);
+      const int nv = live ? min(C::T, a.nvec - v0) : 0;
       const float2* src = G_FIRST ? static_cast<const float2*>(a.in) : a.act_in;
       if constexpr (DIRECT) {
-        load_a_direct<C>(src + (size_t)(item / a.ntiles) * nn, n, n, off, v0 + t.v, t.v < nv, pf);
+        load_a_direct_masked<C>(src + (size_t)(item / a.ntiles) * nn, n, n, off, v0 + t.v, t.v < nv,
+                                G_FIRST ? gmask : ~0u, pf);
       } else {
         tile_issue<C, AXIS>(pft, src + (size_t)(item / a.ntiles) * nn, false, n, Consecutive{v0}, nv);
       }
     }
   };
-  if (rank < total) issue_next(rank);
+  if (rank < total) issue_next(rank, true);
 
   for (int it = rank; it < total; it += a.workers) {
     const int tile = it % a.ntiles;
@@ -603,7 +625,8 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
     auto prefetch = [&] {
       if constexpr (PREFETCH) {
         __builtin_amdgcn_sched_barrier(0);  // not hoisted above the last use of the registers it reuses
-        issue_next(it + a.workers < total ? it + a.workers : it);
+        const bool more = it + a.workers < total;
+        issue_next(more ? it + a.workers : it, more);
       }
     };
 
@@ -625,7 +648,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
       float2 ar[N1];
       if constexpr (DIRECT) {
         static_for<0, N1>([&](auto k) { ar[k.value] = pf[k.value]; });
-        load_a_direct<C>(fin, n, n, off, vec, vok, x);
+        load_a_direct_masked<C>(fin, n, n, off, vec, vok, gmask, x);
         prop(ar, false, nothing);
       } else {
         __syncthreads();  // shared memory reuse across items
@@ -1072,7 +1095,7 @@ template <int N, int KIND, int AXIS>
 struct LayerTile {
   static constexpr int T = TileT<N>::T;
 };
-template <> struct LayerTile<200, kFwdMid, kCol> { static constexpr int T = 24; };
+template <> struct LayerTile<200, kFwdMid, kCol> { static constexpr int T = 32; };
 template <> struct LayerTile<200, kPropOnce, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kFwdMid, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kBwdMid, kRow> { static constexpr int T = 8; };
