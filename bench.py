@@ -34,6 +34,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", type=int, default=3, help="workload id (3 = 5-layer N=200 train, batch 500)")
     ap.add_argument("--batch", type=int, default=None, help="override the batch size")
+    ap.add_argument("--n", type=int, default=None,
+                    help="grid size of a runtime-study variant of the workload (unpadded n x n)")
+    ap.add_argument("--layers", type=int, default=None, help="depth of a runtime-study variant")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-samples", type=int, default=None, help="samples in the oracle timing run")
     ap.add_argument("--copy-calibration", type=int, default=None, metavar="MIB",
@@ -95,14 +98,22 @@ def oracle_baseline(w, batch, amp, phi, labels, min_seconds=10.0):
 
     h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
     det = od.Detector(w.detector.size, tuple(w.detector.y0), tuple(w.detector.x0))
-    # whole passes over the same batch until about 10 s of host work (at most 8 passes)
+
+    def one_pass(b):
+        fwd = od.donn_forward(amp[:b], phi, h, 1.0, det)
+        _, gs = od.softmax_cross_entropy(fwd["sums"], labels[:b])
+        od.donn_backward(fwd, phi, h, 1.0, det, grad_sums=gs)
+
+    # a one-sample probe sizes the sample so that a pass takes at most about
+    # min_seconds; then whole passes until about min_seconds (at most 8)
+    tp = time.perf_counter()
+    one_pass(1)
+    t1 = time.perf_counter() - tp
+    batch = max(1, min(batch, int(min_seconds / max(t1, 1e-6))))
     passes = 0
     t0 = time.perf_counter()
     while True:
-        fwd = od.donn_forward(amp[:batch], phi, h, 1.0, det)
-        _, gs = od.softmax_cross_entropy(fwd["sums"], labels[:batch])
-        od.donn_backward(fwd, phi, h, 1.0, det, grad_sums=gs)
-        del fwd
+        one_pass(batch)
         passes += 1
         dt = time.perf_counter() - t0
         if dt >= min_seconds or passes >= 8:
@@ -134,7 +145,7 @@ def main():
         copy_calibration(args.copy_calibration)
         return
     lb.load()
-    w = wl.WORKLOADS[args.workload]
+    w = wl.scaled(wl.WORKLOADS[args.workload], n=args.n, layers=args.layers)
     if w.kind != "train" or w.grad != "ce":
         raise SystemExit("bench measures the cross-entropy training workload")
     batch = w.batch if args.batch is None else args.batch
@@ -198,12 +209,14 @@ def main():
                 "traffic_unit": "HBM bytes per launch (FETCH_SIZE, WRITE_SIZE scaled by a copy calibration)",
                 "traffic_gbps": round(traffic / avg_s / 1e9, 1) if traffic else None}
 
-    # whole-step algorithmic traffic per sample: forward reads the amplitude (4 n^2), writes every
-    # activation and reads it back once (16 n^2 per layer) and keeps the detector regions of U_D
-    # (0.8 n^2); backward reads the regions and U_L and writes G (16.8 n^2), then per inner layer
-    # reads G and U_l and writes G (24 n^2), and finally reads G and U_1 (16 n^2): (40 L - 10.4) n^2
+    # whole-step algorithmic traffic per sample, the one-pass minimum: forward reads the
+    # amplitude (4 n^2), each layer reads a field and writes one (16 n^2 per layer; the first
+    # writes only), and the last hop reads one (8 n^2): (16 L + 4) n^2; backward reads one field
+    # and writes the detector-plane gradient (16 n^2), each inner layer reads the gradient and one
+    # saved field and writes the gradient (24 n^2), and layer 1 reads two fields (16 n^2):
+    # (24 L + 8) n^2.  Together (40 L + 12) n^2, without the savings of detector pruning.
     nn = w.n * w.n
-    step_bytes = batch * nn * (40.0 * w.layers - 10.4)
+    step_bytes = batch * nn * (40.0 * w.layers + 12.0)
     out = {
         "metric": "DONN samples/sec (5-layer N=200 fwd+bwd) and achieved HBM GB/s vs peak",
         "value": round(value, 1),

@@ -85,14 +85,14 @@ constexpr cdbl unit_root(long long m, long long N, int sign) {
   return cdbl{c, sign * s};
 }
 
-// Table of exp(-2*pi*i*k/N), k < N, as floats.
+// Table of exp(-2*pi*i*k/N), k <= N (entry N repeats entry 0), as floats.
 template <int N>
-struct RootTable { float2 w[N]; };
+struct RootTable { float2 w[N + 1]; };
 
 template <int N>
 constexpr RootTable<N> make_root_table() {
   RootTable<N> t{};
-  for (int k = 0; k < N; ++k) {
+  for (int k = 0; k <= N; ++k) {
     const cdbl z = unit_root(k, N, -1);
     t.w[k].x = static_cast<float>(z.re);
     t.w[k].y = static_cast<float>(z.im);

@@ -265,6 +265,7 @@ bool fft_size_supported(int N) {
     case 200:
     case 256:
     case 400:
+    case 500:
     case 512:
     case 1000:
     case 1024:
@@ -282,6 +283,7 @@ TileShape tile_shape(int N, int) {
     case 200: return shape_n<200>();
     case 256: return shape_n<256>();
     case 400: return shape_n<400>();
+    case 500: return shape_n<500>();
     case 512: return shape_n<512>();
     case 1000: return shape_n<1000>();
     case 1024: return shape_n<1024>();
@@ -297,6 +299,7 @@ hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& 
     case 200: return launch_fr_n<200>(kind, axis, a, st);
     case 256: return launch_fr_n<256>(kind, axis, a, st);
     case 400: return launch_fr_n<400>(kind, axis, a, st);
+    case 500: return launch_fr_n<500>(kind, axis, a, st);
     case 512: return launch_fr_n<512>(kind, axis, a, st);
     case 1000: return launch_fr_n<1000>(kind, axis, a, st);
     case 1024: return launch_fr_n<1024>(kind, axis, a, st);
@@ -312,6 +315,7 @@ int fresnel_pass_tile(int N, PassKind kind, Axis axis) {
     case 200: return tile_fr_n<200>(kind, axis);
     case 256: return tile_fr_n<256>(kind, axis);
     case 400: return tile_fr_n<400>(kind, axis);
+    case 500: return tile_fr_n<500>(kind, axis);
     case 512: return tile_fr_n<512>(kind, axis);
     case 1000: return tile_fr_n<1000>(kind, axis);
     case 1024: return tile_fr_n<1024>(kind, axis);
@@ -327,6 +331,7 @@ int fresnel_pass_slots(int N, PassKind kind, Axis axis) {
     case 200: return slots_fr_n<200>(kind, axis);
     case 256: return slots_fr_n<256>(kind, axis);
     case 400: return slots_fr_n<400>(kind, axis);
+    case 500: return slots_fr_n<500>(kind, axis);
     case 512: return slots_fr_n<512>(kind, axis);
     case 1000: return slots_fr_n<1000>(kind, axis);
     case 1024: return slots_fr_n<1024>(kind, axis);
@@ -342,6 +347,7 @@ hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t
     case 200: return launch_as_n<200>(kind, a, st);
     case 256: return launch_as_n<256>(kind, a, st);
     case 400: return launch_as_n<400>(kind, a, st);
+    case 500: return launch_as_n<500>(kind, a, st);
     case 512: return launch_as_n<512>(kind, a, st);
     case 1000: return launch_as_n<1000>(kind, a, st);
     case 1024: return launch_as_n<1024>(kind, a, st);
@@ -358,6 +364,7 @@ hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, hipStream_t 
     case 200: return prep_as_n<200>(H, Hp, st);
     case 256: return prep_as_n<256>(H, Hp, st);
     case 400: return prep_as_n<400>(H, Hp, st);
+    case 500: return prep_as_n<500>(H, Hp, st);
     case 512: return prep_as_n<512>(H, Hp, st);
     case 1000: return prep_as_n<1000>(H, Hp, st);
     case 1024: return prep_as_n<1024>(H, Hp, st);

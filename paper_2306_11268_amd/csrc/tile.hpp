@@ -74,22 +74,34 @@ __device__ __forceinline__ void write_b(const Tile<C>& t, int k1, const float2 (
   static_for<0, C::N2>([&](auto j) { p[j.value * C::TP] = y[j.value]; });
 }
 
-// Forward half of the B-step: twiddles (Cooley-Tukey only), then DFT over j.
+// Root exp(-2*pi*i*m/N), m <= N, read at a 32-bit offset from the table's
+// uniform base (one address register per load, nothing to keep live).
+template <int N>
+__device__ __forceinline__ float2 root_at(unsigned m) {
+  return *reinterpret_cast<const float2*>(reinterpret_cast<const char*>(Roots<N>::table.w) + m * 8u);
+}
+
+// Forward half of the B-step: twiddles exp(-2*pi*i*k1*j/N) (Cooley-Tukey
+// only), then DFT over j.
 template <class C>
 __device__ __forceinline__ void b_forward(int k1, float2 (&y)[C::N2]) {
   using PL = typename C::Plan;
   if constexpr (!PL::PFA) {
-    static_for<1, C::N2>([&](auto j) { y[j.value] = cmul(y[j.value], PL::twiddle(k1, j.value)); });
+    static_for<1, C::N2>([&](auto j) { y[j.value] = cmul(y[j.value], root_at<C::N>((unsigned)(k1 * j.value))); });
   }
   Dft<C::N2, -1>::run(y);
 }
-// Inverse half of the B-step: inverse DFT over k2, then conjugate twiddles.
+// Inverse half of the B-step: inverse DFT over k2, then the conjugate
+// twiddles, read from the mirrored entries N - k1*j (different addresses, so
+// they are loaded where they are used instead of being kept live from the
+// forward half).
 template <class C>
 __device__ __forceinline__ void b_inverse(int k1, float2 (&y)[C::N2]) {
   using PL = typename C::Plan;
   Dft<C::N2, 1>::run(y);
   if constexpr (!PL::PFA) {
-    static_for<1, C::N2>([&](auto j) { y[j.value] = cmulc(y[j.value], PL::twiddle(k1, j.value)); });
+    static_for<1, C::N2>(
+        [&](auto j) { y[j.value] = cmul(y[j.value], root_at<C::N>((unsigned)(C::N - k1 * j.value))); });
   }
 }
 
@@ -116,24 +128,49 @@ __device__ __forceinline__ void stage_table_by_freq(float2* lds, const float2* _
 // B-step "forward, multiply by the staged per-frequency table, inverse" used
 // by every propagation; conj selects conj(table).  The items of a thread are
 // unrolled so their shared-memory reads overlap.
+// One B-item of the spectral B-step.  For long items (N2 >= 16) scheduling
+// barriers keep each phase's loads (data, twiddles, table) next to their
+// use: hoisted to the front, they kept 3*N2 complex values live at once.
+template <class C>
+__device__ __forceinline__ void b_spectral_item(const Tile<C>& t, int k1, bool conj_tab) {
+  constexpr bool FENCE = C::N2 >= 16;
+  auto fence = [] {
+    if constexpr (FENCE) __builtin_amdgcn_sched_barrier(0);
+  };
+  float2 y[C::N2];
+  read_b(t, k1, y);
+  b_forward<C>(k1, y);
+  fence();
+  const float2* tk = t.lds + (C::N2 * k1) * C::TP + C::T;
+  if (conj_tab) {
+    static_for<0, C::N2>([&](auto k) { y[k.value] = cmulc(y[k.value], tk[k.value * C::TP]); });
+  } else {
+    static_for<0, C::N2>([&](auto k) { y[k.value] = cmul(y[k.value], tk[k.value * C::TP]); });
+  }
+  fence();
+  b_inverse<C>(k1, y);
+  fence();
+  write_b(t, k1, y);
+}
 template <class C>
 __device__ __forceinline__ void b_spectral(const Tile<C>& t, bool conj_tab) {
-  static_for<0, C::IB>([&](auto ic) {
-    const int k1 = t.s + C::S * decltype(ic)::value;
-    if (C::B_FULL || k1 < C::N1) {
-      float2 y[C::N2];
-      read_b(t, k1, y);
-      b_forward<C>(k1, y);
-      const float2* tk = t.lds + (C::N2 * k1) * C::TP + C::T;
-      if (conj_tab) {
-        static_for<0, C::N2>([&](auto k) { y[k.value] = cmulc(y[k.value], tk[k.value * C::TP]); });
-      } else {
-        static_for<0, C::N2>([&](auto k) { y[k.value] = cmul(y[k.value], tk[k.value * C::TP]); });
-      }
-      b_inverse<C>(k1, y);
-      write_b(t, k1, y);
+  // The B-item index behind an empty asm statement: twiddle offsets derived
+  // from it are formed here, not hoisted out of the caller's loops.
+  int s = t.s;
+  asm volatile("" : "+v"(s));
+  if constexpr (C::N2 >= 16) {
+    // long B-items: one at a time, so that their registers are not doubled
+#pragma unroll 1
+    for (int ic = 0; ic < C::IB; ++ic) {
+      const int k1 = s + C::S * ic;
+      if (C::B_FULL || k1 < C::N1) b_spectral_item(t, k1, conj_tab);
     }
-  });
+  } else {
+    static_for<0, C::IB>([&](auto ic) {
+      const int k1 = s + C::S * decltype(ic)::value;
+      if (C::B_FULL || k1 < C::N1) b_spectral_item(t, k1, conj_tab);
+    });
+  }
 }
 
 // ---- reductions ------------------------------------------------------------

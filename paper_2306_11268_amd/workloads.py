@@ -114,14 +114,23 @@ def stroke_image(g: np.random.Generator) -> np.ndarray:
     return np.clip(img, 0.0, 1.0)
 
 
+def stroke_scale(n: int) -> int:
+    """Nearest-upsampling factor of the 28 x 28 strokes on an n x n plane: the
+    image spans about 70 % of the plane (x5, 140 px, at n = 200)."""
+    return max(1, (7 * n) // 280)
+
+
 def strokes_batch(wid: int, batch: int, n: int = 200) -> np.ndarray:
-    """Stroke digits upsampled x5 (nearest) to 140 x 140, centred in n x n."""
+    """Stroke digits upsampled (nearest, x stroke_scale(n); x5 to 140 x 140 at
+    n = 200), centred in n x n."""
     g = rng(wid, 0)
+    f = stroke_scale(n)
+    s = 28 * f
     out = np.zeros((batch, n, n))
-    o = (n - 140) // 2
-    block = np.ones((5, 5))
+    o = (n - s) // 2
+    block = np.ones((f, f))
     for b in range(batch):
-        out[b, o:o + 140, o:o + 140] = np.kron(stroke_image(g), block)
+        out[b, o:o + s, o:o + s] = np.kron(stroke_image(g), block)
     return out.astype(np.float32)
 
 
@@ -194,6 +203,30 @@ def upstream_intensity_grad(w: Workload, batch: Optional[int] = None) -> np.ndar
     b = w.batch if batch is None else batch
     g = rng(w.wid, 3)
     return np.stack([g.standard_normal((w.n, w.n)) for _ in range(b)]).astype(np.float32)
+
+
+def ten_class_layout(n: int) -> DetectorLayout:
+    """The ten-region layout of the 200 x 200 prototype scaled to an n x n plane."""
+    if n == 200:
+        return TEN_CLASS_LAYOUT_200
+    f = n / 200.0
+    t = TEN_CLASS_LAYOUT_200
+    return DetectorLayout(max(1, int(round(t.size * f))), tuple(int(round(v * f)) for v in t.y0),
+                          tuple(int(round(v * f)) for v in t.x0))
+
+
+def scaled(w: Workload, n: Optional[int] = None, layers: Optional[int] = None) -> Workload:
+    """Workload w on an unpadded n x n grid with `layers` layers: the depth and
+    size variants of the paper's runtime study (§5.3: {1, 3, 5, 7, 10} layers
+    on grids up to 500 x 500, and deeper networks).  The random streams stay
+    those of w, so a variant with w's own n and depth is w itself."""
+    n = w.n if n is None else int(n)
+    layers = w.layers if layers is None else int(layers)
+    if n == w.n and layers == w.layers:
+        return w
+    det = ten_class_layout(n) if w.detector is not None else None
+    name = f"donn{layers}_n{n}_b{w.batch}_{w.kind}"
+    return dataclasses.replace(w, name=name, n=n, n_fft=n, layers=layers, detector=det)
 
 
 def layout_grid(n: int, num: int, size: int) -> DetectorLayout:

@@ -152,7 +152,7 @@ int main() {
   ok &= check_codelet<32>(g); ok &= check_codelet<40>(g);
   ok &= check_plan<64>(g); ok &= check_plan<100>(g); ok &= check_plan<128>(g);
   ok &= check_plan<200>(g); ok &= check_plan<256>(g); ok &= check_plan<400>(g);
-  ok &= check_plan<512>(g); ok &= check_plan<1000>(g);
+  ok &= check_plan<500>(g); ok &= check_plan<512>(g); ok &= check_plan<1000>(g);
   ok &= check_plan<1024>(g);
   std::printf(ok ? "ALL OK\n" : "FAILURES\n");
   return ok ? 0 : 1;

@@ -223,3 +223,19 @@ def test_training_iteration_at_full_size(lrb):
     lrb.lr_adam_update(phi_dev, grad, m, v, 1, **ADAM_F32)
     ref_phi, _, _ = od.adam_update(phi, g32, np.zeros(phi.shape), np.zeros(phi.shape), 1, **ADAM_F32)
     assert rel(host(phi_dev), ref_phi) < 1e-6
+
+
+# Depth and grid variants of the benchmark workload (the paper's runtime
+# study, §5.3): deep networks accumulate rounding over many hops, and N=500
+# runs the 25 x 20 Cooley-Tukey plan with its twiddled 20-point B-step.
+@pytest.mark.parametrize("n,layers,b", [(100, 30, 2), (200, 10, 3), (500, 3, 2)])
+def test_cross_entropy_step_depth_and_grid_variants(lrb, n, layers, b):
+    w = wl.scaled(wl.WORKLOADS[3], n=n, layers=layers)
+    net, phi, saved, out, ref, h = sums_only_forward(lrb, w, b, layers, w.detector)
+    assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
+    labels = wl.labels(w, b)
+    grad, loss = lrb.lr_donn_backward(net, dev(phi), saved, sums=out["sums"], labels=dev(labels))
+    ref_loss, gs = od.softmax_cross_entropy(ref["sums"], labels)
+    ref_grad = od.donn_backward(ref, phi, h, 1.0, odet(w.detector), grad_sums=gs)
+    assert abs(float(loss) - ref_loss) / abs(ref_loss) < TOL_FIELD
+    assert rel(host(grad), ref_grad) < TOL_GRAD

@@ -56,3 +56,25 @@ def test_other_generators_shapes_and_ranges():
     assert bl.shape == (2, 512, 512) and bl.min() >= 0 and bl.max() > 0.4
     g = wl.upstream_intensity_grad(wl.WORKLOADS[5], batch=2)
     assert g.shape == (2, 1000, 1000) and abs(float(g.mean())) < 0.01
+
+
+def test_scaled_variants():
+    w = wl.WORKLOADS[3]
+    assert wl.scaled(w) is w and wl.scaled(w, n=200, layers=5) is w
+    v = wl.scaled(w, n=500, layers=30)
+    assert (v.n, v.n_fft, v.layers, v.batch, v.wid) == (500, 500, 30, w.batch, w.wid)
+    d = v.detector
+    assert d.num == 10 and d.size == 50
+    for y0, x0 in zip(d.y0, d.x0):
+        assert 0 <= y0 and y0 + d.size <= 500 and 0 <= x0 and x0 + d.size <= 500
+    # the regions stay pairwise disjoint when scaled
+    boxes = list(zip(d.y0, d.x0))
+    for i in range(len(boxes)):
+        for k in range(i + 1, len(boxes)):
+            (ya, xa), (yb, xb) = boxes[i], boxes[k]
+            assert abs(ya - yb) >= d.size or abs(xa - xb) >= d.size
+    a = wl.amplitudes(v, 2)
+    assert a.shape == (2, 500, 500) and a.min() >= 0.0 and a.max() <= 1.0
+    f = wl.stroke_scale(500)
+    o = (500 - 28 * f) // 2
+    assert np.all(a[:, :o, :] == 0) and np.all(a[:, :, :o] == 0)
