@@ -8,7 +8,9 @@ hot path computes, written from the LightRidge paper (arXiv 2306.11268):
 * free-space diffraction as a spectral product (§3.1.1, Eqs. (forward_diff)
   and (diffraction_freq)) with the Fresnel transfer function (Eq. (fresnel))
   or the Rayleigh-Sommerfeld one in angular-spectrum form (Eqs. (sommerfeld),
-  (r01));
+  (r01)), or with H the sampled impulse response's DFT (the Fresnel or the
+  Rayleigh-Sommerfeld kernel on the grid of displacements);
+* the Fraunhofer far field (Eq. (fraunhofer)) as one scaled Fourier sum;
 * phase modulation by exp(j*phi) with the amplitude scale gamma
   (§3.1.2, Eqs. (phase_euler), (phase_mod_matrix); §3.2);
 * the detector: intensity |U|^2 summed over rectangular regions (§2.1);
@@ -18,7 +20,13 @@ hot path computes, written from the LightRidge paper (arXiv 2306.11268):
 Readings taken where the paper is silent or ambiguous:
 
 * transfer functions are the analytic ones, sampled on the unshifted DFT
-  frequency grid f_k = k'/(M*dx), k' = k for k < (M+1)//2 else k - M;
+  frequency grid f_k = k'/(M*dx), k' = k for k < (M+1)//2 else k - M; the
+  impulse-response variants sample the kernel h at the displacements
+  d_i = i'*dx on the same wrapped index grid and take H = dx^2 * DFT2(h),
+  which makes the spectral product the discrete linear convolution
+  sum_xi U(xi) h(x - xi) dx^2 of Eq. (forward_diff) on the padded grid;
+* the Fraunhofer input and output grids are centred: input sample i sits at
+  xi = (i - M/2)*dx, output sample k at x = (k - M/2)*lambda*z/(M*dx);
 * forward DFT uses exp(-2*pi*i*jk/M) and is unnormalised, the inverse uses
   exp(+2*pi*i*jk/M) / M (per axis);
 * an L-layer network performs L+1 hops of the same distance z: source to
@@ -44,6 +52,8 @@ import numpy as np
 
 FRESNEL = 0
 ANGULAR_SPECTRUM = 1
+FRESNEL_IR = 2   # H = dx^2 DFT2 of the sampled Fresnel kernel (Eq. (fresnel))
+RS_IR = 3        # H = dx^2 DFT2 of the sampled Rayleigh-Sommerfeld kernel (Eqs. (sommerfeld), (r01))
 
 
 # ---------------------------------------------------------------------------
@@ -87,6 +97,40 @@ def frequencies(m: int, pixel_pitch: float) -> np.ndarray:
     return ks.astype(np.float64) / (m * pixel_pitch)
 
 
+def displacements(m: int, pixel_pitch: float) -> np.ndarray:
+    """Displacements d_i = i' * dx of the wrapped index grid (i' = i for
+    i < (m+1)//2 else i - m), in metres: index i of a circular convolution
+    kernel holds the kernel at d_i."""
+    i = np.arange(m, dtype=np.int64)
+    ii = np.where(i < (m + 1) // 2, i, i - m)
+    return ii.astype(np.float64) * pixel_pitch
+
+
+def impulse_response(wavelength: float, pixel_pitch: float, distance: float,
+                     approx: int, m: int) -> np.ndarray:
+    """The diffraction kernel h(x - xi, y - eta, z) of Eq. (forward_diff) at the
+    m x m displacements of the wrapped grid, complex128.
+
+    FRESNEL_IR (Eq. (fresnel)): h = exp(jkz)/(j*lambda*z) * exp(jk(dx^2+dy^2)/(2z)).
+    RS_IR (Eqs. (sommerfeld), (r01)): h = z/(j*lambda) * exp(jkr)/r^2 with
+    r = sqrt(z^2 + dx^2 + dy^2).
+    The phase kz is carried as exp(jkz) and the rest of the phase added
+    separately (k(r - z) = k(dx^2 + dy^2)/(r + z)), so that no large argument
+    loses precision.
+    """
+    d = displacements(m, pixel_pitch)
+    rho2 = d[:, None] ** 2 + d[None, :] ** 2
+    k = 2.0 * np.pi / wavelength
+    z = distance
+    ekz = np.exp(1j * 2.0 * np.pi * np.fmod(z / wavelength, 1.0))
+    if approx == FRESNEL_IR:
+        return ekz / (1j * wavelength * z) * np.exp(1j * k * rho2 / (2.0 * z))
+    if approx == RS_IR:
+        r = np.sqrt(z * z + rho2)
+        return z / (1j * wavelength) * ekz * np.exp(1j * k * rho2 / (r + z)) / (r * r)
+    raise ValueError(f"no impulse response for approximation {approx}")
+
+
 def transfer_function(wavelength: float, pixel_pitch: float, distance: float,
                       approx: int, m: int) -> np.ndarray:
     """H[ky, kx] for one hop of length ``distance`` on an m x m grid, complex128.
@@ -99,7 +143,12 @@ def transfer_function(wavelength: float, pixel_pitch: float, distance: float,
     Rayleigh-Sommerfeld kernel, H = exp(jkz*sqrt(1 - lambda^2 (fx^2 + fy^2)))
     on propagating frequencies and exp(-kz*sqrt(lambda^2 f^2 - 1)) on
     evanescent ones.
+
+    FRESNEL_IR, RS_IR: dx^2 times the DFT of the sampled kernel
+    (impulse_response), the discrete form of Eq. (forward_diff).
     """
+    if approx in (FRESNEL_IR, RS_IR):
+        return pixel_pitch ** 2 * dft2(impulse_response(wavelength, pixel_pitch, distance, approx, m))
     f = frequencies(m, pixel_pitch)
     f2 = f[:, None] ** 2 + f[None, :] ** 2
     k = 2.0 * np.pi / wavelength
@@ -135,6 +184,43 @@ def propagate(u: np.ndarray, h: np.ndarray, adjoint: bool = False) -> np.ndarray
     x[..., o:o + n, o:o + n] = u
     spec = dft2(x) * (np.conj(h) if adjoint else h)
     return idft2(spec)[..., o:o + n, o:o + n]
+
+
+# ---------------------------------------------------------------------------
+# Fraunhofer far field (§3.1.1, Eq. (fraunhofer)).
+# ---------------------------------------------------------------------------
+
+def fraunhofer(u: np.ndarray, wavelength: float, pixel_pitch: float, distance: float, m: int) -> np.ndarray:
+    """Far field of fields u [..., n, n] on the centred m x m output grid.
+
+    U(x, y) = exp(jkz) exp(jk(x^2+y^2)/(2z)) / (j*lambda*z)
+              * sum_{xi, eta} U(xi, eta) exp(-j*2*pi*(x*xi + y*eta)/(lambda*z)) dx^2,
+    the input sitting centred in the m x m grid (sample i at xi = (i - m/2) dx)
+    and the output at x = (k - m/2) * lambda*z/(m*dx), k < m (pitch
+    fraunhofer_pitch).  With those grids the exponent is
+    -2*pi*i*(k - m/2)*(i - m/2)/m, evaluated with the product reduced modulo m
+    in integers.  m must be even.
+    """
+    n = u.shape[-1]
+    if u.shape[-2] != n or n > m or (m - n) % 2 or m % 2:
+        raise ValueError("field must be n x n with n <= m, m - n even and m even")
+    o = (m - n) // 2
+    x = np.zeros(u.shape[:-2] + (m, m), dtype=np.complex128)
+    x[..., o:o + n, o:o + n] = u
+    c = np.arange(m, dtype=np.int64) - m // 2
+    e = np.outer(c, c) % m
+    w = np.exp(-2j * np.pi * e.astype(np.float64) / m)
+    s = w @ x @ w.T * pixel_pitch ** 2
+    k = 2.0 * np.pi / wavelength
+    xo = c.astype(np.float64) * fraunhofer_pitch(wavelength, pixel_pitch, distance, m)
+    r2 = xo[:, None] ** 2 + xo[None, :] ** 2
+    ekz = np.exp(1j * 2.0 * np.pi * np.fmod(distance / wavelength, 1.0))
+    return ekz * np.exp(1j * k * r2 / (2.0 * distance)) / (1j * wavelength * distance) * s
+
+
+def fraunhofer_pitch(wavelength: float, pixel_pitch: float, distance: float, m: int) -> float:
+    """Sample pitch of the Fraunhofer output plane, lambda*z/(m*dx)."""
+    return wavelength * distance / (m * pixel_pitch)
 
 
 # ---------------------------------------------------------------------------

@@ -383,3 +383,111 @@ def global_phase_invariance():
             d = od.donn_backward(out, phi, h, gamma, grad_intensity=gi)
         worst = max(worst, float(np.max(np.abs(d.sum(axis=(1, 2))) / np.abs(d).sum(axis=(1, 2)))))
     return worst
+
+
+# --- sampled impulse response and Fraunhofer far field ----------------------
+
+def _kernel_direct(lam, z, approx, ddy, ddx):
+    """The diffraction kernels of Eqs. (fresnel) and (sommerfeld)/(r01) at one
+    displacement, evaluated directly (one point at a time)."""
+    k = 2.0 * np.pi / lam
+    rho2 = ddy * ddy + ddx * ddx
+    ekz = np.exp(1j * 2.0 * np.pi * np.fmod(z / lam, 1.0))
+    if approx == od.FRESNEL_IR:
+        return ekz / (1j * lam * z) * np.exp(1j * k * rho2 / (2.0 * z))
+    r = np.sqrt(z * z + rho2)
+    return z / (1j * lam) * ekz * np.exp(1j * k * rho2 / (r + z)) / (r * r)
+
+
+def ir_linear_convolution(approx, lam=LAM, dx=DX, z=0.05, n=6, m=12):
+    """The spectral hop with the sampled-kernel H equals the brute-force linear
+    convolution sum_xi U(xi) h(x - xi) dx^2 of Eq. (forward_diff) on the
+    aperture (m >= 2n - 1, so no displacement wraps)."""
+    g = np.random.default_rng(31)
+    u = crand(g, (n, n))
+    h = od.transfer_function(lam, dx, z, approx, m)
+    got = od.propagate(u[None], h)[0]
+    ref = np.zeros((n, n), complex)
+    for y in range(n):
+        for x in range(n):
+            acc = 0.0 + 0.0j
+            for eta in range(n):
+                for xi in range(n):
+                    acc += u[eta, xi] * _kernel_direct(lam, z, approx, (y - eta) * dx, (x - xi) * dx)
+            ref[y, x] = acc * dx * dx
+    return rel(got, ref)
+
+
+def fresnel_ir_gaussian(lam=LAM, dx=DX, n=64, m=128, z=0.35, w0_px=6.0):
+    """A Gaussian beam through the sampled Fresnel kernel against the
+    closed-form Gaussian beam (tolerance: Riemann-sum and kernel-truncation
+    error of the discrete convolution, about 1e-4 here)."""
+    u0 = gaussian_field(n, w0_px, 0.0, lam, dx)
+    ref = gaussian_field(n, w0_px, z, lam, dx)
+    h = od.transfer_function(lam, dx, z, od.FRESNEL_IR, m)
+    return rel(od.propagate(u0[None], h)[0], ref)
+
+
+def rs_ir_paraxial_bound(lam=1550e-9, dx=8e-6, z=0.05, n=16, m=32):
+    """Rayleigh-Sommerfeld against Fresnel sampled kernels: pointwise
+    |h_RS/h_F - 1| <= eps = rho^2/z^2 + k rho^4/(8 z^3) (binomial expansion of
+    r in Eq. (r01) and the r^2 -> z^2 of the denominator), so
+    |U_RS - U_F| <= eps dx^2/(lambda z) sum|U|.  Returns the ratio of the
+    largest difference to that bound (must be <= 1) and the size of the
+    difference relative to the field (must not vanish: the kernels differ)."""
+    g = np.random.default_rng(32)
+    u = crand(g, (n, n))
+    a = od.propagate(u[None], od.transfer_function(lam, dx, z, od.RS_IR, m))[0]
+    b = od.propagate(u[None], od.transfer_function(lam, dx, z, od.FRESNEL_IR, m))[0]
+    rho2 = 2.0 * ((n - 1) * dx) ** 2
+    k = 2.0 * np.pi / lam
+    eps = rho2 / z ** 2 + k * rho2 ** 2 / (8.0 * z ** 3)
+    bound = eps * dx * dx / (lam * z) * np.sum(np.abs(u))
+    return float(np.max(np.abs(a - b)) / bound), rel(a, b)
+
+
+def fresnel_ir_separable(lam=LAM, dx=DX, z=0.3, m=40):
+    """The Fresnel kernel factors in x and y, so its 2-D DFT has rank one:
+    H[ky,kx] H[0,0] = H[ky,0] H[0,kx]."""
+    h = od.transfer_function(lam, dx, z, od.FRESNEL_IR, m)
+    return rel(h * h[0, 0], np.outer(h[:, 0], h[0, :]))
+
+
+def fraunhofer_vs_fresnel_sum(lam=LAM, dx=DX, m=32, n=16):
+    """Expanding (x - xi)^2 in Eq. (fresnel) turns the Fresnel sum into the
+    Fraunhofer sum of U(xi) exp(jk xi^2/(2z)) at the same x.  At
+    z = m dx^2/lambda the Fraunhofer output pitch lambda z/(m dx) equals dx,
+    so the sampled-kernel Fresnel hop and Eq. (fraunhofer) must agree exactly
+    on the aperture."""
+    z = m * dx * dx / lam
+    g = np.random.default_rng(33)
+    u = crand(g, (n, n))
+    k = 2.0 * np.pi / lam
+    c = (np.arange(n) - n / 2.0) * dx           # the n-window's coordinates in the centred m grid
+    chirp = np.exp(1j * k * (c[:, None] ** 2 + c[None, :] ** 2) / (2.0 * z))
+    far = od.fraunhofer((u * chirp)[None], lam, dx, z, m)[0]
+    o = (m - n) // 2
+    near = od.propagate(u[None], od.transfer_function(lam, dx, z, od.FRESNEL_IR, m))[0]
+    return rel(far[o:o + n, o:o + n], near)
+
+
+def fraunhofer_rectangle(lam=LAM, dx=DX, z=5.0, m=64, a=6, b=10):
+    """Far field of a uniform a x b rectangle centred in the grid: the
+    Fourier sum is a product of geometric series, |sum_i exp(-2 pi i u i / m)|
+    = |sin(pi u a / m) / sin(pi u / m)|, u = k - m/2; the magnitude of
+    Eq. (fraunhofer) is that product times dx^2/(lambda z)."""
+    n = max(a, b) + (max(a, b) % 2)
+    u = np.zeros((n, n))
+    oy, ox = (n - a) // 2, (n - b) // 2
+    u[oy:oy + a, ox:ox + b] = 1.0
+    got = np.abs(od.fraunhofer(u[None], lam, dx, z, m)[0])
+
+    def dirichlet(cnt):
+        v = np.arange(m) - m // 2
+        out = np.full(m, float(cnt))
+        nz = v % m != 0
+        out[nz] = np.abs(np.sin(np.pi * v[nz] * cnt / m) / np.sin(np.pi * v[nz] / m))
+        return out
+
+    ref = np.outer(dirichlet(a), dirichlet(b)) * dx * dx / (lam * z)
+    return rel(got, ref)

@@ -14,7 +14,8 @@ import oracle_checks as c
 _orig = {name: getattr(od, name) for name in (
     "dft_matrix", "idft2", "transfer_function", "frequencies", "propagate",
     "modulate", "detector_readout", "region_scatter", "softmax_cross_entropy",
-    "mse_softmax_loss", "donn_forward", "donn_backward", "adam_update")}
+    "mse_softmax_loss", "donn_forward", "donn_backward", "adam_update",
+    "impulse_response", "displacements", "fraunhofer", "fraunhofer_pitch")}
 
 
 def _dft_sign_flipped(m, inverse=False):
@@ -145,6 +146,44 @@ def _fails_grad(**kw):
     return c.grad_fd(**kw)[0] > 1e-3
 
 
+def _ir_no_area_element(lam, dx, z, approx, m):
+    h = _orig["transfer_function"](lam, dx, z, approx, m)
+    return h / (dx * dx) if approx in (od.FRESNEL_IR, od.RS_IR) else h
+
+
+def _displacements_unwrapped(m, dx):
+    return np.arange(m, dtype=np.float64) * dx
+
+
+def _rs_one_over_r(lam, dx, z, approx, m):
+    h = _orig["impulse_response"](lam, dx, z, approx, m)
+    if approx == od.RS_IR:
+        d = _orig["displacements"](m, dx)
+        r = np.sqrt(z * z + d[:, None] ** 2 + d[None, :] ** 2)
+        h = h * r
+    return h
+
+
+def _rs_kernel_conjugated(lam, dx, z, approx, m):
+    h = _orig["impulse_response"](lam, dx, z, approx, m)
+    return np.conj(h) if approx == od.RS_IR else h
+
+
+def _fraunhofer_output_uncentred(u, lam, dx, z, m):
+    return np.roll(_orig["fraunhofer"](u, lam, dx, z, m), (m // 2, m // 2), axis=(-2, -1))
+
+
+def _fraunhofer_no_output_chirp(u, lam, dx, z, m):
+    out = _orig["fraunhofer"](u, lam, dx, z, m)
+    c = (np.arange(m) - m // 2) * _orig["fraunhofer_pitch"](lam, dx, z, m)
+    k = 2.0 * np.pi / lam
+    return out * np.exp(-1j * k * (c[:, None] ** 2 + c[None, :] ** 2) / (2.0 * z))
+
+
+def _fraunhofer_pitch_no_m(lam, dx, z, m):
+    return lam * z / dx
+
+
 MUTANTS = [
     ("dft_sign", "dft_matrix", _dft_sign_flipped, lambda: c.dft_vs_numpy() > 1e-3),
     ("idft_norm", "idft2", _idft_unnormalised, lambda: c.dft_delta_parseval() > 1e-3),
@@ -161,6 +200,13 @@ MUTANTS = [
     ("mse_no_softmax_jacobian", "mse_softmax_loss", _mse_no_softmax_jacobian,
      lambda: c.loss_fd(od.mse_softmax_loss) > 1e-3),
     ("mse_norm_not_squared", "mse_softmax_loss", _mse_not_squared, lambda: c.mse_known_values() > 1e-3),
+    ("ir_no_dx2", "transfer_function", _ir_no_area_element, lambda: c.ir_linear_convolution(od.FRESNEL_IR) > 1e-3),
+    ("ir_unwrapped", "displacements", _displacements_unwrapped, lambda: c.ir_linear_convolution(od.RS_IR) > 1e-3),
+    ("rs_one_over_r", "impulse_response", _rs_one_over_r, lambda: c.rs_ir_paraxial_bound()[0] > 10.0),
+    ("rs_conjugated", "impulse_response", _rs_kernel_conjugated, lambda: c.rs_ir_paraxial_bound()[0] > 10.0),
+    ("fraunhofer_uncentred", "fraunhofer", _fraunhofer_output_uncentred, lambda: c.fraunhofer_rectangle() > 1e-3),
+    ("fraunhofer_no_chirp", "fraunhofer", _fraunhofer_no_output_chirp, lambda: c.fraunhofer_vs_fresnel_sum() > 1e-3),
+    ("fraunhofer_pitch", "fraunhofer_pitch", _fraunhofer_pitch_no_m, lambda: c.fraunhofer_vs_fresnel_sum() > 1e-3),
     ("adam_no_bias_correction", "adam_update", _adam_no_bias_correction, lambda: c.adam_first_step() > 1e-3),
     ("adam_eps_inside_sqrt", "adam_update", _adam_eps_inside_sqrt, lambda: c.adam_constant_gradient() > 1e-3),
     ("adam_betas_swapped", "adam_update", _adam_betas_swapped, lambda: c.adam_vs_torch() > 1e-3),

@@ -126,3 +126,35 @@ def test_phase_gradient_global_phase_invariance():
 def test_transfer_function_rejects_unknown_approximation():
     with pytest.raises(ValueError):
         od.transfer_function(532e-9, 36e-6, 0.3, 7, 8)
+
+
+@pytest.mark.parametrize("approx", [od.FRESNEL_IR, od.RS_IR])
+def test_sampled_kernel_hop_is_linear_convolution(approx):
+    # the padded spectral hop against the direct sum of Eq. (forward_diff)
+    assert c.ir_linear_convolution(approx) < 1e-12
+
+
+def test_sampled_fresnel_kernel_gaussian_beam():
+    # Riemann-sum error of the discrete convolution of a 6-px Gaussian (~1e-10 measured)
+    assert c.fresnel_ir_gaussian() < 1e-7
+
+
+def test_sampled_rayleigh_sommerfeld_within_paraxial_bound():
+    ratio, diff = c.rs_ir_paraxial_bound()
+    assert ratio <= 1.0 and diff > 1e-8
+
+
+def test_sampled_fresnel_kernel_is_separable():
+    assert c.fresnel_ir_separable() < 1e-12
+
+
+def test_fraunhofer_is_the_expanded_fresnel_sum():
+    assert c.fraunhofer_vs_fresnel_sum() < 1e-12
+
+
+def test_fraunhofer_rectangle_dirichlet_kernel():
+    assert c.fraunhofer_rectangle() < 1e-12
+
+
+def test_fraunhofer_output_pitch():
+    assert abs(od.fraunhofer_pitch(532e-9, 36e-6, 1.0, 100) - 532e-9 / (100 * 36e-6)) < 1e-20
