@@ -50,10 +50,19 @@ typedef struct lr_c64 {
   float im;
 } lr_c64;
 
-/* Diffraction approximations (§3.1.1). */
+/* Diffraction approximations (§3.1.1).  The first two are the analytic
+ * transfer functions; the next two take H as the DFT of the diffraction
+ * kernel h of Eq. (forward_diff) sampled on the n_fft grid of displacements
+ * (the discrete linear convolution of the field with h, exact on the
+ * aperture when n_fft >= 2n - 1); the last is the far field of
+ * Eq. (fraunhofer), a single scaled Fourier transform that changes the
+ * sample pitch and is available through lr_propagate only. */
 enum lr_approx {
   LR_FRESNEL = 0,           /* Eq. (fresnel): H = exp(jkz) exp(-j pi lambda z (fx^2+fy^2)) */
-  LR_ANGULAR_SPECTRUM = 1   /* Eqs. (sommerfeld),(r01): H = exp(jkz sqrt(1 - lambda^2 f^2)) */
+  LR_ANGULAR_SPECTRUM = 1,  /* Eqs. (sommerfeld),(r01): H = exp(jkz sqrt(1 - lambda^2 f^2)) */
+  LR_FRESNEL_IR = 2,        /* Eq. (fresnel) kernel exp(jkz)/(j lambda z) exp(jk(dx^2+dy^2)/(2z)), H = dx^2 DFT2(h) */
+  LR_RS_IR = 3,             /* Eqs. (sommerfeld),(r01) kernel z/(j lambda) exp(jkr)/r^2, H = dx^2 DFT2(h) */
+  LR_FRAUNHOFER = 4         /* Eq. (fraunhofer): far field on the centred pitch lambda z/(n_fft dx) grid */
 };
 
 enum lr_status {
@@ -106,15 +115,28 @@ typedef struct lr_donn {
                            The Fresnel path relies on its separability. */
 } lr_donn;
 
-/* Transfer function of one hop (§3.1.1, Eqs. (fresnel), (sommerfeld), (r01)).
+/* Transfer function of one hop (§3.1.1, Eqs. (fresnel), (sommerfeld), (r01),
+ * (forward_diff), (fraunhofer)).
  * Writes d_H[ky][kx], ky, kx in [0, n_fft), at the unshifted DFT frequencies
  * f = k'/(n_fft*pixel_pitch), k' = k for k < (n_fft+1)/2 else k - n_fft.
  * Evaluated in float64 on the host (the phase kz is reduced modulo 2*pi
- * before the quadratic term is added) and rounded once to complex64.
- * The angular spectrum decays as exp(-kz sqrt(lambda^2 f^2 - 1)) on
- * evanescent frequencies.  Blocking: returns after the upload has completed.
+ * before the rest is added) and rounded once to complex64.
+ *   LR_FRESNEL, LR_ANGULAR_SPECTRUM: the analytic transfer functions; the
+ *     angular spectrum decays as exp(-kz sqrt(lambda^2 f^2 - 1)) on
+ *     evanescent frequencies.
+ *   LR_FRESNEL_IR, LR_RS_IR: pixel_pitch^2 times the 2-D DFT (float64,
+ *     mixed radix) of the kernel sampled at the displacements
+ *     (y', x') * pixel_pitch, y' and x' wrapped like k'.  n_fft must have no
+ *     prime factor above 5; distance > 0.
+ *   LR_FRAUNHOFER: not a transfer function but the far-field output table
+ *     used by lr_propagate: entry (dy, dx) is
+ *     (-1)^(dy+dx) pixel_pitch^2 exp(jkz) exp(jk(x^2+y^2)/(2z)) / (j lambda z)
+ *     at x = dx' lambda z/(n_fft pixel_pitch), y likewise.  n_fft even;
+ *     distance > 0.
+ * Blocking: returns after the upload has completed.
  * Errors: LR_E_NULL (d_H), LR_E_ARG (non-finite or non-positive lambda / pitch,
- * non-finite z), LR_E_APPROX, LR_E_SIZE (n_fft < 1 or > 4096), LR_E_HIP. */
+ * non-finite z, z <= 0 for the last three), LR_E_APPROX, LR_E_SIZE (n_fft < 1
+ * or > 4096, or not as required above), LR_E_HIP. */
 int lr_tf_build(double wavelength, double pixel_pitch, double distance, int32_t approx,
                 int32_t n_fft, lr_c64* d_H, void* stream);
 
@@ -135,7 +157,14 @@ int64_t lr_saved_size(const lr_donn* net, int32_t batch);
  * adjoint P_z^H (the same pad/crop with conj(H), i.e. back-propagation) when
  * adjoint != 0.  Uses net->wavelength..net->d_H; net->num_layers, gamma and
  * det are ignored.  d_in, d_out: complex64 [batch][n][n]; they must not alias.
- * d_work: >= lr_workspace_size(net, batch, LR_OP_PROPAGATE) bytes. */
+ * d_work: >= lr_workspace_size(net, batch, LR_OP_PROPAGATE) bytes.
+ * With net->approx == LR_FRAUNHOFER (d_H the far-field table of lr_tf_build)
+ * d_out is the far field of Eq. (fraunhofer), complex64 [batch][n_fft][n_fft]
+ * on the centred output grid: sample (ky, kx) at
+ * ((ky - n_fft/2), (kx - n_fft/2)) * lambda z/(n_fft pixel_pitch), the input
+ * sitting centred in the n_fft grid (sample i at (i - n_fft/2) pixel_pitch);
+ * adjoint must be 0.  lr_donn_forward / lr_donn_backward reject
+ * LR_FRAUNHOFER (LR_E_APPROX): the far field does not chain layers. */
 int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* d_out,
                  int32_t adjoint, void* d_work, size_t work_bytes, void* stream);
 

@@ -17,6 +17,9 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "liblr.so")
 
 LR_FRESNEL = 0
 LR_ANGULAR_SPECTRUM = 1
+LR_FRESNEL_IR = 2
+LR_RS_IR = 3
+LR_FRAUNHOFER = 4
 LR_OP_PROPAGATE = 0
 LR_OP_FORWARD = 1
 LR_OP_BACKWARD = 2
@@ -209,15 +212,17 @@ def lr_tf_build(wavelength: float, pixel_pitch: float, distance: float, approx: 
 
 
 def lr_propagate(net: Network, field, adjoint: bool = False, out=None):
-    """One hop P_z (or its adjoint) of a complex64 batch [B, n, n]."""
+    """One hop P_z (or its adjoint) of a complex64 batch [B, n, n]; with
+    LR_FRAUNHOFER the far field [B, n_fft, n_fft]."""
     torch = _torch()
     b = int(field.shape[0])
+    m = net.n_fft if net.c.approx == LR_FRAUNHOFER else net.n
     if out is None:
-        out = torch.empty_like(field)
+        out = torch.empty((b, m, m), dtype=torch.complex64, device=field.device)
     w = net.workspace(b, LR_OP_PROPAGATE)
     _check(load().lr_propagate(ctypes.byref(net.c), b,
                                _ptr(field, torch.complex64, (b, net.n, net.n), "field"),
-                               _ptr(out, torch.complex64, (b, net.n, net.n), "out"),
+                               _ptr(out, torch.complex64, (b, m, m), "out"),
                                1 if adjoint else 0, _ptr(w), w.numel(), _stream(net.device)), "lr_propagate")
     return out
 

@@ -5,6 +5,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <complex>
 #include <cstdio>
 #include <cstring>
 #include <map>
@@ -107,7 +108,10 @@ int validate_net(const lr_donn* net, bool need_layers) {
   if (!net) return LR_E_NULL;
   if (!finite_pos(net->wavelength) || !finite_pos(net->pixel_pitch) || !std::isfinite(net->distance))
     return LR_E_ARG;
-  if (net->approx != LR_FRESNEL && net->approx != LR_ANGULAR_SPECTRUM) return LR_E_APPROX;
+  if (net->approx < LR_FRESNEL || net->approx > LR_FRAUNHOFER) return LR_E_APPROX;
+  // the far field changes the sample pitch and does not chain layers
+  if (need_layers && net->approx == LR_FRAUNHOFER) return LR_E_APPROX;
+  if (net->approx == LR_FRAUNHOFER && (net->n_fft % 2)) return LR_E_SIZE;
   if (!lr::fft_size_supported(net->n_fft)) return LR_E_SIZE;
   if (net->n < 1 || net->n > net->n_fft || ((net->n_fft - net->n) & 1)) return LR_E_SIZE;
   if (need_layers) {
@@ -141,7 +145,7 @@ Layout make_layout(const lr_donn* net, int batch, int op) {
   Layout L;
   const int n = net->n;
   const int N = net->n_fft;
-  const bool as = net->approx == LR_ANGULAR_SPECTRUM;
+  const bool as = net->approx != LR_FRESNEL;  // the non-separable passes
   const lr::TileShape sh = lr::tile_shape(N, 0);
   L.ntiles_vec = ceil_div(n, sh.T);
   L.ntiles_spec = ceil_div(N, sh.T);
@@ -196,7 +200,7 @@ T* at(void* base, size_t off) {
 Axis pass_axis(int p) { return (p & 1) ? lr::kRow : lr::kCol; }
 // Layer l (1-based) is modulated in pass l+1: transposed storage when that pass is a row pass.
 int layer_transposed(const lr_donn* net, int l) {
-  if (net->approx == LR_ANGULAR_SPECTRUM) return 1;
+  if (net->approx != LR_FRESNEL) return 1;
   return pass_axis(l + 1) == lr::kRow ? 1 : 0;
 }
 
@@ -206,7 +210,7 @@ const char* kind_name(int k) {
 }
 const char* as_kind_name(int k) {
   static const char* names[] = {"row_first", "col", "row_mid", "row_last", "row_bwd_first", "row_bwd_mid",
-                                "row_bwd_last", "row_ifft"};
+                                "row_bwd_last", "row_ifft", "col_far"};
   return names[k];
 }
 
@@ -319,6 +323,13 @@ int check_work(const lr_donn* net, int batch, int op, void* d_work, size_t work_
   return LR_OK;
 }
 
+// Scale of the column-permuted 2-D table: 1/N^2 (the inverse transform's
+// normalisation) for a propagation, 1 for the far-field table.
+float as_table_scale(const lr_donn* net) {
+  const double N = static_cast<double>(net->n_fft);
+  return net->approx == LR_FRAUNHOFER ? 1.0f : static_cast<float>(1.0 / (N * N));
+}
+
 // Transfer-function tables of the passes: the separable Fresnel chirps (in
 // natural frequency order; each pass stages them in its own plan order) or the
 // column-permuted copy of H the angular-spectrum passes read.
@@ -331,8 +342,9 @@ int prep_tables(const lr_donn* net, const Layout& L, void* w, hipStream_t st) {
                                     at<float2>(w, L.chirp_y), st);
     });
   }
-  return run_timed("prep_as_table", st,
-                   [&] { return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), st); });
+  return run_timed("prep_as_table", st, [&] {
+    return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), as_table_scale(net), st);
+  });
 }
 
 // Per-call tables of a forward or backward pass in one launch: the modulation
@@ -346,8 +358,9 @@ int prep_layers(const lr_donn* net, const float* d_phi, bool regions, const Layo
   const bool fresnel = net->approx == LR_FRESNEL;
   const float2* H = reinterpret_cast<const float2*>(net->d_H);
   if (!fresnel) {
-    LR_TRY(run_timed("prep_as_table", st,
-                     [&] { return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), st); }));
+    LR_TRY(run_timed("prep_as_table", st, [&] {
+      return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), as_table_scale(net), st);
+    }));
   }
   return run_timed("prep_layers", st, [&] {
     return lr::launch_prep_layers(d_phi, net->num_layers, net->n, net->gamma, orient, at<float2>(w, L.mod),
@@ -356,6 +369,120 @@ int prep_layers(const lr_donn* net, const float* d_phi, bool regions, const Layo
                                   at<int>(w, L.row_perm), at<int>(w, L.col_perm), fresnel ? H : nullptr,
                                   net->n_fft, at<float2>(w, L.chirp_x), at<float2>(w, L.chirp_y), st);
   });
+}
+
+// ---------------------------------------------------------------------------
+// Host-side float64 tables of lr_tf_build
+// ---------------------------------------------------------------------------
+using cd = std::complex<double>;
+
+// Unnormalised forward DFT (exp(-2*pi*i*jk/m)) of the m samples x[0], x[s],
+// x[2s], ... into X[0..m), by recursive decimation in time over the
+// smallest prime factor (2, 3 or 5; lengths with other factors are rejected
+// by the caller).  w holds exp(-2*pi*i*e/M) for e < M, M a multiple of m:
+// exp(-2*pi*i*e/m) = w[(e mod m) * (M/m)].
+void dft_rec(const cd* x, cd* X, int m, int s, const std::vector<cd>& w, std::vector<cd>& tmp) {
+  if (m == 1) {
+    X[0] = x[0];
+    return;
+  }
+  const int M = static_cast<int>(w.size());
+  const int p = m % 2 == 0 ? 2 : (m % 3 == 0 ? 3 : 5);
+  const int q = m / p;
+  for (int r = 0; r < p; ++r)
+    dft_rec(x + static_cast<size_t>(r) * s, X + static_cast<size_t>(r) * q, q, s * p, w, tmp);
+  // X[k + q*t] = sum_r exp(-2*pi*i*r*(k + q*t)/m) Y_r[k]
+  tmp.assign(m, cd(0.0, 0.0));
+  const long long stride = M / m;
+  for (int k = 0; k < q; ++k)
+    for (int t = 0; t < p; ++t) {
+      cd acc(0.0, 0.0);
+      for (int r = 0; r < p; ++r) {
+        const long long e = (static_cast<long long>(r) * (k + q * t)) % m;
+        acc += w[static_cast<size_t>(e * stride)] * X[r * q + k];
+      }
+      tmp[k + q * t] = acc;
+    }
+  for (int i = 0; i < m; ++i) X[i] = tmp[i];
+}
+
+bool smooth_235(int m) {
+  for (int p : {2, 3, 5})
+    while (m % p == 0) m /= p;
+  return m == 1;
+}
+
+// In-place 2-D forward DFT of an m x m row-major array.
+void dft2_host(std::vector<cd>& a, int m) {
+  std::vector<cd> w(m);
+  for (int e = 0; e < m; ++e) {
+    const double ang = -kTwoPi * static_cast<double>(e) / static_cast<double>(m);
+    w[e] = cd(std::cos(ang), std::sin(ang));
+  }
+  std::vector<cd> in(m), out(m), tmp;
+  for (int y = 0; y < m; ++y) {
+    for (int x = 0; x < m; ++x) in[x] = a[static_cast<size_t>(y) * m + x];
+    dft_rec(in.data(), out.data(), m, 1, w, tmp);
+    for (int x = 0; x < m; ++x) a[static_cast<size_t>(y) * m + x] = out[x];
+  }
+  for (int x = 0; x < m; ++x) {
+    for (int y = 0; y < m; ++y) in[y] = a[static_cast<size_t>(y) * m + x];
+    dft_rec(in.data(), out.data(), m, 1, w, tmp);
+    for (int y = 0; y < m; ++y) a[static_cast<size_t>(y) * m + x] = out[y];
+  }
+}
+
+// Wrapped index i -> i' (i' = i for i < (m+1)/2, else i - m).
+int wrapped(int i, int m) { return i < (m + 1) / 2 ? i : i - m; }
+
+// Sampled-kernel transfer function (Eq. (forward_diff) with the kernel of
+// Eq. (fresnel) or of Eqs. (sommerfeld), (r01)): H = dx^2 DFT2(h), h at the
+// displacements (y', x') * dx of the wrapped grid.  exp(jkz) is carried
+// separately and k(r - z) = k*rho^2/(r + z), so no large phase is formed.
+void impulse_response_tf(int approx, double lam, double dx, double z, int M, std::vector<cd>& H) {
+  const double k = kTwoPi / lam;
+  const cd ekz = std::polar(1.0, kTwoPi * std::fmod(z / lam, 1.0));
+  const cd j(0.0, 1.0);
+  H.assign(static_cast<size_t>(M) * M, cd(0.0, 0.0));
+  for (int y = 0; y < M; ++y) {
+    const double dy = wrapped(y, M) * dx;
+    for (int x = 0; x < M; ++x) {
+      const double dxx = wrapped(x, M) * dx;
+      const double rho2 = dy * dy + dxx * dxx;
+      cd h;
+      if (approx == LR_FRESNEL_IR) {
+        h = ekz / (j * lam * z) * std::polar(1.0, k * rho2 / (2.0 * z));
+      } else {
+        const double r = std::sqrt(z * z + rho2);
+        h = z / (j * lam) * ekz * std::polar(1.0, k * rho2 / (r + z)) / (r * r);
+      }
+      H[static_cast<size_t>(y) * M + x] = h;
+    }
+  }
+  dft2_host(H, M);
+  for (auto& v : H) v *= dx * dx;
+}
+
+// Far-field table of Eq. (fraunhofer) in DFT-index order: with the input
+// centred in the M x M grid (sample i at xi = (i - M/2) dx) and the output
+// centred (sample k at x = (k - M/2) lambda z/(M dx)), output k holds
+// (-1)^d DFT[d], d = (k + M/2) mod M, per axis.  Entry (dy, dx) is
+// (-1)^(dy+dx) dx^2 exp(jkz) exp(jk(x^2+y^2)/(2z)) / (j lambda z) at the
+// output coordinates (x, y) = (dx', dy') * lambda z/(M dx), d' the wrapped
+// index.
+void fraunhofer_table(double lam, double pitch, double z, int M, std::vector<cd>& Q) {
+  const double k = kTwoPi / lam;
+  const double po = lam * z / (static_cast<double>(M) * pitch);
+  const cd pre = std::polar(1.0, kTwoPi * std::fmod(z / lam, 1.0)) / (cd(0.0, 1.0) * lam * z) * (pitch * pitch);
+  Q.assign(static_cast<size_t>(M) * M, cd(0.0, 0.0));
+  for (int y = 0; y < M; ++y) {
+    const double yo = wrapped(y, M) * po;
+    for (int x = 0; x < M; ++x) {
+      const double xo = wrapped(x, M) * po;
+      const double sgn = ((x + y) & 1) ? -1.0 : 1.0;
+      Q[static_cast<size_t>(y) * M + x] = sgn * pre * std::polar(1.0, k * (xo * xo + yo * yo) / (2.0 * z));
+    }
+  }
 }
 
 }  // namespace
@@ -385,9 +512,28 @@ int lr_tf_build(double wavelength, double pixel_pitch, double distance, int32_t 
                 lr_c64* d_H, void* stream) {
   if (!d_H) return LR_E_NULL;
   if (!finite_pos(wavelength) || !finite_pos(pixel_pitch) || !std::isfinite(distance)) return LR_E_ARG;
-  if (approx != LR_FRESNEL && approx != LR_ANGULAR_SPECTRUM) return LR_E_APPROX;
+  if (approx < LR_FRESNEL || approx > LR_FRAUNHOFER) return LR_E_APPROX;
   if (n_fft < 1 || n_fft > 4096) return LR_E_SIZE;
   const int M = n_fft;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  if (approx == LR_FRESNEL_IR || approx == LR_RS_IR || approx == LR_FRAUNHOFER) {
+    if (!(distance > 0.0)) return LR_E_ARG;
+    std::vector<cd> t;
+    if (approx == LR_FRAUNHOFER) {
+      if (M % 2) return LR_E_SIZE;
+      fraunhofer_table(wavelength, pixel_pitch, distance, M, t);
+    } else {
+      if (!smooth_235(M)) return LR_E_SIZE;
+      impulse_response_tf(approx, wavelength, pixel_pitch, distance, M, t);
+    }
+    std::vector<lr_c64> hc(t.size());
+    for (size_t i = 0; i < t.size(); ++i)
+      hc[i] = lr_c64{static_cast<float>(t[i].real()), static_cast<float>(t[i].imag())};
+    if (hipMemcpyAsync(d_H, hc.data(), hc.size() * sizeof(lr_c64), hipMemcpyHostToDevice, st) != hipSuccess)
+      return LR_E_HIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return LR_E_HIP;
+    return LR_OK;
+  }
   const double lam = wavelength;
   const double z = distance;
   const double kz = kTwoPi * z / lam;
@@ -420,7 +566,6 @@ int lr_tf_build(double wavelength, double pixel_pitch, double distance, int32_t 
       h[static_cast<size_t>(ky) * M + kx] = lr_c64{static_cast<float>(re), static_cast<float>(im)};
     }
   }
-  hipStream_t st = static_cast<hipStream_t>(stream);
   if (hipMemcpyAsync(d_H, h.data(), h.size() * sizeof(lr_c64), hipMemcpyHostToDevice, st) != hipSuccess)
     return LR_E_HIP;
   if (hipStreamSynchronize(st) != hipSuccess) return LR_E_HIP;
@@ -449,6 +594,7 @@ int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* 
   if (batch == 0) return LR_OK;
   if (!d_in || !d_out) return LR_E_NULL;
   if (static_cast<const void*>(d_in) == static_cast<const void*>(d_out)) return LR_E_ALIAS;
+  if (net->approx == LR_FRAUNHOFER && adjoint) return LR_E_ARG;
   Layout L;
   LR_TRY(check_work(net, batch, LR_OP_PROPAGATE, d_work, work_bytes, &L));
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -473,6 +619,15 @@ int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* 
   a.ntiles = L.ntiles_vec;
   a.out = at<float2>(d_work, L.w0);
   LR_TRY(as_pass(N, lr::kAsRowFirst, a, st));
+  if (net->approx == LR_FRAUNHOFER) {
+    // far field: the column DFT with the output factors, straight into d_out ([batch][N][N])
+    a.in = at<float2>(d_work, L.w0);
+    a.out = reinterpret_cast<float2*>(d_out);
+    a.nvec = N;
+    a.ntiles = L.ntiles_spec;
+    a.tab = at<float2>(d_work, L.hp);
+    return as_pass(N, lr::kAsColFar, a, st);
+  }
   a.in = at<float2>(d_work, L.w0);
   a.out = at<float2>(d_work, L.w1);
   a.nvec = N;

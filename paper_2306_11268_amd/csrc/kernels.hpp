@@ -32,6 +32,7 @@ enum AsPassKind : int {
   kAsRowBwdMid = 5,  // rows: IFFT_x -> crop -> dphi_l -> x conj(M_l) -> pad -> FFT_x
   kAsRowBwdLast = 6, // rows: IFFT_x -> crop -> dphi_1
   kAsRowIfft = 7,    // rows: IFFT_x -> crop -> store field (plain propagation)
+  kAsColFar = 8,     // columns: pad -> FFT_y -> x table -> store [N][N], both indices shifted by N/2
 };
 
 struct PassArgs {
@@ -114,7 +115,8 @@ int fresnel_pass_tile(int N, PassKind kind, Axis axis);
 hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t st);
 
 // Small helper kernels.
-hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, hipStream_t st);
+// Hp[ky][c] = scale * H[ky][kx(c)] (columns in the row plan's slot order).
+hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, float scale, hipStream_t st);
 hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, float* sums, hipStream_t st);
 // Loss of the detector sums (kind 0: softmax cross-entropy, 1: squared norm
 // of softmax minus one-hot), mean over the batch, and dL/dS; grad and loss

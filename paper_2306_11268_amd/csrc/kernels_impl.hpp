@@ -981,6 +981,32 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
       store_a_direct<C>(a.out + (size_t)b * n * N, N, n, off, vec, vok, x);
       continue;
     }
+    if constexpr (KIND == kAsColFar) {
+      // unnormalised DFT along y of the x-spectrum column vec (row-plan slot
+      // order); frequency (ky, kx) goes to [(ky + N/2) mod N][(kx + N/2) mod N]
+      // times the table (which carries the far-field factors)
+      const float2* __restrict__ in = static_cast<const float2*>(a.in) + (size_t)b * n * N;
+      __syncthreads();
+      load_a_direct<C>(in, N, n, off, vec, vok, x);
+      Dft<N1, -1>::run(x);
+      write_a(t, j, x);
+      __syncthreads();
+      b_forward_all<C>(t);
+      __syncthreads();
+      if (vok) {
+        using RPL = typename RowPlanFor<N>::type;
+        const int kx = RPL::freq(vec / RPL::N2, vec % RPL::N2);
+        const int ocol = kx + N / 2 < N ? kx + N / 2 : kx - N / 2;
+        float2* __restrict__ out = a.out + (size_t)b * N * N;
+#pragma unroll 4
+        for (int ky = t.s; ky < N; ky += C::S) {
+          const float2 v = t.lds[PL::slot_of_freq(ky) * C::TP + t.v];
+          const int orow = ky + N / 2 < N ? ky + N / 2 : ky - N / 2;
+          st(out, orow * N + ocol, cmul(v, ld(a.tab, ky * N + vec)));
+        }
+      }
+      continue;
+    }
 
     // ---- row passes: vectors are layer rows y = vec0 + v
     __syncthreads();
@@ -1049,12 +1075,12 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
 // ---------------------------------------------------------------------------
 
 // Column-permuted 2-D table for the angular-spectrum column pass:
-// Hp[ky][c] = H[ky][kx(c)] / N^2, c the slot of frequency kx in the row plan
-// (the layout in which row passes store x-spectra).
+// Hp[ky][c] = inv * H[ky][kx(c)] (inv = 1/N^2 for a propagation, 1 for the
+// far-field table), c the slot of frequency kx in the row plan (the layout
+// in which row passes store x-spectra).
 template <class PL>
-__global__ void prep_as_table_kernel(const float2* __restrict__ H, float2* __restrict__ Hp) {
+__global__ void prep_as_table_kernel(const float2* __restrict__ H, float2* __restrict__ Hp, float inv) {
   constexpr int N = PL::N;
-  const float inv = 1.0f / ((float)N * (float)N);
   const size_t total = (size_t)N * N;
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
     const int ky = (int)(i / N);
@@ -1213,7 +1239,7 @@ hipError_t launch_fr_n(PassKind kind, Axis axis, const PassArgs& a, hipStream_t 
 
 template <int N, int KIND>
 hipError_t launch_as(const PassArgs& a, hipStream_t st) {
-  using C = std::conditional_t<KIND == kAsCol, CfgFor<N>, RowCfgFor<N>>;
+  using C = std::conditional_t<KIND == kAsCol || KIND == kAsColFar, CfgFor<N>, RowCfgFor<N>>;
   const dim3 grid(work_grid(a.ntiles, (a.batch + a.spg - 1) / a.spg));
   hipLaunchKernelGGL((as_pass<C, KIND>), grid, dim3(C::P), 0, st, a);
   return hipGetLastError();
@@ -1230,15 +1256,16 @@ hipError_t launch_as_n(AsPassKind kind, const PassArgs& a, hipStream_t st) {
     case kAsRowBwdMid: return launch_as<N, kAsRowBwdMid>(a, st);
     case kAsRowBwdLast: return launch_as<N, kAsRowBwdLast>(a, st);
     case kAsRowIfft: return launch_as<N, kAsRowIfft>(a, st);
+    case kAsColFar: return launch_as<N, kAsColFar>(a, st);
   }
   return hipErrorInvalidValue;
 }
 
 template <int N>
-hipError_t prep_as_n(const float2* H, float2* Hp, hipStream_t st) {
+hipError_t prep_as_n(const float2* H, float2* Hp, float scale, hipStream_t st) {
   const int blocks = (int)(((size_t)N * N + 255) / 256);
   hipLaunchKernelGGL((prep_as_table_kernel<typename RowPlanFor<N>::type>), dim3(blocks < 4096 ? blocks : 4096), dim3(256),
-                     0, st, H, Hp);
+                     0, st, H, Hp, scale);
   return hipGetLastError();
 }
 

@@ -58,7 +58,8 @@ def test_status_strings_and_version():
 @needs_lib
 @pytest.mark.parametrize("kw,status", [
     (dict(wavelength=float("nan")), 3), (dict(wavelength=-1.0), 3), (dict(pixel_pitch=0.0), 3),
-    (dict(distance=float("inf")), 3), (dict(approx=2), 4), (dict(n_fft=201, n=201), 2),
+    (dict(distance=float("inf")), 3), (dict(approx=5), 4), (dict(approx=-1), 4), (dict(approx=4), 4),
+    (dict(n_fft=201, n=201), 2),
     (dict(n=202), 2), (dict(n=199), 2), (dict(n=0), 2), (dict(num_layers=0), 2), (dict(num_layers=65), 2),
     (dict(gamma=float("nan")), 3), (dict(d_H=ctypes.c_void_p(0)), 1),
 ])
@@ -102,6 +103,17 @@ def test_entry_points_reject_bad_arguments_without_touching_the_gpu():
     assert lib.lr_tf_build(0.0, 36e-6, 0.3, 0, 64, dummy, None) == 3
     assert lib.lr_tf_build(532e-9, 36e-6, 0.3, 5, 64, dummy, None) == 4
     assert lib.lr_tf_build(532e-9, 36e-6, 0.3, 0, 0, dummy, None) == 2
+    # sampled kernels: lengths with a prime factor above 5, non-positive distance; far field: odd grid
+    assert lib.lr_tf_build(532e-9, 36e-6, 0.3, 2, 14, dummy, None) == 2
+    assert lib.lr_tf_build(532e-9, 36e-6, 0.0, 3, 64, dummy, None) == 3
+    assert lib.lr_tf_build(532e-9, 36e-6, 0.3, 4, 63, dummy, None) == 2
+    assert lib.lr_tf_build(532e-9, 36e-6, -1.0, 4, 64, dummy, None) == 3
+    # the far field propagates only, forwards only
+    far = _net(approx=4)
+    assert _ws(far, 4, 0) > 0
+    assert _ws(far, 4, 1) == -4 and _ws(far, 4, 2) == -4
+    assert lib.lr_propagate(ctypes.byref(far), 2, dummy, P(0x3000), 1, dummy, 1 << 30, None) == 3
+    assert _ws(_net(approx=5), 4, 0) == -4
     # propagate: null fields, aliasing, missing / short workspace
     assert lib.lr_propagate(ref, 2, None, dummy, 0, dummy, 1 << 30, None) == 1
     assert lib.lr_propagate(ref, 2, dummy, dummy, 0, dummy, 1 << 30, None) == 7
