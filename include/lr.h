@@ -113,7 +113,20 @@ typedef struct lr_donn {
   const lr_c64* d_H;    /* device [n_fft][n_fft], written by lr_tf_build for the same
                            wavelength / pixel_pitch / distance / approx / n_fft.
                            The Fresnel path relies on its separability. */
+  int32_t flags;        /* 0 or LR_ACCUMULATE */
 } lr_donn;
+
+/* lr_donn.flags: lr_donn_forward adds its detector sums and intensity map
+ * into d_sums / d_intensity instead of overwriting them (d_field_out must
+ * then be NULL).  This is the detector of the multi-channel DONN of §5.6.1:
+ * several optical channels (each an lr_donn with its own masks and input)
+ * project onto one detector, where their intensities add.  A training step
+ * of such a system runs lr_donn_forward per channel (the first without,
+ * the others with LR_ACCUMULATE, or all with it on zeroed outputs),
+ * lr_loss on the merged sums, and lr_donn_backward per channel with the
+ * same d_grad_sums: the merged sums are the sum of the channels' sums, so
+ * every channel receives the whole dL/dS. */
+#define LR_ACCUMULATE 1
 
 /* Transfer function of one hop (§3.1.1, Eqs. (fresnel), (sommerfeld), (r01),
  * (forward_diff), (fraunhofer)).

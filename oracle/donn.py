@@ -375,6 +375,27 @@ def donn_backward(fwd: dict, phi: np.ndarray, h: np.ndarray, gamma: float = 1.0,
 # trained with Adam, learning rate 0.5, batch 500).
 # ---------------------------------------------------------------------------
 
+def multichannel_forward(amps: Sequence[np.ndarray], phis: Sequence[np.ndarray], h: np.ndarray, gamma: float,
+                         det: Detector):
+    """Multi-channel DONN (§5.6.1): channel c is a DONN with its own masks
+    phis[c] on its own input amps[c]; the channels project onto one detector,
+    where their intensities add, so the merged region sums are the sum of the
+    channels' sums.  Returns (per-channel forward dicts, merged sums)."""
+    fwds = [donn_forward(a, p, h, gamma, det) for a, p in zip(amps, phis)]
+    merged = fwds[0]["sums"].copy()
+    for f in fwds[1:]:
+        merged = merged + f["sums"]
+    return fwds, merged
+
+
+def multichannel_backward(fwds, phis: Sequence[np.ndarray], h: np.ndarray, gamma: float, det: Detector,
+                          grad_sums: np.ndarray):
+    """dL/dphi of every channel for an upstream dL/dS of the merged sums: the
+    merged sums depend on each channel's sums with unit weight, so every
+    channel's backward pass receives the same dL/dS."""
+    return [donn_backward(f, p, h, gamma, det, grad_sums=grad_sums) for f, p in zip(fwds, phis)]
+
+
 def adam_update(phi: np.ndarray, grad: np.ndarray, m: np.ndarray, v: np.ndarray, step: int,
                 lr: float = 0.5, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8):
     """One Adam step (Kingma and Ba, 2014, Algorithm 1) on the phase masks.

@@ -20,6 +20,7 @@ LR_ANGULAR_SPECTRUM = 1
 LR_FRESNEL_IR = 2
 LR_RS_IR = 3
 LR_FRAUNHOFER = 4
+LR_ACCUMULATE = 1
 LR_OP_PROPAGATE = 0
 LR_OP_FORWARD = 1
 LR_OP_BACKWARD = 2
@@ -42,7 +43,7 @@ class LrDonn(ctypes.Structure):
     _fields_ = [
         ("wavelength", c_double), ("pixel_pitch", c_double), ("distance", c_double),
         ("approx", c_int32), ("n", c_int32), ("n_fft", c_int32), ("num_layers", c_int32),
-        ("gamma", c_float), ("det", LrDetector), ("d_H", c_void_p),
+        ("gamma", c_float), ("det", LrDetector), ("d_H", c_void_p), ("flags", c_int32),
     ]
 
 
@@ -240,12 +241,21 @@ def lr_detector_readout(field, detector: Detector, out=None):
 
 
 def lr_donn_forward(net: Network, amp, phi, saved=None, sums: bool = True, intensity: bool = False,
-                    field: bool = False, out_sums=None, out_intensity=None, out_field=None):
-    """Forward pass; returns a dict with the requested outputs (device tensors)."""
+                    field: bool = False, out_sums=None, out_intensity=None, out_field=None,
+                    accumulate: bool = False):
+    """Forward pass; returns a dict with the requested outputs (device tensors).
+    With accumulate the sums / intensity are added into out_sums / out_intensity
+    (LR_ACCUMULATE), which must then be given."""
     torch = _torch()
     b = int(amp.shape[0])
     n, L = net.n, net.num_layers
     dev = net.device
+    desc = net.c
+    if accumulate:
+        if (sums and out_sums is None) or (intensity and out_intensity is None) or field:
+            raise ValueError("accumulate needs out_sums / out_intensity and no field output")
+        desc = LrDonn.from_buffer_copy(net.c)
+        desc.flags = LR_ACCUMULATE
     if sums and net.detector.num > 0 and out_sums is None:
         out_sums = torch.empty((b, net.detector.num), dtype=torch.float32, device=dev)
     if intensity and out_intensity is None:
@@ -256,7 +266,7 @@ def lr_donn_forward(net: Network, amp, phi, saved=None, sums: bool = True, inten
     if saved is not None and saved.numel() < net.saved_size(b):
         raise ValueError("saved buffer too small")
     _check(load().lr_donn_forward(
-        ctypes.byref(net.c), b,
+        ctypes.byref(desc), b,
         _ptr(amp, torch.float32, (b, n, n), "amp"), _ptr(phi, torch.float32, (L, n, n), "phi"),
         _ptr(saved, torch.uint8, None, "saved"),
         _ptr(out_sums, torch.float32, None, "sums"), _ptr(out_intensity, torch.float32, None, "intensity"),
@@ -325,3 +335,20 @@ def kernel_timing_report() -> dict:
     buf = ctypes.create_string_buffer(need + 1)
     lib.lr_kernel_timing_report(buf, need + 1)
     return json.loads(buf.value.decode())
+
+
+def multichannel_train_step(nets, amps, phis, saveds, labels, kind: int = LR_LOSS_SOFTMAX_CE):
+    """One training step of the multi-channel DONN of §5.6.1 through the C ABI.
+
+    Channel c (its own lr_donn, masks phis[c] and input amps[c]) runs its
+    forward pass; the detector sums of all channels add into one merged
+    array (LR_ACCUMULATE from the second channel on), the loss is taken on
+    the merged sums, and every channel's backward pass receives the same
+    dL/dS.  Returns (loss, merged sums, [dL/dphi of each channel])."""
+    merged = None
+    for c, (net, amp, phi, saved) in enumerate(zip(nets, amps, phis, saveds)):
+        merged = lr_donn_forward(net, amp, phi, saved=saved, sums=True, out_sums=merged, accumulate=c > 0)["sums"]
+    loss, grad_sums = lr_loss(merged, labels, kind=kind)
+    grads = [lr_donn_backward(net, phi, saved, grad_sums=grad_sums)[0]
+             for net, phi, saved in zip(nets, phis, saveds)]
+    return loss, merged, grads

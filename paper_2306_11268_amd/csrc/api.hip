@@ -106,6 +106,7 @@ int validate_detector(const lr_detector& d, int n) {
 
 int validate_net(const lr_donn* net, bool need_layers) {
   if (!net) return LR_E_NULL;
+  if (net->flags & ~LR_ACCUMULATE) return LR_E_ARG;
   if (!finite_pos(net->wavelength) || !finite_pos(net->pixel_pitch) || !std::isfinite(net->distance))
     return LR_E_ARG;
   if (net->approx < LR_FRESNEL || net->approx > LR_FRAUNHOFER) return LR_E_APPROX;
@@ -663,6 +664,8 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   if (batch == 0) return LR_OK;
   if (!d_amp || !d_phi) return LR_E_NULL;
   if (d_sums && net->det.num == 0) return LR_E_ARG;
+  const bool accumulate = (net->flags & LR_ACCUMULATE) != 0;
+  if (accumulate && d_field_out) return LR_E_ARG;  // fields of separate channels do not add
   Layout L;
   LR_TRY(check_work(net, batch, LR_OP_FORWARD, d_work, work_bytes, &L));
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -677,6 +680,7 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   LR_TRY(prep_layers(net, d_phi, d_sums != nullptr, L, d_work, st));
 
   PassArgs a = base_args(net, batch);
+  a.accumulate = accumulate ? 1 : 0;
   const int tile_t = lr::tile_shape(N, 0).T;
   int sum_tiles = L.ntiles_vec;  // tiles that wrote partial detector sums
   if (net->approx == LR_FRESNEL) {
@@ -763,7 +767,8 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   }
   if (d_sums) {
     LR_TRY(run_timed("finish_sums", st, [&] {
-      return lr::launch_finish_sums(at<float>(d_work, L.sums_part), batch, sum_tiles, net->det.num, d_sums, st);
+      return lr::launch_finish_sums(at<float>(d_work, L.sums_part), batch, sum_tiles, net->det.num, d_sums,
+                                    accumulate ? 1 : 0, st);
     }));
   }
   return LR_OK;

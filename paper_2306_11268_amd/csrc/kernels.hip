@@ -37,14 +37,15 @@ __device__ __forceinline__ void prep_mod_body(const float* __restrict__ phi, int
   }
 }
 
-__global__ void finish_sums_kernel(const float* __restrict__ part, int batch, int ntiles, int K, float* __restrict__ sums) {
+__global__ void finish_sums_kernel(const float* __restrict__ part, int batch, int ntiles, int K, float* __restrict__ sums,
+                                   int accumulate) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= batch * K) return;
   const int b = i / K;
   const int k = i - b * K;
   float s = 0.f;
   for (int tl = 0; tl < ntiles; ++tl) s += part[((size_t)b * ntiles + tl) * K + k];
-  sums[i] = s;
+  sums[i] = accumulate ? sums[i] + s : s;
 }
 
 // Loss of the detector sums, averaged over the batch, and its gradient
@@ -393,9 +394,11 @@ hipError_t launch_prep_layers(const float* phi, int layers, int n, float gamma, 
   return hipGetLastError();
 }
 
-hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, float* sums, hipStream_t st) {
+hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, float* sums, int accumulate,
+                              hipStream_t st) {
   const int total = batch * K;
-  hipLaunchKernelGGL(finish_sums_kernel, dim3((total + 255) / 256), dim3(256), 0, st, part, batch, ntiles, K, sums);
+  hipLaunchKernelGGL(finish_sums_kernel, dim3((total + 255) / 256), dim3(256), 0, st, part, batch, ntiles, K, sums,
+                     accumulate);
   return hipGetLastError();
 }
 

@@ -88,6 +88,7 @@ struct PassArgs {
   // row_mask[y] / col_mask[x] have bit k set when region k covers row y / column x
   int K;
   int det_size;
+  int accumulate;  // detector-plane intensity is added to the output instead of stored
   const int2* regions;
   const unsigned long long* row_mask;
   const unsigned long long* col_mask;
@@ -117,7 +118,9 @@ hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t
 // Small helper kernels.
 // Hp[ky][c] = scale * H[ky][kx(c)] (columns in the row plan's slot order).
 hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, float scale, hipStream_t st);
-hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, float* sums, hipStream_t st);
+// sums[b][k] = (accumulate ? sums[b][k] : 0) + the per-tile partial sums, in tile order.
+hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, float* sums, int accumulate,
+                              hipStream_t st);
 // Loss of the detector sums (kind 0: softmax cross-entropy, 1: squared norm
 // of softmax minus one-hot), mean over the batch, and dL/dS; grad and loss
 // are nullable.

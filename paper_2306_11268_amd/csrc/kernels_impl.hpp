@@ -415,7 +415,7 @@ __device__ __forceinline__ void tile_outputs(const float2* lds, float* rsum, con
             const int idx = nat_index<AXIS>(n, vf(v), q);
             if (fo) st(fo, idx, buf[i.value]);
             if (sv) st(sv, idx, buf[i.value]);
-            if (io) st(io, idx, cabs2(buf[i.value]));
+            if (io) st(io, idx, a.accumulate ? ld(io, idx) + cabs2(buf[i.value]) : cabs2(buf[i.value]));
           }
         });
   }

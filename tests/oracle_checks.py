@@ -491,3 +491,44 @@ def fraunhofer_rectangle(lam=LAM, dx=DX, z=5.0, m=64, a=6, b=10):
 
     ref = np.outer(dirichlet(a), dirichlet(b)) * dx * dx / (lam * z)
     return rel(got, ref)
+
+
+def multichannel_grad_fd(channels=3):
+    """Central finite differences of the cross-entropy of the merged sums of a
+    multi-channel DONN against multichannel_backward, over every phase entry
+    of every channel."""
+    amp, phi, h, gamma, det, t, gi = _tiny_net(n=10, m=10, L=2, B=3)
+    g = np.random.default_rng(41)
+    amps = [amp] + [g.uniform(0, 1, amp.shape) for _ in range(channels - 1)]
+    phis = [phi] + [g.uniform(0, 2 * np.pi, phi.shape) for _ in range(channels - 1)]
+
+    def loss(ph):
+        return od.softmax_cross_entropy(od.multichannel_forward(amps, ph, h, gamma, det)[1], t)[0]
+
+    fwds, merged = od.multichannel_forward(amps, phis, h, gamma, det)
+    _, gs = od.softmax_cross_entropy(merged, t)
+    grads = od.multichannel_backward(fwds, phis, h, gamma, det, gs)
+    eps = 1e-6
+    worst = 0.0
+    for c in range(channels):
+        fd = np.zeros_like(phis[c])
+        for idx in np.ndindex(phis[c].shape):
+            pp = [p.copy() for p in phis]
+            pm = [p.copy() for p in phis]
+            pp[c][idx] += eps
+            pm[c][idx] -= eps
+            fd[idx] = (loss(pp) - loss(pm)) / (2 * eps)
+        worst = max(worst, rel(grads[c], fd))
+    return worst
+
+
+def multichannel_sums_add():
+    """The merged sums are the channels' sums added, and one channel is the plain network."""
+    amp, phi, h, gamma, det, t, gi = _tiny_net(n=10, m=12, L=2, B=2)
+    g = np.random.default_rng(42)
+    amps = [amp, g.uniform(0, 1, amp.shape)]
+    phis = [phi, g.uniform(0, 2 * np.pi, phi.shape)]
+    _, merged = od.multichannel_forward(amps, phis, h, gamma, det)
+    parts = [od.detector_readout(od.intensity(od.donn_forward(a, p, h, gamma)["field"]), det) for a, p in zip(amps, phis)]
+    one = od.multichannel_forward(amps[:1], phis[:1], h, gamma, det)[1]
+    return max(rel(merged, parts[0] + parts[1]), rel(one, od.donn_forward(amp, phi, h, gamma, det)["sums"]))

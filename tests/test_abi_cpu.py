@@ -114,6 +114,14 @@ def test_entry_points_reject_bad_arguments_without_touching_the_gpu():
     assert _ws(far, 4, 1) == -4 and _ws(far, 4, 2) == -4
     assert lib.lr_propagate(ctypes.byref(far), 2, dummy, P(0x3000), 1, dummy, 1 << 30, None) == 3
     assert _ws(_net(approx=5), 4, 0) == -4
+    # flags: unknown bits; accumulating outputs cannot include the field
+    bad = _net()
+    bad.flags = 2
+    assert _ws(bad, 4, 1) == -3
+    acc = _net(det=lb.LrDetector(0, 1, None, None))
+    acc.flags = 1
+    assert lib.lr_donn_forward(ctypes.byref(acc), 2, dummy, dummy, None, None, None, P(0x3000), dummy, 1 << 30,
+                               None) == 3
     # propagate: null fields, aliasing, missing / short workspace
     assert lib.lr_propagate(ref, 2, None, dummy, 0, dummy, 1 << 30, None) == 1
     assert lib.lr_propagate(ref, 2, dummy, dummy, 0, dummy, 1 << 30, None) == 7

@@ -239,3 +239,44 @@ def test_cross_entropy_step_depth_and_grid_variants(lrb, n, layers, b):
     ref_grad = od.donn_backward(ref, phi, h, 1.0, odet(w.detector), grad_sums=gs)
     assert abs(float(loss) - ref_loss) / abs(ref_loss) < TOL_FIELD
     assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+# The multi-channel DONN of §5.6.1: three channels (own masks, own inputs)
+# whose intensities add at one detector, trained on the shared loss.
+def test_multichannel_training_step(lrb):
+    w = wl.WORKLOADS[3]
+    b, layers, channels = 4, 5, 3
+    det = w.detector
+    g = np.random.default_rng(7)
+    amps = [wl.amplitudes(w, b)] + [g.uniform(0, 1, (b, w.n, w.n)).astype(np.float32) for _ in range(channels - 1)]
+    phis = [wl.phases(w)] + [g.uniform(0, 2 * np.pi, (layers, w.n, w.n)).astype(np.float32)
+                             for _ in range(channels - 1)]
+    nets = [lrb.Network(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n, w.n_fft, layers, 1.0,
+                        lrb.Detector(det.size, det.y0, det.x0)) for _ in range(channels)]
+    saveds = [net.new_saved(b) for net in nets]
+    labels = wl.labels(w, b)
+    loss, merged, grads = lrb.multichannel_train_step(nets, [dev(a) for a in amps], [dev(p) for p in phis], saveds,
+                                                      dev(labels))
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
+    fwds, ref_merged = od.multichannel_forward(amps, phis, h, 1.0, odet(det))
+    ref_loss, gs = od.softmax_cross_entropy(ref_merged, labels)
+    ref_grads = od.multichannel_backward(fwds, phis, h, 1.0, odet(det), gs)
+    assert rel(host(merged), ref_merged) < TOL_FIELD
+    assert abs(float(loss) - ref_loss) / abs(ref_loss) < TOL_FIELD
+    for gr, rg in zip(grads, ref_grads):
+        assert rel(host(gr), rg) < TOL_GRAD
+
+
+def test_accumulated_intensity_maps(lrb):
+    w = wl.WORKLOADS[2]
+    b = 3
+    g = np.random.default_rng(8)
+    amps = [wl.amplitudes(w, b), g.uniform(0, 1, (b, w.n, w.n)).astype(np.float32)]
+    phis = [wl.phases(w), g.uniform(0, 2 * np.pi, (w.layers, w.n, w.n)).astype(np.float32)]
+    net = lrb.Network(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n, w.n_fft, w.layers)
+    out = lrb.lr_donn_forward(net, dev(amps[0]), dev(phis[0]), sums=False, intensity=True)
+    lrb.lr_donn_forward(net, dev(amps[1]), dev(phis[1]), sums=False, intensity=True,
+                        out_intensity=out["intensity"], accumulate=True)
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
+    ref = sum(od.donn_forward(a, p, h, 1.0)["intensity"] for a, p in zip(amps, phis))
+    assert rel(host(out["intensity"]), ref) < TOL_FIELD

@@ -15,7 +15,8 @@ _orig = {name: getattr(od, name) for name in (
     "dft_matrix", "idft2", "transfer_function", "frequencies", "propagate",
     "modulate", "detector_readout", "region_scatter", "softmax_cross_entropy",
     "mse_softmax_loss", "donn_forward", "donn_backward", "adam_update",
-    "impulse_response", "displacements", "fraunhofer", "fraunhofer_pitch")}
+    "impulse_response", "displacements", "fraunhofer", "fraunhofer_pitch",
+    "multichannel_forward", "multichannel_backward")}
 
 
 def _dft_sign_flipped(m, inverse=False):
@@ -184,6 +185,15 @@ def _fraunhofer_pitch_no_m(lam, dx, z, m):
     return lam * z / dx
 
 
+def _multichannel_sums_averaged(amps, phis, h, gamma, det):
+    fwds, merged = _orig["multichannel_forward"](amps, phis, h, gamma, det)
+    return fwds, merged / len(fwds)
+
+
+def _multichannel_grad_split(fwds, phis, h, gamma, det, grad_sums):
+    return _orig["multichannel_backward"](fwds, phis, h, gamma, det, grad_sums / len(fwds))
+
+
 MUTANTS = [
     ("dft_sign", "dft_matrix", _dft_sign_flipped, lambda: c.dft_vs_numpy() > 1e-3),
     ("idft_norm", "idft2", _idft_unnormalised, lambda: c.dft_delta_parseval() > 1e-3),
@@ -207,6 +217,10 @@ MUTANTS = [
     ("fraunhofer_uncentred", "fraunhofer", _fraunhofer_output_uncentred, lambda: c.fraunhofer_rectangle() > 1e-3),
     ("fraunhofer_no_chirp", "fraunhofer", _fraunhofer_no_output_chirp, lambda: c.fraunhofer_vs_fresnel_sum() > 1e-3),
     ("fraunhofer_pitch", "fraunhofer_pitch", _fraunhofer_pitch_no_m, lambda: c.fraunhofer_vs_fresnel_sum() > 1e-3),
+    ("multichannel_sums_averaged", "multichannel_forward", _multichannel_sums_averaged,
+     lambda: c.multichannel_sums_add() > 1e-3),
+    ("multichannel_grad_split", "multichannel_backward", _multichannel_grad_split,
+     lambda: c.multichannel_grad_fd() > 1e-3),
     ("adam_no_bias_correction", "adam_update", _adam_no_bias_correction, lambda: c.adam_first_step() > 1e-3),
     ("adam_eps_inside_sqrt", "adam_update", _adam_eps_inside_sqrt, lambda: c.adam_constant_gradient() > 1e-3),
     ("adam_betas_swapped", "adam_update", _adam_betas_swapped, lambda: c.adam_vs_torch() > 1e-3),

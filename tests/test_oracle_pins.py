@@ -158,3 +158,12 @@ def test_fraunhofer_rectangle_dirichlet_kernel():
 
 def test_fraunhofer_output_pitch():
     assert abs(od.fraunhofer_pitch(532e-9, 36e-6, 1.0, 100) - 532e-9 / (100 * 36e-6)) < 1e-20
+
+
+def test_multichannel_sums_add():
+    assert c.multichannel_sums_add() < 1e-13
+
+
+def test_multichannel_gradients_by_finite_differences():
+    # central differences with step 1e-6 in float64: ~1e-8 truncation and rounding
+    assert c.multichannel_grad_fd() < 1e-6
