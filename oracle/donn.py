@@ -396,6 +396,38 @@ def multichannel_backward(fwds, phis: Sequence[np.ndarray], h: np.ndarray, gamma
     return [donn_backward(f, p, h, gamma, det, grad_sums=grad_sums) for f, p in zip(fwds, phis)]
 
 
+def codesign_phase(logits: np.ndarray, noise: np.ndarray, levels: np.ndarray, tau: float, hard: bool = False):
+    """Hardware-level phase of the codesign layer (§3.2: the measured,
+    discrete device responses mapped with Gumbel-Softmax).
+
+    logits, noise [..., K]: per-pixel scores of the K device levels and the
+    Gumbel(0, 1) draws; levels [K]: the device's phase values (radians).
+    w = softmax((logits + noise) / tau) over K; the phase is sum_k w_k
+    levels_k, or with ``hard`` the level of the largest logits + noise (the
+    straight-through estimator keeps the soft w for the gradient).
+    Returns (phi [...], w [..., K])."""
+    y = (np.asarray(logits, np.float64) + np.asarray(noise, np.float64)) / tau
+    y = y - y.max(axis=-1, keepdims=True)
+    e = np.exp(y)
+    w = e / e.sum(axis=-1, keepdims=True)
+    lv = np.asarray(levels, np.float64)
+    if hard:
+        phi = lv[np.argmax(np.asarray(logits, np.float64) + np.asarray(noise, np.float64), axis=-1)]
+    else:
+        phi = w @ lv
+    return phi, w
+
+
+def codesign_backward(w: np.ndarray, levels: np.ndarray, tau: float, grad_phi: np.ndarray) -> np.ndarray:
+    """dL/dlogits of the codesign layer from dL/dphi through the softmax
+    Jacobian of the soft phase sum_k w_k levels_k (also the straight-through
+    gradient of the hard layer):
+    dL/dlogit_j = w_j (levels_j - sum_k w_k levels_k) dL/dphi / tau."""
+    lv = np.asarray(levels, np.float64)
+    mean = w @ lv
+    return w * (lv - mean[..., None]) * (np.asarray(grad_phi, np.float64)[..., None] / tau)
+
+
 def adam_update(phi: np.ndarray, grad: np.ndarray, m: np.ndarray, v: np.ndarray, step: int,
                 lr: float = 0.5, beta1: float = 0.9, beta2: float = 0.999, eps: float = 1e-8):
     """One Adam step (Kingma and Ba, 2014, Algorithm 1) on the phase masks.

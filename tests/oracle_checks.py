@@ -532,3 +532,49 @@ def multichannel_sums_add():
     parts = [od.detector_readout(od.intensity(od.donn_forward(a, p, h, gamma)["field"]), det) for a, p in zip(amps, phis)]
     one = od.multichannel_forward(amps[:1], phis[:1], h, gamma, det)[1]
     return max(rel(merged, parts[0] + parts[1]), rel(one, od.donn_forward(amp, phi, h, gamma, det)["sums"]))
+
+
+# --- codesign layer (Gumbel-Softmax over device levels) ---------------------
+
+def _codesign_case(K=16, shape=(3, 5), seed=51):
+    g = np.random.default_rng(seed)
+    logits = g.standard_normal(shape + (K,))
+    u = g.uniform(1e-12, 1.0, shape + (K,))
+    noise = -np.log(-np.log(u))
+    levels = np.sort(g.uniform(0.0, 2.0 * np.pi, K))
+    return logits, noise, levels
+
+
+def codesign_limits():
+    """Uniform scores give the mean level; a low temperature gives the level
+    of the largest score (the hard layer); the soft phase stays in the
+    levels' range; the gradient over the K scores of a pixel sums to zero
+    (softmax is invariant to a common shift)."""
+    logits, noise, levels = _codesign_case()
+    e1 = abs(od.codesign_phase(np.zeros(8), np.zeros(8), levels[:8], 1.0)[0] - np.mean(levels[:8]))
+    soft, _ = od.codesign_phase(logits, noise, levels, 1e-4)
+    hard, _ = od.codesign_phase(logits, noise, levels, 1.0, hard=True)
+    e2 = float(np.max(np.abs(soft - hard)))
+    phi, w = od.codesign_phase(logits, noise, levels, 0.7)
+    e3 = float(max(0.0, levels.min() - phi.min(), phi.max() - levels.max()))
+    gl = od.codesign_backward(w, levels, 0.7, np.ones(phi.shape))
+    e4 = float(np.max(np.abs(gl.sum(axis=-1))))
+    return max(e1, e2, e3, e4)
+
+
+def codesign_grad_fd(tau=0.7):
+    """Central finite differences of L = sum c * phi against codesign_backward."""
+    logits, noise, levels = _codesign_case(K=6, shape=(2, 3))
+    c = np.random.default_rng(52).standard_normal((2, 3))
+    _, w = od.codesign_phase(logits, noise, levels, tau)
+    got = od.codesign_backward(w, levels, tau, c)
+    eps = 1e-6
+    fd = np.zeros_like(logits)
+    for idx in np.ndindex(logits.shape):
+        lp = logits.copy()
+        lm = logits.copy()
+        lp[idx] += eps
+        lm[idx] -= eps
+        fd[idx] = (np.sum(c * od.codesign_phase(lp, noise, levels, tau)[0]) -
+                   np.sum(c * od.codesign_phase(lm, noise, levels, tau)[0])) / (2 * eps)
+    return rel(got, fd)

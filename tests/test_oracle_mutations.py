@@ -16,7 +16,7 @@ _orig = {name: getattr(od, name) for name in (
     "modulate", "detector_readout", "region_scatter", "softmax_cross_entropy",
     "mse_softmax_loss", "donn_forward", "donn_backward", "adam_update",
     "impulse_response", "displacements", "fraunhofer", "fraunhofer_pitch",
-    "multichannel_forward", "multichannel_backward")}
+    "multichannel_forward", "multichannel_backward", "codesign_phase", "codesign_backward")}
 
 
 def _dft_sign_flipped(m, inverse=False):
@@ -194,6 +194,15 @@ def _multichannel_grad_split(fwds, phis, h, gamma, det, grad_sums):
     return _orig["multichannel_backward"](fwds, phis, h, gamma, det, grad_sums / len(fwds))
 
 
+def _codesign_no_temperature(logits, noise, levels, tau, hard=False):
+    return _orig["codesign_phase"](logits, noise, levels, 1.0, hard)
+
+
+def _codesign_backward_no_centering(w, levels, tau, grad_phi):
+    lv = np.asarray(levels, np.float64)
+    return w * lv * (np.asarray(grad_phi, np.float64)[..., None] / tau)
+
+
 MUTANTS = [
     ("dft_sign", "dft_matrix", _dft_sign_flipped, lambda: c.dft_vs_numpy() > 1e-3),
     ("idft_norm", "idft2", _idft_unnormalised, lambda: c.dft_delta_parseval() > 1e-3),
@@ -221,6 +230,9 @@ MUTANTS = [
      lambda: c.multichannel_sums_add() > 1e-3),
     ("multichannel_grad_split", "multichannel_backward", _multichannel_grad_split,
      lambda: c.multichannel_grad_fd() > 1e-3),
+    ("codesign_no_temperature", "codesign_phase", _codesign_no_temperature, lambda: c.codesign_limits() > 1e-3),
+    ("codesign_grad_not_centred", "codesign_backward", _codesign_backward_no_centering,
+     lambda: c.codesign_grad_fd() > 1e-3),
     ("adam_no_bias_correction", "adam_update", _adam_no_bias_correction, lambda: c.adam_first_step() > 1e-3),
     ("adam_eps_inside_sqrt", "adam_update", _adam_eps_inside_sqrt, lambda: c.adam_constant_gradient() > 1e-3),
     ("adam_betas_swapped", "adam_update", _adam_betas_swapped, lambda: c.adam_vs_torch() > 1e-3),

@@ -167,3 +167,11 @@ def test_multichannel_sums_add():
 def test_multichannel_gradients_by_finite_differences():
     # central differences with step 1e-6 in float64: ~1e-8 truncation and rounding
     assert c.multichannel_grad_fd() < 1e-6
+
+
+def test_codesign_limits_and_shift_invariance():
+    assert c.codesign_limits() < 1e-9
+
+
+def test_codesign_gradient_by_finite_differences():
+    assert c.codesign_grad_fd() < 1e-8
