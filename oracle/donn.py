@@ -404,7 +404,9 @@ def codesign_phase(logits: np.ndarray, noise: np.ndarray, levels: np.ndarray, ta
     Gumbel(0, 1) draws; levels [K]: the device's phase values (radians).
     w = softmax((logits + noise) / tau) over K; the phase is sum_k w_k
     levels_k, or with ``hard`` the level of the largest logits + noise (the
-    straight-through estimator keeps the soft w for the gradient).
+    straight-through estimator keeps the soft w for the gradient).  The hard
+    choice is an integer decision and is taken on float32 logits + noise, the
+    precision of the device path.
     Returns (phi [...], w [..., K])."""
     y = (np.asarray(logits, np.float64) + np.asarray(noise, np.float64)) / tau
     y = y - y.max(axis=-1, keepdims=True)
@@ -412,7 +414,9 @@ def codesign_phase(logits: np.ndarray, noise: np.ndarray, levels: np.ndarray, ta
     w = e / e.sum(axis=-1, keepdims=True)
     lv = np.asarray(levels, np.float64)
     if hard:
-        phi = lv[np.argmax(np.asarray(logits, np.float64) + np.asarray(noise, np.float64), axis=-1)]
+        # an integer decision: taken on the float32 sums the device forms (first index on ties)
+        score = np.asarray(logits, np.float32) + np.asarray(noise, np.float32)
+        phi = lv[np.argmax(score, axis=-1)]
     else:
         phi = w @ lv
     return phi, w
