@@ -237,6 +237,28 @@ enum lr_loss_kind {
 int lr_loss(int32_t kind, const float* d_sums, const int32_t* d_labels, int32_t batch, int32_t classes,
             float* d_loss, float* d_grad_sums, void* stream);
 
+/* Codesign layer (§3.2): trainable scores over the discrete, measured
+ * optical responses of the hardware, relaxed with Gumbel-Softmax so that the
+ * masks train directly on the available device levels.
+ *   d_logits, d_noise: float32 [count][levels], the scores of each pixel's
+ *     levels and Gumbel(0, 1) draws (-log(-log U)), supplied by the caller;
+ *   d_levels: float32 [levels], the device's phase responses in radians;
+ *   w = softmax((logits + noise) / tau) over the levels of a pixel.
+ * lr_codesign_phase writes d_phi[p] = sum_k w_k levels_k, or with hard != 0
+ * the level with the largest float32 logits + noise (the first on ties):
+ * the phase masks (count = L n n) that lr_donn_forward then takes.
+ * lr_codesign_backward writes dL/dlogits [count][levels] =
+ * w_j (levels_j - sum_k w_k levels_k) dL/dphi / tau from dL/dphi [count]
+ * (lr_donn_backward's output); for the hard layer this is the
+ * straight-through gradient.  1 <= levels <= LR_MAX_LEVELS; tau finite > 0.
+ * Errors: LR_E_SIZE, LR_E_ARG, LR_E_NULL, LR_E_ALIAS (output aliases an
+ * input). */
+#define LR_MAX_LEVELS 1024
+int lr_codesign_phase(const float* d_logits, const float* d_noise, const float* d_levels, int32_t levels,
+                      int64_t count, float tau, int32_t hard, float* d_phi, void* stream);
+int lr_codesign_backward(const float* d_logits, const float* d_noise, const float* d_levels, int32_t levels,
+                         int64_t count, float tau, const float* d_grad_phi, float* d_grad_logits, void* stream);
+
 /* One Adam step on the phase masks (§5.1 trains them with Adam, learning
  * rate 0.5), element-wise over count floats, in place:
  *   m = beta1 m + (1 - beta1) g,  v = beta2 v + (1 - beta2) g^2,

@@ -30,7 +30,7 @@ LR_LOSS_SOFTMAX_MSE = 1
 EXPORTS = (
     "lr_tf_build", "lr_workspace_size", "lr_saved_size",
     "lr_propagate", "lr_detector_readout", "lr_donn_forward", "lr_donn_backward",
-    "lr_loss", "lr_adam_update",
+    "lr_loss", "lr_adam_update", "lr_codesign_phase", "lr_codesign_backward",
     "lr_status_string", "lr_kernel_timing", "lr_kernel_timing_report", "lr_version",
 )
 
@@ -76,6 +76,8 @@ def load() -> ctypes.CDLL:
     lib.lr_donn_backward.argtypes = [POINTER(LrDonn), c_int32, P, P, P, P, P, P, P, P, P, c_size_t, P]
     lib.lr_loss.argtypes = [c_int32, P, P, c_int32, c_int32, P, P, P]
     lib.lr_adam_update.argtypes = [P, P, P, P, c_int64, c_int32, c_float, c_float, c_float, c_float, P]
+    lib.lr_codesign_phase.argtypes = [P, P, P, c_int32, c_int64, c_float, c_int32, P, P]
+    lib.lr_codesign_backward.argtypes = [P, P, P, c_int32, c_int64, c_float, P, P, P]
     lib.lr_status_string.argtypes = [ctypes.c_int]
     lib.lr_status_string.restype = c_char_p
     lib.lr_kernel_timing.argtypes = [c_int32]
@@ -335,6 +337,39 @@ def kernel_timing_report() -> dict:
     buf = ctypes.create_string_buffer(need + 1)
     lib.lr_kernel_timing_report(buf, need + 1)
     return json.loads(buf.value.decode())
+
+
+def lr_codesign_phase(logits, noise, levels, tau: float, hard: bool = False, out=None):
+    """Phase masks [...] from scores and Gumbel draws [..., K] over the device's
+    phase levels [K] (soft sum or, with hard, the chosen level)."""
+    torch = _torch()
+    shape = tuple(logits.shape)
+    k = int(shape[-1])
+    count = int(logits.numel()) // max(k, 1)
+    if out is None:
+        out = torch.empty(shape[:-1], dtype=torch.float32, device=logits.device)
+    _check(load().lr_codesign_phase(_ptr(logits, torch.float32, shape, "logits"), _ptr(noise, torch.float32, shape, "noise"),
+                                    _ptr(levels, torch.float32, (k,), "levels"), k, count, float(tau),
+                                    1 if hard else 0, _ptr(out, torch.float32, shape[:-1], "phi"),
+                                    _stream(logits.device)), "lr_codesign_phase")
+    return out
+
+
+def lr_codesign_backward(logits, noise, levels, tau: float, grad_phi, out=None):
+    """dL/dlogits [..., K] from dL/dphi [...]."""
+    torch = _torch()
+    shape = tuple(logits.shape)
+    k = int(shape[-1])
+    count = int(logits.numel()) // max(k, 1)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.float32, device=logits.device)
+    _check(load().lr_codesign_backward(_ptr(logits, torch.float32, shape, "logits"),
+                                       _ptr(noise, torch.float32, shape, "noise"),
+                                       _ptr(levels, torch.float32, (k,), "levels"), k, count, float(tau),
+                                       _ptr(grad_phi, torch.float32, shape[:-1], "grad_phi"),
+                                       _ptr(out, torch.float32, shape, "grad_logits"), _stream(logits.device)),
+           "lr_codesign_backward")
+    return out
 
 
 def multichannel_train_step(nets, amps, phis, saveds, labels, kind: int = LR_LOSS_SOFTMAX_CE):

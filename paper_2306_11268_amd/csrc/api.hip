@@ -926,6 +926,36 @@ int lr_loss(int32_t kind, const float* d_sums, const int32_t* d_labels, int32_t 
   });
 }
 
+int lr_codesign_phase(const float* d_logits, const float* d_noise, const float* d_levels, int32_t levels,
+                      int64_t count, float tau, int32_t hard, float* d_phi, void* stream) {
+  if (levels < 1 || levels > LR_MAX_LEVELS || count < 0) return LR_E_SIZE;
+  if (!(tau > 0.f) || !std::isfinite(tau)) return LR_E_ARG;
+  if (count == 0) return LR_OK;
+  if (!d_logits || !d_noise || !d_levels || !d_phi) return LR_E_NULL;
+  const void* out = d_phi;
+  if (out == d_logits || out == d_noise || out == d_levels) return LR_E_ALIAS;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return run_timed("codesign", st, [&] {
+    return lr::launch_codesign(d_logits, d_noise, d_levels, levels, static_cast<long long>(count), tau, hard ? 1 : 0,
+                               nullptr, d_phi, st);
+  });
+}
+
+int lr_codesign_backward(const float* d_logits, const float* d_noise, const float* d_levels, int32_t levels,
+                         int64_t count, float tau, const float* d_grad_phi, float* d_grad_logits, void* stream) {
+  if (levels < 1 || levels > LR_MAX_LEVELS || count < 0) return LR_E_SIZE;
+  if (!(tau > 0.f) || !std::isfinite(tau)) return LR_E_ARG;
+  if (count == 0) return LR_OK;
+  if (!d_logits || !d_noise || !d_levels || !d_grad_phi || !d_grad_logits) return LR_E_NULL;
+  const void* out = d_grad_logits;
+  if (out == d_logits || out == d_noise || out == d_levels || out == d_grad_phi) return LR_E_ALIAS;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  return run_timed("codesign_bwd", st, [&] {
+    return lr::launch_codesign(d_logits, d_noise, d_levels, levels, static_cast<long long>(count), tau, 0,
+                               d_grad_phi, d_grad_logits, st);
+  });
+}
+
 int lr_adam_update(float* d_phi, const float* d_grad, float* d_m, float* d_v, int64_t count, int32_t step, float lr,
                    float beta1, float beta2, float eps, void* stream) {
   if (count < 0 || step < 1) return LR_E_SIZE;

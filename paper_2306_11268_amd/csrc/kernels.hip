@@ -100,6 +100,95 @@ __global__ void __launch_bounds__(1024) loss_kernel(int kind, const float* __res
 
 // One Adam step on every element: m = b1 m + (1-b1) g, v = b2 v + (1-b2) g^2,
 // phi -= lr * (m / bc1) / (sqrt(v / bc2) + eps), bc = 1 - beta^t.
+// Codesign layer (§3.2): per pixel, w = softmax((logits + noise) / tau) over
+// the K device levels; the phase is sum_k w_k levels_k, or (hard) the level
+// of the largest logits + noise, the first on ties.  One wave per pixel; lane
+// l handles levels l, l + 64, ...; the scores are read coalesced.
+constexpr int kCodesignMaxLevels = 1024;
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmaxf(x, __shfl_xor(x, o, 64));
+  return x;
+}
+__device__ __forceinline__ int wave_min_int(int x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = min(x, __shfl_xor(x, o, 64));
+  return x;
+}
+
+// Per-pixel softmax statistics: max of y = (logits + noise) / tau, the first
+// level index reaching the largest logits + noise, and sum_k exp(y_k - max).
+struct CodesignStats {
+  float ymax;
+  int kbest;
+  float esum;
+};
+__device__ __forceinline__ CodesignStats codesign_stats(const float* __restrict__ lg, const float* __restrict__ nz, int K,
+                                                        float inv_tau, int lane) {
+  float smax = -INFINITY;
+  for (int k = lane; k < K; k += 64) smax = fmaxf(smax, lg[k] + nz[k]);
+  smax = wave_max(smax);
+  int kb = K;
+  for (int k = lane; k < K; k += 64)
+    if (lg[k] + nz[k] == smax) {
+      kb = k;
+      break;
+    }
+  kb = wave_min_int(kb);
+  const float ymax = smax * inv_tau;
+  float es = 0.f;
+  for (int k = lane; k < K; k += 64) es += expf((lg[k] + nz[k]) * inv_tau - ymax);
+  return CodesignStats{ymax, kb, wave_sum(es)};
+}
+
+__global__ void __launch_bounds__(256) codesign_kernel(const float* __restrict__ logits, const float* __restrict__ noise,
+                                                       const float* __restrict__ levels, int K, long long count,
+                                                       float inv_tau, int hard, float* __restrict__ phi) {
+  const int lane = threadIdx.x & 63;
+  const long long waves = (long long)gridDim.x * (blockDim.x >> 6);
+  for (long long p = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); p < count; p += waves) {
+    const float* lg = logits + p * K;
+    const float* nz = noise + p * K;
+    const CodesignStats cs = codesign_stats(lg, nz, K, inv_tau, lane);
+    float out;
+    if (hard) {
+      out = levels[cs.kbest < K ? cs.kbest : 0];  // (no index reaches the maximum only for NaN scores)
+    } else {
+      float acc = 0.f;
+      for (int k = lane; k < K; k += 64) acc += expf((lg[k] + nz[k]) * inv_tau - cs.ymax) * levels[k];
+      out = wave_sum(acc) / cs.esum;
+    }
+    if (lane == 0) phi[p] = out;
+  }
+}
+
+// dL/dlogit_j = w_j (levels_j - sum_k w_k levels_k) dL/dphi / tau (the soft
+// Jacobian, also the straight-through gradient of the hard layer).
+__global__ void __launch_bounds__(256) codesign_bwd_kernel(const float* __restrict__ logits,
+                                                           const float* __restrict__ noise,
+                                                           const float* __restrict__ levels, int K, long long count,
+                                                           float inv_tau, const float* __restrict__ grad_phi,
+                                                           float* __restrict__ grad_logits) {
+  const int lane = threadIdx.x & 63;
+  const long long waves = (long long)gridDim.x * (blockDim.x >> 6);
+  for (long long p = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); p < count; p += waves) {
+    const float* lg = logits + p * K;
+    const float* nz = noise + p * K;
+    const CodesignStats cs = codesign_stats(lg, nz, K, inv_tau, lane);
+    const float inv_s = 1.f / cs.esum;
+    float acc = 0.f;
+    for (int k = lane; k < K; k += 64) acc += expf((lg[k] + nz[k]) * inv_tau - cs.ymax) * levels[k];
+    const float mean = wave_sum(acc) * inv_s;
+    const float gs = grad_phi[p] * inv_tau;
+    float* gl = grad_logits + p * K;
+    for (int k = lane; k < K; k += 64) {
+      const float w = expf((lg[k] + nz[k]) * inv_tau - cs.ymax) * inv_s;
+      gl[k] = w * (levels[k] - mean) * gs;
+    }
+  }
+}
+
 __global__ void adam_kernel(float* __restrict__ phi, const float* __restrict__ g, float* __restrict__ m,
                             float* __restrict__ v, long long count, float lr, float b1, float b2, float eps,
                             float bc1, float bc2) {
@@ -405,6 +494,21 @@ hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, f
 hipError_t launch_loss(int kind, const float* sums, const int32_t* labels, int batch, int K, float* grad, float* loss,
                        hipStream_t st) {
   hipLaunchKernelGGL(loss_kernel, dim3(1), dim3(1024), 0, st, kind, sums, labels, batch, K, grad, loss);
+  return hipGetLastError();
+}
+
+hipError_t launch_codesign(const float* logits, const float* noise, const float* levels, int K, long long count,
+                           float tau, int hard, const float* grad_phi, float* phi_or_grad, hipStream_t st) {
+  if (count <= 0) return hipSuccess;
+  long long blocks = (count + 3) / 4;  // four pixels (waves) per workgroup
+  if (blocks > 65536) blocks = 65536;
+  if (grad_phi) {
+    hipLaunchKernelGGL(codesign_bwd_kernel, dim3((unsigned)blocks), dim3(256), 0, st, logits, noise, levels, K, count,
+                       1.f / tau, grad_phi, phi_or_grad);
+  } else {
+    hipLaunchKernelGGL(codesign_kernel, dim3((unsigned)blocks), dim3(256), 0, st, logits, noise, levels, K, count,
+                       1.f / tau, hard, phi_or_grad);
+  }
   return hipGetLastError();
 }
 

@@ -126,6 +126,11 @@ hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, f
 // are nullable.
 hipError_t launch_loss(int kind, const float* sums, const int32_t* labels, int batch, int K, float* grad_sums,
                        float* loss, hipStream_t st);
+// Codesign layer: with grad_phi NULL, phi_or_grad[p] = the phase of pixel p
+// (soft sum or, with hard, the chosen level); otherwise phi_or_grad
+// [count][K] = dL/dlogits.  logits, noise [count][K]; levels [K]; K <= 1024.
+hipError_t launch_codesign(const float* logits, const float* noise, const float* levels, int K, long long count,
+                           float tau, int hard, const float* grad_phi, float* phi_or_grad, hipStream_t st);
 // One Adam step over count elements (bc1, bc2: bias corrections 1 - beta^t).
 hipError_t launch_adam(float* phi, const float* g, float* m, float* v, long long count, float lr, float b1, float b2,
                        float eps, float bc1, float bc2, hipStream_t st);

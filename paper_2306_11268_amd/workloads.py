@@ -7,7 +7,7 @@ oracle and the HIP library receive the very same arrays.
 
 Every stream is ``np.random.default_rng([230611268, workload_id, stream])``
 with stream 0 = input amplitudes, 1 = phase masks, 2 = labels, 3 = upstream
-intensity gradient.  Samples are drawn one after another, so the first B'
+intensity gradient, 4 = device levels, 5 = codesign scores, 6 = Gumbel draws.  Samples are drawn one after another, so the first B'
 samples of a batch of B are the batch of B'.
 
 The paper's datasets (MNIST-style digits, CityScapes scenes) are not
@@ -243,3 +243,28 @@ def layout_grid(n: int, num: int, size: int) -> DetectorLayout:
         y0.append(gy + r * (size + gy))
         x0.append(gx + c * (size + gx))
     return DetectorLayout(size, tuple(y0), tuple(x0))
+
+
+# ---------------------------------------------------------------------------
+# Codesign layer inputs (§3.2): a device's discrete phase responses, per-pixel
+# scores over them and the Gumbel draws of one training step.  No measured
+# device vector is available; the synthetic one has the paper's 256 states
+# covering [0, 2*pi) with a smooth non-linear (SLM-like) response curve.
+# ---------------------------------------------------------------------------
+
+def device_levels(wid: int, levels: int = 256) -> np.ndarray:
+    """Monotone phase responses in [0, 2*pi), float32 [levels] (stream 4)."""
+    g = rng(wid, 4)
+    x = (np.arange(levels, dtype=np.float64) + g.uniform(0.0, 0.3, levels)) / levels
+    return np.sort(2.0 * np.pi * x ** 1.3).astype(np.float32)
+
+
+def codesign_scores(wid: int, shape, levels: int) -> np.ndarray:
+    """Per-pixel scores ~ N(0, 1), float32 [*shape, levels] (stream 5)."""
+    return rng(wid, 5).standard_normal(tuple(shape) + (levels,)).astype(np.float32)
+
+
+def gumbel_draws(wid: int, shape, levels: int) -> np.ndarray:
+    """Gumbel(0, 1) draws -log(-log U), float32 [*shape, levels] (stream 6)."""
+    u = rng(wid, 6).uniform(1e-12, 1.0, tuple(shape) + (levels,))
+    return (-np.log(-np.log(u))).astype(np.float32)

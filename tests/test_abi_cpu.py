@@ -174,3 +174,21 @@ def test_kernel_timing_toggle_without_launches():
     lb.kernel_timing(True)
     assert lb.kernel_timing_report() == {}
     lb.kernel_timing(False)
+
+
+@needs_lib
+def test_codesign_rejects_bad_arguments_without_touching_the_gpu():
+    lib = lb.load()
+    P = ctypes.c_void_p
+    a, b, c, d = P(0x1000), P(0x2000), P(0x3000), P(0x4000)
+    assert lib.lr_codesign_phase(a, b, c, 0, 10, 1.0, 0, d, None) == 2
+    assert lib.lr_codesign_phase(a, b, c, 1025, 10, 1.0, 0, d, None) == 2
+    assert lib.lr_codesign_phase(a, b, c, 16, -1, 1.0, 0, d, None) == 2
+    assert lib.lr_codesign_phase(a, b, c, 16, 10, 0.0, 0, d, None) == 3
+    assert lib.lr_codesign_phase(a, b, c, 16, 10, float("nan"), 0, d, None) == 3
+    assert lib.lr_codesign_phase(None, b, c, 16, 10, 1.0, 0, d, None) == 1
+    assert lib.lr_codesign_phase(a, b, c, 16, 10, 1.0, 0, a, None) == 7
+    assert lib.lr_codesign_phase(None, None, None, 16, 0, 1.0, 0, None, None) == 0
+    assert lib.lr_codesign_backward(a, b, c, 16, 10, 1.0, d, None, None) == 1
+    assert lib.lr_codesign_backward(a, b, c, 16, 10, 1.0, d, d, None) == 7
+    assert lib.lr_codesign_backward(a, b, c, 16, 10, -2.0, d, P(0x5000), None) == 3
