@@ -61,7 +61,15 @@ typedef int lr_v2i __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ Rsrc make_rsrc(const void* base, unsigned bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
+// Field loads carry the non-temporal hint (cache policy bit 1): every field
+// is read once per pass, and the hint keeps those lines from displacing the
+// field the previous pass just wrote, which the large last-level cache can
+// still hold when this pass reads it.  Tables shared by the batch load
+// without it (bload_keep).
 __device__ __forceinline__ float2 bload(Rsrc r, unsigned off) {
+  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 2));
+}
+__device__ __forceinline__ float2 bload_keep(Rsrc r, unsigned off) {
   return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
 }
 __device__ __forceinline__ void bstore(Rsrc r, unsigned off, float2 v) {
@@ -506,7 +514,10 @@ __device__ __forceinline__ void load_a_direct_masked(const float2* __restrict__ 
 template <class C>
 __device__ __forceinline__ void load_a_table(const float2* __restrict__ tab, int n, int off, int vec, bool vok,
                                              float2 (&m)[C::N1]) {
-  load_a_direct<C>(tab, n, n, off, vec, vok, m);
+  const Rsrc r = make_rsrc(tab, (unsigned)(n * n) * 8u);
+  for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool valid) {
+    m[k.value] = bload_keep(r, valid ? (unsigned)idx * 8u : kOutOfRange);
+  });
 }
 
 // ---------------------------------------------------------------------------
