@@ -7,9 +7,10 @@ softmax cross-entropy over the ten detector sums, adjoint backward pass to
 dL/dphi for all five masks.  Inputs are resident in HBM before timing.
 
 Prints one JSON line.  `value` is samples per second over exactly --steps
-steps bracketed by device synchronisation; the per-kernel durations used for
-the roofline come from HIP events recorded around every kernel launch on the
-launch stream during a second, instrumented run of the same steps.
+steps bracketed by device synchronisation (with --graph the step is recorded
+once as a HIP graph and the timed steps replay it).  The per-kernel durations used for the roofline come
+from HIP events recorded around every kernel launch on the launch stream
+during a second, instrumented run of the same steps.
 """
 
 from __future__ import annotations
@@ -38,6 +39,9 @@ def parse():
                     help="grid size of a runtime-study variant of the workload (unpadded n x n)")
     ap.add_argument("--layers", type=int, default=None, help="depth of a runtime-study variant")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--graph", action="store_true",
+                    help="record the step once as a HIP graph and time its replays (measured slower than "
+                         "launching the kernels one by one on this stack, so not the default)")
     ap.add_argument("--cpu-samples", type=int, default=None, help="samples in the oracle timing run")
     ap.add_argument("--copy-calibration", type=int, default=None, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB three times (the reference "
@@ -171,13 +175,29 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    run = step
+    if args.graph:
+        # The step's launches (kernels only: no copies, fills or host waits)
+        # recorded once as a HIP graph and replayed: the same kernels on the
+        # same buffers, without the per-launch dispatch gaps.
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            _, loss_graph = step()
+        torch.cuda.synchronize()
+
+        def run():
+            graph.replay()
+            return grad, loss_graph
+
+        run()
+        torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     ev0.record(stream)
     for _ in range(args.steps):
-        _, loss = step()
+        _, loss = run()
     ev1.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -230,6 +250,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
+        "execution": "graph_replay" if args.graph else "eager",
         "config": {"workload": w.name, "n": w.n, "n_fft": w.n_fft, "layers": w.layers, "batch": batch,
                    "approx": "fresnel" if w.approx == 0 else "angular_spectrum",
                    "wavelength_m": w.wavelength, "pixel_pitch_m": w.pixel_pitch, "distance_m": w.distance,
