@@ -1137,6 +1137,7 @@ template <> struct LayerTile<200, kFwdMid, kCol> { static constexpr int T = 32; 
 template <> struct LayerTile<200, kPropOnce, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kFwdMid, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kBwdMid, kRow> { static constexpr int T = 8; };
+template <> struct LayerTile<200, kBwdLast, kCol> { static constexpr int T = 32; };
 
 template <int N, int KIND, int AXIS>
 using LayerCfg = Cfg<std::conditional_t<AXIS == kRow, typename RowPlanFor<N>::type, typename PlanFor<N>::type>,
