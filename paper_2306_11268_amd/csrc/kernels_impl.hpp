@@ -865,11 +865,16 @@ __global__ void __launch_bounds__(C::P, C::WAVES) detector_pass(PassArgs a) {
 // Angular-spectrum passes.  Between passes a sample is stored as n rows of
 // N x-spectrum values in the plan's slot order ([B][n][N]).
 // ---------------------------------------------------------------------------
+// (The B-item index goes behind an empty asm statement, as in b_spectral:
+// twiddle offsets derived from it are formed at their use, not hoisted out
+// of the per-sample loop.)
 template <class C>
 __device__ __forceinline__ void b_forward_all(const Tile<C>& t) {
+  int s = t.s;
+  asm volatile("" : "+v"(s));
 #pragma unroll 1
   for (int ii = 0; ii < C::IB; ++ii) {
-    const int k1 = t.s + C::S * ii;
+    const int k1 = s + C::S * ii;
     if (!C::B_FULL && k1 >= C::N1) break;
     float2 y[C::N2];
     read_b(t, k1, y);
@@ -879,9 +884,11 @@ __device__ __forceinline__ void b_forward_all(const Tile<C>& t) {
 }
 template <class C>
 __device__ __forceinline__ void b_inverse_all(const Tile<C>& t) {
+  int s = t.s;
+  asm volatile("" : "+v"(s));
 #pragma unroll 1
   for (int ii = 0; ii < C::IB; ++ii) {
-    const int k1 = t.s + C::S * ii;
+    const int k1 = s + C::S * ii;
     if (!C::B_FULL && k1 >= C::N1) break;
     float2 y[C::N2];
     read_b(t, k1, y);
@@ -895,12 +902,13 @@ template <class C>
 __device__ __forceinline__ void load_spec_rows(float2* lds, const float2* __restrict__ in, int vec0, int nvalid) {
   float2 buf[C::N1];
   const int total = nvalid * C::N;
+  const int tid = opaque_tid();
   static_for<0, C::N1>([&](auto i) {
-    const int e = threadIdx.x + i.value * C::P;
+    const int e = tid + i.value * C::P;
     if (e < total) buf[i.value] = ld(in, vec0 * C::N + e);
   });
   static_for<0, C::N1>([&](auto i) {
-    const int e = threadIdx.x + i.value * C::P;
+    const int e = tid + i.value * C::P;
     const int v = e / C::N;
     if (e < total) lds[(e - v * C::N) * C::TP + v] = buf[i.value];
   });
@@ -909,13 +917,14 @@ template <class C>
 __device__ __forceinline__ void store_spec_rows(const float2* lds, float2* __restrict__ out, int vec0, int nvalid) {
   float2 buf[C::N1];
   const int total = nvalid * C::N;
+  const int tid = opaque_tid();
   static_for<0, C::N1>([&](auto i) {
-    const int e = threadIdx.x + i.value * C::P;
+    const int e = tid + i.value * C::P;
     const int v = e / C::N;
     if (e < total) buf[i.value] = lds[(e - v * C::N) * C::TP + v];
   });
   static_for<0, C::N1>([&](auto i) {
-    const int e = threadIdx.x + i.value * C::P;
+    const int e = tid + i.value * C::P;
     if (e < total) st(out, vec0 * C::N + e, buf[i.value]);
   });
 }
@@ -967,15 +976,19 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
       Dft<N1, -1>::run(x);
       write_a(t, j, x);
       __syncthreads();
-      // B-step with the 2-D table: element k2 of item k1 is ky = freq(k1, k2)
+      // B-step with the 2-D table: element k2 of item k1 is ky = freq(k1, k2);
+      // scheduling barriers keep the twiddle and table loads next to their use
       const bool cj = a.conj_tab != 0;
+      int s_op = t.s;
+      asm volatile("" : "+v"(s_op));
 #pragma unroll 1
       for (int ii = 0; ii < C::IB; ++ii) {
-        const int k1 = t.s + C::S * ii;
+        const int k1 = s_op + C::S * ii;
         if (!C::B_FULL && k1 >= C::N1) break;
         float2 y[C::N2];
         read_b(t, k1, y);
         b_forward<C>(k1, y);
+        __builtin_amdgcn_sched_barrier(0);
         if (vok) {
           static_for<0, C::N2>([&](auto kc) {
             constexpr int k2 = decltype(kc)::value;
@@ -983,7 +996,9 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
             y[k2] = cj ? cmulc(y[k2], h) : cmul(y[k2], h);
           });
         }
+        __builtin_amdgcn_sched_barrier(0);
         b_inverse<C>(k1, y);
+        __builtin_amdgcn_sched_barrier(0);
         write_b(t, k1, y);
       }
       __syncthreads();
@@ -1119,7 +1134,7 @@ template <> struct TileT<400>  { static constexpr int T = 8; };
 template <> struct TileT<500>  { static constexpr int T = 16; };  // 20 slots: T * 20 threads must be whole waves
 template <> struct TileT<512>  { static constexpr int T = 8; };
 template <> struct TileT<1000> { static constexpr int T = 8; };
-template <> struct TileT<1024> { static constexpr int T = 4; };
+template <> struct TileT<1024> { static constexpr int T = 8; };
 
 template <int N>
 using CfgFor = Cfg<typename PlanFor<N>::type, TileT<N>::T>;

@@ -31,10 +31,12 @@ struct Cfg {
   static constexpr int LDS_ELEMS = (N + 1) * TP;
   static constexpr int LDS_BYTES = LDS_ELEMS * 8 + (P / 64) * 4;
   // Waves per SIMD that shared memory (160 KiB per CU) allows; the kernels
-  // ask the compiler to fit their registers to this occupancy.
+  // ask the compiler to fit their registers to this occupancy, and to at
+  // least 2 waves (256 registers): allowed 512 at one wave per SIMD, the
+  // large-N kernels took them all and hid no latency.
   static constexpr int WG_PER_CU = (160 * 1024) / LDS_BYTES;
   static constexpr int WAVES_RAW = (WG_PER_CU * (P / 64)) / 4;
-  static constexpr int WAVES = WAVES_RAW < 1 ? 1 : (WAVES_RAW > 4 ? 4 : WAVES_RAW);
+  static constexpr int WAVES = WAVES_RAW < 2 ? 2 : (WAVES_RAW > 4 ? 4 : WAVES_RAW);
   // kernels that also carry per-element gradient accumulators
   static constexpr int WAVES_ACC = WAVES > 2 ? 2 : WAVES;
   static_assert(P % 64 == 0, "workgroup must be whole wavefronts");
@@ -83,11 +85,42 @@ __device__ __forceinline__ float2 root_at(unsigned m) {
 
 // Forward half of the B-step: twiddles exp(-2*pi*i*k1*j/N) (Cooley-Tukey
 // only), then DFT over j.
+// Twiddles of long B-items as products of two roots, w^(k1*j) =
+// w^(k1*(j mod 8)) * w^(8*k1*(j/8)): 7 + (N2/8 - 1) loads instead of N2 - 1.
+template <class C, bool INV>
+__device__ __forceinline__ void b_twiddle_split(int k1, float2 (&y)[C::N2]) {
+  constexpr int NB = (C::N2 + 7) / 8;
+  float2 lo[8];
+  float2 hi[NB];
+  static_for<1, 8>([&](auto j) {
+    lo[j.value] = root_at<C::N>(INV ? (unsigned)(C::N - k1 * j.value) : (unsigned)(k1 * j.value));
+  });
+  static_for<1, NB>([&](auto b) {
+    hi[b.value] = root_at<C::N>(INV ? (unsigned)(C::N - 8 * k1 * b.value) : (unsigned)(8 * k1 * b.value));
+  });
+  static_for<1, C::N2>([&](auto jc) {
+    constexpr int j = decltype(jc)::value;
+    constexpr int jl = j % 8;
+    constexpr int jh = j / 8;
+    if constexpr (jh == 0) {
+      y[j] = cmul(y[j], lo[jl]);
+    } else if constexpr (jl == 0) {
+      y[j] = cmul(y[j], hi[jh]);
+    } else {
+      y[j] = cmul(y[j], cmul(lo[jl], hi[jh]));
+    }
+  });
+}
+
 template <class C>
 __device__ __forceinline__ void b_forward(int k1, float2 (&y)[C::N2]) {
   using PL = typename C::Plan;
   if constexpr (!PL::PFA) {
-    static_for<1, C::N2>([&](auto j) { y[j.value] = cmul(y[j.value], root_at<C::N>((unsigned)(k1 * j.value))); });
+    if constexpr (C::N2 >= 32) {
+      b_twiddle_split<C, false>(k1, y);
+    } else {
+      static_for<1, C::N2>([&](auto j) { y[j.value] = cmul(y[j.value], root_at<C::N>((unsigned)(k1 * j.value))); });
+    }
   }
   Dft<C::N2, -1>::run(y);
 }
@@ -100,8 +133,12 @@ __device__ __forceinline__ void b_inverse(int k1, float2 (&y)[C::N2]) {
   using PL = typename C::Plan;
   Dft<C::N2, 1>::run(y);
   if constexpr (!PL::PFA) {
-    static_for<1, C::N2>(
-        [&](auto j) { y[j.value] = cmul(y[j.value], root_at<C::N>((unsigned)(C::N - k1 * j.value))); });
+    if constexpr (C::N2 >= 32) {
+      b_twiddle_split<C, true>(k1, y);
+    } else {
+      static_for<1, C::N2>(
+          [&](auto j) { y[j.value] = cmul(y[j.value], root_at<C::N>((unsigned)(C::N - k1 * j.value))); });
+    }
   }
 }
 
