@@ -606,7 +606,12 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
       });
     }
   }
-  constexpr bool PREFETCH = ACC && (DIRECT || KIND == kBwdMid);
+  // At N >= 1000 an A-item is 25-32 values: the prefetch buffer and a
+  // modulation loaded during the B-step no longer fit next to the
+  // propagating item in 256 registers (they spilled), so these sizes load
+  // each input when it is needed and rely on the other resident waves.
+  constexpr bool BIG = C::N >= 1000;
+  constexpr bool PREFETCH = ACC && (DIRECT || KIND == kBwdMid) && !BIG;
   constexpr bool G_FIRST = DIRECT && KIND == kBwdLast;
   float2 pf[PREFETCH && DIRECT ? N1 : 1];
   TileBuf<C, AXIS> pft;  // row tiles
@@ -645,10 +650,19 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
     if constexpr (G_FIRST) {
       // G_1 = adjoint of the first-axis half of hop 2, while W_0 is in flight
       float2 ar[N1];
-      static_for<0, N1>([&](auto k) { x[k.value] = pf[k.value]; });
+      if constexpr (PREFETCH) {
+        static_for<0, N1>([&](auto k) { x[k.value] = pf[k.value]; });
+      } else {
+        load_a_direct_masked<C>(fin, n, n, off, vec, vok, gmask, x);
+      }
       load_a_direct<C>(a.act_in + (size_t)b * nn, n, n, off, vec, vok, ar);
       float2 m[N1];
-      prop(x, true, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+      if constexpr (BIG) {
+        prop(x, true, nothing);
+        load_a_table<C>(a.mod, n, off, vec, vok, m);
+      } else {
+        prop(x, true, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+      }
       static_for<0, N1>([&](auto k) { x[k.value] = cmulc(x[k.value], m[k.value]); });
       // A_1, then dphi_1 += Im(conj(A_1) conj(M_1) G_1)
       prop(ar, false, prefetch);
@@ -658,7 +672,11 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
       // with respect to W_l) is in flight
       float2 ar[N1];
       if constexpr (DIRECT) {
-        static_for<0, N1>([&](auto k) { ar[k.value] = pf[k.value]; });
+        if constexpr (PREFETCH) {
+          static_for<0, N1>([&](auto k) { ar[k.value] = pf[k.value]; });
+        } else {
+          load_a_direct<C>(a.act_in + (size_t)b * nn, n, n, off, vec, vok, ar);
+        }
         load_a_direct_masked<C>(fin, n, n, off, vec, vok, gmask, x);
         prop(ar, false, nothing);
       } else {
@@ -677,9 +695,14 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
         read_a(t, j, x);
       }
       // G_l = adjoint of the first-axis half of hop l+1; the modulation is
-      // loaded during its B-step
+      // loaded during its B-step (after it at N >= 1000)
       float2 m[N1];
-      prop(x, true, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+      if constexpr (BIG) {
+        prop(x, true, nothing);
+        load_a_table<C>(a.mod, n, off, vec, vok, m);
+      } else {
+        prop(x, true, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+      }
       // conj(M_l) G_l (zero outside the aperture) and dphi_l += Im(conj(U_l) G_l) = Im(conj(A_l) conj(M_l) G_l)
       static_for<0, N1>([&](auto k) {
         const float2 h = cmulc(x[k.value], m[k.value]);
