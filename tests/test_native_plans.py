@@ -34,3 +34,20 @@ def test_plans_against_direct_dft(tmp_path):
     out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=300)
     assert out.returncode == 0, out.stdout[-4000:]
     assert "ALL OK" in out.stdout
+
+
+def test_tile_shared_memory_layout(tmp_path):
+    """Shared-memory layout of the tile kernels (host-side, no kernel launch):
+    every (slot, vector) entry distinct and in bounds, and the spare slot and
+    the workgroup's buffer fit."""
+    cc = _hipcc()
+    if cc is None:
+        pytest.skip("hipcc not available")
+    exe = tmp_path / "tile_layout_host"
+    r = subprocess.run([cc, "-O2", "-std=c++17", "--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang",
+                        "-packed-fp32-ops", os.path.join(HERE, "native", "tile_layout_host.hip"), "-o", str(exe)],
+                       capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-4000:]
+    out = subprocess.run([str(exe)], capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, out.stdout[-4000:]
+    assert "ALL OK" in out.stdout
