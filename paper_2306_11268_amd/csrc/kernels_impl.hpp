@@ -609,7 +609,8 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
   // At N >= 1000 an A-item is 25-32 values: the prefetch buffer and a
   // modulation loaded during the B-step no longer fit next to the
   // propagating item in 256 registers (they spilled), so these sizes load
-  // each input when it is needed and rely on the other resident waves.
+  // each input when it is needed and rely on the other resident waves (the
+  // forward layer pass likewise loads its modulation after the B-step).
   constexpr bool BIG = C::N >= 1000;
   constexpr bool PREFETCH = ACC && (DIRECT || KIND == kBwdMid) && !BIG;
   constexpr bool G_FIRST = DIRECT && KIND == kBwdLast;
@@ -728,7 +729,12 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
       }
       if constexpr (KIND == kFwdMid) {
         float2 m[N1];
-        prop(x, conj_tab, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+        if constexpr (BIG) {
+          prop(x, conj_tab, nothing);
+          load_a_table<C>(a.mod, n, off, vec, vok, m);
+        } else {
+          prop(x, conj_tab, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+        }
         // U_l = M_l A_l, zero outside the aperture (crop)
         static_for<0, N1>([&](auto k) { x[k.value] = cmul(x[k.value], m[k.value]); });
       }
@@ -920,7 +926,8 @@ __device__ __forceinline__ void b_inverse_all(const Tile<C>& t) {
   }
 }
 
-// Spectrum rows (pitch N, slot order) of a row tile <-> shared memory.
+// Spectrum rows (pitch N, slot order) of a row tile <-> shared memory (the
+// loads are non-temporal: each row is read once per pass).
 template <class C>
 __device__ __forceinline__ void load_spec_rows(float2* lds, const float2* __restrict__ in, int vec0, int nvalid) {
   float2 buf[C::N1];
@@ -928,7 +935,7 @@ __device__ __forceinline__ void load_spec_rows(float2* lds, const float2* __rest
   const int tid = opaque_tid();
   static_for<0, C::N1>([&](auto i) {
     const int e = tid + i.value * C::P;
-    if (e < total) buf[i.value] = ld(in, vec0 * C::N + e);
+    if (e < total) buf[i.value] = ld_stream(in, vec0 * C::N + e);
   });
   static_for<0, C::N1>([&](auto i) {
     const int e = tid + i.value * C::P;
