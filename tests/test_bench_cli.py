@@ -1,0 +1,44 @@
+"""Host-side checks of bench.py: the one-GPU guard, the algorithmic byte
+counts behind `roofline.achieved`, and the traffic lookup that reports
+counter bytes only for the device sources they were measured on."""
+
+import json
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    doc = json.loads(r.stdout.strip().splitlines()[-1])
+    assert doc["n_gpus"] == 2 and "one GPU" in doc["error"]
+
+
+def test_algorithmic_bytes_per_sample():
+    # one field read and one written (complex64) forward; gradient read, saved field read,
+    # gradient written backward
+    assert bench.algorithmic_bytes_per_sample("fwd_mid", 200) == 16 * 200 * 200
+    assert bench.algorithmic_bytes_per_sample("bwd_mid", 200) == 24 * 200 * 200
+
+
+def test_traffic_reported_only_for_matching_sources(tmp_path, monkeypatch):
+    from paper_2306_11268_amd import build as lb
+
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    name = "wl"
+    doc = {"source_digest": lb.source_digest(), "kernels": {"k": {"hbm_bytes_per_dispatch": 123}}}
+    (prof / f"fresnel_passes__{name}__traffic.json").write_text(json.dumps(doc))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.recorded_traffic(name, "k") == 123
+    assert bench.recorded_traffic(name, "other") is None
+    doc["source_digest"] = "0" * 16
+    (prof / f"fresnel_passes__{name}__traffic.json").write_text(json.dumps(doc))
+    assert bench.recorded_traffic(name, "k") is None
