@@ -40,7 +40,16 @@ Readings taken where the paper is silent or ambiguous:
   dL/dI may be given instead;
 * gradients follow the Wirtinger convention g = dL/dRe(U) + j dL/dIm(U), so
   dL/dI contributes 2*(dL/dI)*U and dL/dphi_l = Im(conj(U_l) * g_l), with
-  g_l the gradient with respect to the modulated field of layer l.
+  g_l the gradient with respect to the modulated field of layer l;
+* the segmentation DONN (§5.6.2), whose topology the paper gives only in a
+  figure: its optical skip connection is read as the residual form
+  y = F(x) + x with the whole diffractive stack as F, i.e. the input field
+  is relayed unchanged to the detector plane and added to the field the
+  last hop delivers, U_D = P(U_L) + U_0 (``skip``: any field added there);
+  its layer normalisation (training only, before the detector) normalises
+  each sample's intensity map over its n x n pixels to zero mean and unit
+  variance, (I - mean) / sqrt(var + eps) with the biased variance, without
+  a learnable gain or bias.
 """
 
 from __future__ import annotations
@@ -278,12 +287,15 @@ def region_scatter(grad_sums: np.ndarray, det: Detector, n: int) -> np.ndarray:
 # ---------------------------------------------------------------------------
 
 def donn_forward(amp: np.ndarray, phi: np.ndarray, h: np.ndarray, gamma: float = 1.0,
-                 det: Optional[Detector] = None) -> dict:
+                 det: Optional[Detector] = None, skip: Optional[np.ndarray] = None) -> dict:
     """Forward pass of an L-layer DONN on a batch.
 
     amp [B, n, n] amplitudes, phi [L, n, n] phase masks, h [m, m].
     Returns acts [L, B, n, n] (modulated field of each layer), field (the
     detector-plane field U_D), intensity |U_D|^2 and, with a detector, sums.
+    skip [B, n, n] (complex), when given, is added to the detector-plane
+    field (the segmentation DONN's optical skip connection, §5.6.2: the
+    input field itself under the residual reading).
     """
     u = encode_amplitude(amp)
     phi = np.asarray(phi, dtype=np.float64)
@@ -292,6 +304,8 @@ def donn_forward(amp: np.ndarray, phi: np.ndarray, h: np.ndarray, gamma: float =
         u = modulate(propagate(u, h), phi[layer], gamma)
         acts.append(u)
     ud = propagate(u, h)
+    if skip is not None:
+        ud = ud + np.asarray(skip, dtype=np.complex128)
     i_map = intensity(ud)
     return {
         "acts": np.stack(acts) if acts else np.zeros((0,) + u.shape, np.complex128),
@@ -368,6 +382,31 @@ def donn_backward(fwd: dict, phi: np.ndarray, h: np.ndarray, gamma: float = 1.0,
         if layer > 0:
             g = propagate(g, h, adjoint=True)
     return dphi
+
+
+# ---------------------------------------------------------------------------
+# Layer normalisation before the detector of the segmentation DONN (§5.6.2,
+# training only), per sample over the intensity map.
+# ---------------------------------------------------------------------------
+
+def layer_norm(i_map: np.ndarray, eps: float = 1e-5):
+    """(I - mean) / sqrt(var + eps) over the last two axes of each sample
+    (biased variance).  Returns (normalised map, mean [B], 1/sqrt(var+eps) [B])."""
+    x = np.asarray(i_map, dtype=np.float64)
+    mean = x.mean(axis=(-2, -1))
+    var = ((x - mean[:, None, None]) ** 2).mean(axis=(-2, -1))
+    rstd = 1.0 / np.sqrt(var + eps)
+    return (x - mean[:, None, None]) * rstd[:, None, None], mean, rstd
+
+
+def layer_norm_backward(grad_out: np.ndarray, normed: np.ndarray, rstd: np.ndarray) -> np.ndarray:
+    """dL/dI from dL/d(normalised map): with y = (x - mean) * rstd over M
+    pixels, dL/dx = rstd * (g - mean(g) - y * mean(g * y))."""
+    g = np.asarray(grad_out, dtype=np.float64)
+    y = np.asarray(normed, dtype=np.float64)
+    mg = g.mean(axis=(-2, -1))[:, None, None]
+    mgy = (g * y).mean(axis=(-2, -1))[:, None, None]
+    return np.asarray(rstd, dtype=np.float64)[:, None, None] * (g - mg - y * mgy)
 
 
 # ---------------------------------------------------------------------------

@@ -578,3 +578,91 @@ def codesign_grad_fd(tau=0.7):
         fd[idx] = (np.sum(c * od.codesign_phase(lp, noise, levels, tau)[0]) -
                    np.sum(c * od.codesign_phase(lm, noise, levels, tau)[0])) / (2 * eps)
     return rel(got, fd)
+
+
+# ---------------------------------------------------------------------------
+# Segmentation DONN (§5.6.2): optical skip connection and layer normalisation
+# ---------------------------------------------------------------------------
+
+def _skip_case(n=12, m=12, L=2, B=3, seed=61):
+    amp, phi, h, gamma, det, t, gi = _tiny_net(n=n, m=m, L=L, B=B, seed=seed)
+    skip = od.encode_amplitude(amp)   # the residual reading: the input field itself
+    return amp, phi, h, gamma, det, gi, skip
+
+
+def skip_adds_at_detector():
+    """The detector field with the skip minus the field without it is the skip
+    field itself (it is added after the last hop), and with gamma = 0 (no
+    light through the layers) the intensity is |skip|^2."""
+    amp, phi, h, gamma, det, gi, skip = _skip_case()
+    with_skip = od.donn_forward(amp, phi, h, gamma, det, skip=skip)
+    without = od.donn_forward(amp, phi, h, gamma, det)
+    e1 = rel(with_skip["field"] - without["field"], skip)
+    dark = od.donn_forward(amp, phi, h, 0.0, det, skip=skip)
+    e2 = rel(dark["intensity"], np.abs(skip) ** 2)
+    return max(e1, e2)
+
+
+def layer_norm_moments(eps=1e-5):
+    """Each normalised map has mean 0 and variance var / (var + eps); a
+    constant map normalises to zero."""
+    g = np.random.default_rng(62)
+    x = g.uniform(0, 3, (4, 7, 5)) ** 2
+    y, mean, rstd = od.layer_norm(x, eps)
+    var = x.var(axis=(1, 2))
+    e_mean = np.abs(y.mean(axis=(1, 2))).max()
+    e_var = rel(y.var(axis=(1, 2)), var / (var + eps))
+    e_stats = max(rel(mean, x.mean(axis=(1, 2))), rel(rstd, 1.0 / np.sqrt(var + eps)))
+    const, _, _ = od.layer_norm(np.full((2, 3, 3), 5.0), eps)
+    return max(e_mean, e_var, e_stats, np.abs(const).max())
+
+
+def layer_norm_affine_invariance():
+    """With eps = 0 the normalised map does not change under x -> a x + c, a > 0."""
+    g = np.random.default_rng(63)
+    x = g.standard_normal((3, 6, 6))
+    y0, _, _ = od.layer_norm(x, 0.0)
+    y1, _, _ = od.layer_norm(2.5 * x - 7.0, 0.0)
+    return rel(y1, y0)
+
+
+def layer_norm_grad_fd(eps=1e-5):
+    """Central finite differences of L = sum G * LN(x) against layer_norm_backward."""
+    g = np.random.default_rng(64)
+    x = g.uniform(0, 2, (2, 4, 5))
+    G = g.standard_normal(x.shape)
+    y, _, rstd = od.layer_norm(x, eps)
+    dx = od.layer_norm_backward(G, y, rstd)
+    h = 1e-6
+    fd = np.zeros_like(x)
+    for idx in np.ndindex(x.shape):
+        xp = x.copy()
+        xp[idx] += h
+        xm = x.copy()
+        xm[idx] -= h
+        fd[idx] = (np.sum(G * od.layer_norm(xp, eps)[0]) - np.sum(G * od.layer_norm(xm, eps)[0])) / (2 * h)
+    return rel(dx, fd)
+
+
+def segmentation_grad_fd(eps=1e-5):
+    """Whole segmentation training chain, L = sum G * LN(|P(U_L) + U_0|^2):
+    central finite differences in every phase entry against donn_backward
+    seeded with the layer norm's backward."""
+    amp, phi, h, gamma, det, gi, skip = _skip_case(n=8, m=8)
+
+    def loss(p):
+        out = od.donn_forward(amp, p, h, gamma, None, skip=skip)
+        return float(np.sum(gi * od.layer_norm(out["intensity"], eps)[0]))
+
+    out = od.donn_forward(amp, phi, h, gamma, None, skip=skip)
+    y, _, rstd = od.layer_norm(out["intensity"], eps)
+    dphi = od.donn_backward(out, phi, h, gamma, grad_intensity=od.layer_norm_backward(gi, y, rstd))
+    step = 1e-6
+    fd = np.zeros_like(phi)
+    for idx in np.ndindex(phi.shape):
+        pp = phi.copy()
+        pp[idx] += step
+        pm = phi.copy()
+        pm[idx] -= step
+        fd[idx] = (loss(pp) - loss(pm)) / (2 * step)
+    return rel(dphi, fd)

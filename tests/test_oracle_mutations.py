@@ -16,7 +16,8 @@ _orig = {name: getattr(od, name) for name in (
     "modulate", "detector_readout", "region_scatter", "softmax_cross_entropy",
     "mse_softmax_loss", "donn_forward", "donn_backward", "adam_update",
     "impulse_response", "displacements", "fraunhofer", "fraunhofer_pitch",
-    "multichannel_forward", "multichannel_backward", "codesign_phase", "codesign_backward")}
+    "multichannel_forward", "multichannel_backward", "codesign_phase", "codesign_backward",
+    "layer_norm", "layer_norm_backward")}
 
 
 def _dft_sign_flipped(m, inverse=False):
@@ -203,6 +204,39 @@ def _codesign_backward_no_centering(w, levels, tau, grad_phi):
     return w * lv * (np.asarray(grad_phi, np.float64)[..., None] / tau)
 
 
+def _forward_skip_before_last_hop(amp, phi, h, gamma=1.0, det=None, skip=None):
+    if skip is None:
+        return _orig["donn_forward"](amp, phi, h, gamma, det)
+    # the skip field joins the last layer's output instead of the detector-plane field
+    out = _orig["donn_forward"](amp, phi, h, gamma, det)
+    ud = od.propagate(out["acts"][-1] + skip, h)
+    out["field"] = ud
+    out["intensity"] = od.intensity(ud)
+    out["sums"] = od.detector_readout(out["intensity"], det) if det is not None else None
+    return out
+
+
+def _forward_skip_not_in_field(amp, phi, h, gamma=1.0, det=None, skip=None):
+    # the intensity sees the skip, the stored detector field (the adjoint's seed) does not
+    out = _orig["donn_forward"](amp, phi, h, gamma, det, skip=skip)
+    if skip is not None:
+        out["field"] = out["field"] - skip
+    return out
+
+
+def _layer_norm_unbiased(i_map, eps=1e-5):
+    x = np.asarray(i_map, dtype=np.float64)
+    mean = x.mean(axis=(-2, -1))
+    var = x.var(axis=(-2, -1), ddof=1)
+    rstd = 1.0 / np.sqrt(var + eps)
+    return (x - mean[:, None, None]) * rstd[:, None, None], mean, rstd
+
+
+def _layer_norm_backward_no_projection(grad_out, normed, rstd):
+    g = np.asarray(grad_out, dtype=np.float64)
+    return np.asarray(rstd)[:, None, None] * (g - g.mean(axis=(-2, -1))[:, None, None])
+
+
 MUTANTS = [
     ("dft_sign", "dft_matrix", _dft_sign_flipped, lambda: c.dft_vs_numpy() > 1e-3),
     ("idft_norm", "idft2", _idft_unnormalised, lambda: c.dft_delta_parseval() > 1e-3),
@@ -241,6 +275,12 @@ MUTANTS = [
     ("bwd_sign", "donn_backward", _make_backward("sign"), lambda: _fails_grad(mode="ce")),
     ("bwd_mask_not_conj", "donn_backward", _make_backward("mask_not_conj"), lambda: _fails_grad(mode="map")),
     ("bwd_no_gamma", "donn_backward", _make_backward("no_gamma"), lambda: _fails_grad(mode="map", gamma=0.7)),
+    ("skip_before_last_hop", "donn_forward", _forward_skip_before_last_hop,
+     lambda: c.skip_adds_at_detector() > 1e-3),
+    ("skip_not_in_seed", "donn_forward", _forward_skip_not_in_field, lambda: c.segmentation_grad_fd() > 1e-3),
+    ("layer_norm_unbiased_var", "layer_norm", _layer_norm_unbiased, lambda: c.layer_norm_moments() > 1e-3),
+    ("layer_norm_grad_no_projection", "layer_norm_backward", _layer_norm_backward_no_projection,
+     lambda: c.layer_norm_grad_fd() > 1e-3),
 ]
 
 

@@ -175,3 +175,24 @@ def test_codesign_limits_and_shift_invariance():
 
 def test_codesign_gradient_by_finite_differences():
     assert c.codesign_grad_fd() < 1e-8
+
+
+def test_segmentation_skip_adds_at_the_detector():
+    assert c.skip_adds_at_detector() < 1e-13
+
+
+def test_layer_norm_moments_and_constant_map():
+    assert c.layer_norm_moments() < 1e-12
+
+
+def test_layer_norm_affine_invariance():
+    assert c.layer_norm_affine_invariance() < 1e-12
+
+
+def test_layer_norm_gradient_by_finite_differences():
+    assert c.layer_norm_grad_fd() < 1e-7
+
+
+def test_segmentation_chain_gradient_by_finite_differences():
+    # skip + layer norm + DONN, central differences with step 1e-6 in float64
+    assert c.segmentation_grad_fd() < 1e-6
