@@ -114,6 +114,15 @@ typedef struct lr_donn {
                            wavelength / pixel_pitch / distance / approx / n_fft.
                            The Fresnel path relies on its separability. */
   int32_t flags;        /* 0 or LR_ACCUMULATE */
+  const lr_c64* d_skip; /* NULL, or device [batch][n][n]: a field added to the
+                           detector-plane field before the intensity, the sums,
+                           the field output or the backward seed are formed.
+                           This is the optical skip connection of the
+                           segmentation DONN (§5.6.2); under the residual
+                           reading (the stack of layers as F in F(x) + x) it is
+                           the input field itself, relayed to the detector.
+                           lr_donn_forward and lr_donn_backward must see the
+                           same field; it must not alias d_field_out. */
 } lr_donn;
 
 /* lr_donn.flags: lr_donn_forward adds its detector sums and intensity map
@@ -236,6 +245,29 @@ enum lr_loss_kind {
  * in 1..LR_MAX_REGIONS), LR_E_NULL, LR_E_ALIAS. */
 int lr_loss(int32_t kind, const float* d_sums, const int32_t* d_labels, int32_t batch, int32_t classes,
             float* d_loss, float* d_grad_sums, void* stream);
+
+/* Layer normalisation before the detector of the segmentation DONN (§5.6.2,
+ * used in training only): each of the batch maps of count values (an
+ * intensity map, count = n*n) is normalised to zero mean and unit variance,
+ *   y = (x - mean) / sqrt(var + eps),  var the biased variance,
+ * without a learnable gain or bias.  lr_layer_norm_backward returns
+ *   dL/dx = rstd * (g - mean(g) - y * mean(g * y)),  g = dL/dy, rstd = 1/sqrt(var + eps).
+ *   d_x, d_y        float32 [batch][count]; d_y may be d_x
+ *   d_stats         float32 [batch][2]: (mean, rstd) of each map, written by
+ *                   lr_layer_norm and read by lr_layer_norm_backward
+ *   d_grad_y, d_grad_x  float32 [batch][count]; d_grad_x may be d_grad_y
+ *   d_work          lr_layer_norm_workspace_size(batch, count) bytes
+ * The statistics are merged over fixed chunks of 4096 values in a fixed
+ * order (results are reproducible).  Errors: LR_E_SIZE (batch < 0 or
+ * > 65535, count < 1 or > 2^28), LR_E_ARG (eps not finite or < 0),
+ * LR_E_NULL, LR_E_WORKSPACE, LR_E_ALIAS (maps overlapping other than in the
+ * two in-place forms above, or d_stats or the workspace overlapping a map),
+ * LR_E_HIP.  batch = 0 does nothing. */
+int64_t lr_layer_norm_workspace_size(int32_t batch, int64_t count);
+int lr_layer_norm(const float* d_x, int32_t batch, int64_t count, float eps, float* d_y, float* d_stats,
+                  void* d_work, size_t work_bytes, void* stream);
+int lr_layer_norm_backward(const float* d_grad_y, const float* d_y, const float* d_stats, int32_t batch,
+                           int64_t count, float* d_grad_x, void* d_work, size_t work_bytes, void* stream);
 
 /* Codesign layer (§3.2): trainable scores over the discrete, measured
  * optical responses of the hardware, relaxed with Gumbel-Softmax so that the

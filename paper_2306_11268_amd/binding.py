@@ -31,6 +31,7 @@ EXPORTS = (
     "lr_tf_build", "lr_workspace_size", "lr_saved_size",
     "lr_propagate", "lr_detector_readout", "lr_donn_forward", "lr_donn_backward",
     "lr_loss", "lr_adam_update", "lr_codesign_phase", "lr_codesign_backward",
+    "lr_layer_norm_workspace_size", "lr_layer_norm", "lr_layer_norm_backward",
     "lr_status_string", "lr_kernel_timing", "lr_kernel_timing_report", "lr_version",
 )
 
@@ -44,6 +45,7 @@ class LrDonn(ctypes.Structure):
         ("wavelength", c_double), ("pixel_pitch", c_double), ("distance", c_double),
         ("approx", c_int32), ("n", c_int32), ("n_fft", c_int32), ("num_layers", c_int32),
         ("gamma", c_float), ("det", LrDetector), ("d_H", c_void_p), ("flags", c_int32),
+        ("d_skip", c_void_p),
     ]
 
 
@@ -78,6 +80,10 @@ def load() -> ctypes.CDLL:
     lib.lr_adam_update.argtypes = [P, P, P, P, c_int64, c_int32, c_float, c_float, c_float, c_float, P]
     lib.lr_codesign_phase.argtypes = [P, P, P, c_int32, c_int64, c_float, c_int32, P, P]
     lib.lr_codesign_backward.argtypes = [P, P, P, c_int32, c_int64, c_float, P, P, P]
+    lib.lr_layer_norm_workspace_size.argtypes = [c_int32, c_int64]
+    lib.lr_layer_norm_workspace_size.restype = c_int64
+    lib.lr_layer_norm.argtypes = [P, c_int32, c_int64, c_float, P, P, P, c_size_t, P]
+    lib.lr_layer_norm_backward.argtypes = [P, P, P, c_int32, c_int64, P, P, c_size_t, P]
     lib.lr_status_string.argtypes = [ctypes.c_int]
     lib.lr_status_string.restype = c_char_p
     lib.lr_kernel_timing.argtypes = [c_int32]
@@ -242,21 +248,33 @@ def lr_detector_readout(field, detector: Detector, out=None):
     return out
 
 
+def _with_skip(desc, skip, b: int, n: int):
+    """The descriptor with d_skip set to a complex64 [b, n, n] field (a copy), or desc."""
+    if skip is None:
+        return desc
+    torch = _torch()
+    d = LrDonn.from_buffer_copy(desc)
+    d.d_skip = _ptr(skip, torch.complex64, (b, n, n), "skip").value
+    return d
+
+
 def lr_donn_forward(net: Network, amp, phi, saved=None, sums: bool = True, intensity: bool = False,
                     field: bool = False, out_sums=None, out_intensity=None, out_field=None,
-                    accumulate: bool = False):
+                    accumulate: bool = False, skip=None):
     """Forward pass; returns a dict with the requested outputs (device tensors).
     With accumulate the sums / intensity are added into out_sums / out_intensity
-    (LR_ACCUMULATE), which must then be given."""
+    (LR_ACCUMULATE), which must then be given.  skip: complex64 [B, n, n]
+    added to the detector-plane field (lr_donn.d_skip); give the same field
+    to lr_donn_backward."""
     torch = _torch()
     b = int(amp.shape[0])
     n, L = net.n, net.num_layers
     dev = net.device
-    desc = net.c
+    desc = _with_skip(net.c, skip, b, n)
     if accumulate:
         if (sums and out_sums is None) or (intensity and out_intensity is None) or field:
             raise ValueError("accumulate needs out_sums / out_intensity and no field output")
-        desc = LrDonn.from_buffer_copy(net.c)
+        desc = LrDonn.from_buffer_copy(desc)
         desc.flags = LR_ACCUMULATE
     if sums and net.detector.num > 0 and out_sums is None:
         out_sums = torch.empty((b, net.detector.num), dtype=torch.float32, device=dev)
@@ -278,8 +296,9 @@ def lr_donn_forward(net: Network, amp, phi, saved=None, sums: bool = True, inten
 
 
 def lr_donn_backward(net: Network, phi, saved, sums=None, labels=None, grad_sums=None, grad_intensity=None,
-                     out_grad_phi=None, want_loss: bool = True):
-    """dL/dphi [L, n, n] (and the loss when labels are given)."""
+                     out_grad_phi=None, want_loss: bool = True, skip=None):
+    """dL/dphi [L, n, n] (and the loss when labels are given); skip as given
+    to lr_donn_forward."""
     torch = _torch()
     n, L = net.n, net.num_layers
     dev = net.device
@@ -289,8 +308,9 @@ def lr_donn_backward(net: Network, phi, saved, sums=None, labels=None, grad_sums
         out_grad_phi = torch.empty((L, n, n), dtype=torch.float32, device=dev)
     loss = torch.empty((), dtype=torch.float32, device=dev) if (labels is not None and want_loss) else None
     w = net.workspace(b, LR_OP_BACKWARD)
+    desc = _with_skip(net.c, skip, b, n)
     _check(load().lr_donn_backward(
-        ctypes.byref(net.c), b, _ptr(phi, torch.float32, (L, n, n), "phi"), _ptr(saved, torch.uint8, None, "saved"),
+        ctypes.byref(desc), b, _ptr(phi, torch.float32, (L, n, n), "phi"), _ptr(saved, torch.uint8, None, "saved"),
         _ptr(sums, torch.float32, None, "sums"), _ptr(labels, torch.int32, None, "labels"),
         _ptr(grad_sums, torch.float32, None, "grad_sums"), _ptr(grad_intensity, torch.float32, None, "grad_intensity"),
         _ptr(loss, torch.float32, None, "loss"), _ptr(out_grad_phi, torch.float32, (L, n, n), "grad_phi"),
@@ -322,6 +342,48 @@ def lr_adam_update(phi, grad, m, v, step: int, lr: float = 0.5, beta1: float = 0
                                  int(step), float(lr), float(beta1), float(beta2), float(eps),
                                  _stream(phi.device)), "lr_adam_update")
     return phi
+
+
+def _ln_workspace(batch: int, count: int, device):
+    torch = _torch()
+    r = load().lr_layer_norm_workspace_size(int(batch), int(count))
+    if r < 0:
+        raise LrError(int(-r), "lr_layer_norm_workspace_size")
+    return torch.empty(max(int(r), 1), dtype=torch.uint8, device=device)
+
+
+def lr_layer_norm(x, eps: float = 1e-5, out=None, out_stats=None):
+    """Per-sample layer normalisation of maps x [B, ...] (float32): returns
+    (normalised maps, stats [B, 2] = (mean, 1/sqrt(var + eps)))."""
+    torch = _torch()
+    b = int(x.shape[0])
+    shape = tuple(x.shape)
+    count = int(x.numel()) // max(b, 1)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.float32, device=x.device)
+    if out_stats is None:
+        out_stats = torch.empty((b, 2), dtype=torch.float32, device=x.device)
+    w = _ln_workspace(b, count, x.device)
+    _check(load().lr_layer_norm(_ptr(x, torch.float32, shape, "x"), b, count, float(eps),
+                                _ptr(out, torch.float32, shape, "y"), _ptr(out_stats, torch.float32, (b, 2), "stats"),
+                                _ptr(w), w.numel(), _stream(x.device)), "lr_layer_norm")
+    return out, out_stats
+
+
+def lr_layer_norm_backward(grad_y, y, stats, out=None):
+    """dL/dx [B, ...] from dL/dy, the normalised maps y and their stats."""
+    torch = _torch()
+    b = int(y.shape[0])
+    shape = tuple(y.shape)
+    count = int(y.numel()) // max(b, 1)
+    if out is None:
+        out = torch.empty(shape, dtype=torch.float32, device=y.device)
+    w = _ln_workspace(b, count, y.device)
+    _check(load().lr_layer_norm_backward(_ptr(grad_y, torch.float32, shape, "grad_y"), _ptr(y, torch.float32, shape, "y"),
+                                         _ptr(stats, torch.float32, (b, 2), "stats"), b, count,
+                                         _ptr(out, torch.float32, shape, "grad_x"), _ptr(w), w.numel(),
+                                         _stream(y.device)), "lr_layer_norm_backward")
+    return out
 
 
 def kernel_timing(enable: bool) -> None:

@@ -666,6 +666,8 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   if (d_sums && net->det.num == 0) return LR_E_ARG;
   const bool accumulate = (net->flags & LR_ACCUMULATE) != 0;
   if (accumulate && d_field_out) return LR_E_ARG;  // fields of separate channels do not add
+  if (net->d_skip && static_cast<const void*>(net->d_skip) == static_cast<const void*>(d_field_out))
+    return LR_E_ALIAS;
   Layout L;
   LR_TRY(check_work(net, batch, LR_OP_FORWARD, d_work, work_bytes, &L));
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -716,6 +718,7 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
       d.mod = nullptr;
       d.intensity = d_intensity;
       d.field_out = reinterpret_cast<float2*>(d_field_out);
+      d.skip = reinterpret_cast<const float2*>(net->d_skip);
       if (d_sums) {
         set_detector(d, net->det, L, d_work);
         d.sums_part = at<float>(d_work, L.sums_part);
@@ -754,6 +757,7 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
       } else {
         PassArgs r = a;
         r.in = w[cur];
+        r.skip = reinterpret_cast<const float2*>(net->d_skip);
         r.intensity = d_intensity;
         r.field_out = reinterpret_cast<float2*>(d_field_out);
         r.saved_ud = saved ? saved + static_cast<size_t>(Lyr) * batch * nn : nullptr;
@@ -842,6 +846,7 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
       s.in = saved + static_cast<size_t>(Lyr) * batch * nn;
       s.grad_int = d_grad_intensity;
       s.grad_sums = gsum;
+      s.skip = reinterpret_cast<const float2*>(net->d_skip);
       if (gsum) {
         set_detector(s, net->det, L, d_work);
         // The seed vanishes off the covered rows (columns).  A row seed pass
@@ -953,6 +958,76 @@ int lr_codesign_backward(const float* d_logits, const float* d_noise, const floa
   return run_timed("codesign_bwd", st, [&] {
     return lr::launch_codesign(d_logits, d_noise, d_levels, levels, static_cast<long long>(count), tau, 0,
                                d_grad_phi, d_grad_logits, st);
+  });
+}
+
+namespace {
+constexpr int64_t kLnMaxCount = int64_t(1) << 28;
+
+int ln_check(int32_t batch, int64_t count) {
+  if (batch < 0 || batch > 65535 || count < 1 || count > kLnMaxCount) return LR_E_SIZE;
+  return LR_OK;
+}
+
+size_t ln_work_bytes(int32_t batch, int64_t count) {
+  return static_cast<size_t>(batch) * static_cast<size_t>(lr::ln_chunks(count) + 1) * sizeof(float2);
+}
+
+// [p, p + bytes) and [q, q + qbytes) overlap
+bool overlaps(const void* p, size_t bytes, const void* q, size_t qbytes) {
+  const char* a = static_cast<const char*>(p);
+  const char* b = static_cast<const char*>(q);
+  return a < b + qbytes && b < a + bytes;
+}
+}  // namespace
+
+int64_t lr_layer_norm_workspace_size(int32_t batch, int64_t count) {
+  const int e = ln_check(batch, count);
+  if (e != LR_OK) return -static_cast<int64_t>(e);
+  return static_cast<int64_t>(ln_work_bytes(batch, count));
+}
+
+int lr_layer_norm(const float* d_x, int32_t batch, int64_t count, float eps, float* d_y, float* d_stats,
+                  void* d_work, size_t work_bytes, void* stream) {
+  LR_TRY(ln_check(batch, count));
+  if (!std::isfinite(eps) || eps < 0.f) return LR_E_ARG;
+  if (batch == 0) return LR_OK;
+  if (!d_x || !d_y || !d_stats || !d_work) return LR_E_NULL;
+  if (work_bytes < ln_work_bytes(batch, count)) return LR_E_WORKSPACE;
+  const size_t map_bytes = static_cast<size_t>(batch) * static_cast<size_t>(count) * sizeof(float);
+  const size_t stat_bytes = static_cast<size_t>(batch) * 2 * sizeof(float);
+  if (d_y != d_x && overlaps(d_y, map_bytes, d_x, map_bytes)) return LR_E_ALIAS;
+  if (overlaps(d_stats, stat_bytes, d_x, map_bytes) || overlaps(d_stats, stat_bytes, d_y, map_bytes) ||
+      overlaps(d_work, work_bytes, d_x, map_bytes) || overlaps(d_work, work_bytes, d_y, map_bytes))
+    return LR_E_ALIAS;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  float2* part = static_cast<float2*>(d_work);
+  return run_timed("layer_norm", st, [&] {
+    return lr::launch_layer_norm(d_x, batch, static_cast<long long>(count), eps, d_y,
+                                 reinterpret_cast<float2*>(d_stats), part, st);
+  });
+}
+
+int lr_layer_norm_backward(const float* d_grad_y, const float* d_y, const float* d_stats, int32_t batch,
+                           int64_t count, float* d_grad_x, void* d_work, size_t work_bytes, void* stream) {
+  LR_TRY(ln_check(batch, count));
+  if (batch == 0) return LR_OK;
+  if (!d_grad_y || !d_y || !d_stats || !d_grad_x || !d_work) return LR_E_NULL;
+  if (work_bytes < ln_work_bytes(batch, count)) return LR_E_WORKSPACE;
+  const size_t map_bytes = static_cast<size_t>(batch) * static_cast<size_t>(count) * sizeof(float);
+  const size_t stat_bytes = static_cast<size_t>(batch) * 2 * sizeof(float);
+  // dx may replace g (elementwise), not the normalised maps the partial sums read
+  if (d_grad_x != d_grad_y && overlaps(d_grad_x, map_bytes, d_grad_y, map_bytes)) return LR_E_ALIAS;
+  if (overlaps(d_grad_x, map_bytes, d_y, map_bytes) || overlaps(d_grad_x, map_bytes, d_stats, stat_bytes) ||
+      overlaps(d_work, work_bytes, d_grad_x, map_bytes) || overlaps(d_work, work_bytes, d_grad_y, map_bytes) ||
+      overlaps(d_work, work_bytes, d_y, map_bytes) || overlaps(d_work, work_bytes, d_stats, stat_bytes))
+    return LR_E_ALIAS;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  float2* part = static_cast<float2*>(d_work);
+  float2* stats2 = part + static_cast<size_t>(batch) * lr::ln_chunks(count);
+  return run_timed("layer_norm_bwd", st, [&] {
+    return lr::launch_layer_norm_backward(d_grad_y, d_y, reinterpret_cast<const float2*>(d_stats), batch,
+                                          static_cast<long long>(count), d_grad_x, part, stats2, st);
   });
 }
 

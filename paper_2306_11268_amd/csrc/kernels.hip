@@ -462,6 +462,129 @@ hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, float scale,
   }
 }
 
+// ---------------------------------------------------------------------------
+// Layer normalisation of intensity maps (per sample, over count values).
+// Chunk c of sample b covers values [c * kLnChunk, min(count, (c+1) * kLnChunk)).
+// ---------------------------------------------------------------------------
+constexpr int kLnThreads = 256;
+
+// g == nullptr: part = (chunk mean, sum of squared deviations from it);
+// otherwise part = (sum of g, sum of g * y) with y = x the normalised map.
+__global__ void __launch_bounds__(kLnThreads) ln_partial_kernel(const float* __restrict__ x,
+                                                                const float* __restrict__ g, long long count,
+                                                                int nchunks, float2* __restrict__ part) {
+  __shared__ float red[kLnThreads / 64];
+  const int c = blockIdx.x;
+  const int b = blockIdx.y;
+  const size_t base = (size_t)b * (size_t)count;
+  const long long lo = (long long)c * kLnChunk;
+  const long long hi = min(count, lo + kLnChunk);
+  float s1 = 0.f;
+  float s2 = 0.f;
+  if (g == nullptr) {
+    for (long long i = lo + threadIdx.x; i < hi; i += kLnThreads) s1 += x[base + i];
+    const float mean = block_sum<kLnThreads>(s1, red) / (float)(hi - lo);
+    for (long long i = lo + threadIdx.x; i < hi; i += kLnThreads) {
+      const float d = x[base + i] - mean;
+      s2 += d * d;
+    }
+    const float m2 = block_sum<kLnThreads>(s2, red);
+    if (threadIdx.x == 0) part[(size_t)b * nchunks + c] = c2(mean, m2);
+  } else {
+    for (long long i = lo + threadIdx.x; i < hi; i += kLnThreads) {
+      const float gv = g[base + i];
+      s1 += gv;
+      s2 += gv * x[base + i];
+    }
+    const float a = block_sum<kLnThreads>(s1, red);
+    const float bsum = block_sum<kLnThreads>(s2, red);
+    if (threadIdx.x == 0) part[(size_t)b * nchunks + c] = c2(a, bsum);
+  }
+}
+
+// One thread per sample combines its chunks in order.  Forward: the chunk
+// means and squared-deviation sums merge by the pairwise update of Chan et
+// al.; stats = (mean, 1/sqrt(M2 / count + eps)).  Backward: stats2 =
+// (mean of g, mean of g * y).
+__global__ void ln_combine_kernel(const float2* __restrict__ part, int batch, long long count, int nchunks,
+                                  float eps, int backward, float2* __restrict__ out) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= batch) return;
+  const float2* p = part + (size_t)b * nchunks;
+  if (backward) {
+    float a = 0.f;
+    float m = 0.f;
+    for (int c = 0; c < nchunks; ++c) {
+      a += p[c].x;
+      m += p[c].y;
+    }
+    out[b] = c2(a / (float)count, m / (float)count);
+    return;
+  }
+  float n_a = 0.f;
+  float mean = 0.f;
+  float m2 = 0.f;
+  for (int c = 0; c < nchunks; ++c) {
+    const long long lo = (long long)c * kLnChunk;
+    const float n_b = (float)(min(count, lo + kLnChunk) - lo);
+    const float n = n_a + n_b;
+    const float delta = p[c].x - mean;
+    mean += delta * (n_b / n);
+    m2 += p[c].y + delta * delta * (n_a * n_b / n);
+    n_a = n;
+  }
+  out[b] = c2(mean, 1.f / sqrtf(m2 / (float)count + eps));
+}
+
+// Forward: y = (x - mean) * rstd.  Backward (g != nullptr, x = y the
+// normalised map): dx = rstd * (g - mean(g) - y * mean(g * y)).
+__global__ void ln_apply_kernel(const float* __restrict__ x, const float* __restrict__ g,
+                                const float2* __restrict__ stats, const float2* __restrict__ stats2, int batch,
+                                long long count, float* __restrict__ out) {
+  const size_t total = (size_t)batch * (size_t)count;
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
+    const size_t b = i / (size_t)count;
+    const float2 s = stats[b];
+    if (g == nullptr) {
+      out[i] = (x[i] - s.x) * s.y;
+    } else {
+      const float2 s2 = stats2[b];
+      out[i] = s.y * (g[i] - s2.x - x[i] * s2.y);
+    }
+  }
+}
+
+static int ln_apply_blocks(size_t total) {
+  size_t blocks = (total + 255) / 256;
+  if (blocks > 4096) blocks = 4096;
+  return blocks < 1 ? 1 : (int)blocks;
+}
+
+hipError_t launch_layer_norm(const float* x, int batch, long long count, float eps, float* y, float2* stats,
+                             float2* part, hipStream_t st) {
+  if (batch < 1 || batch > 65535 || count < 1 || ln_chunks(count) > (1 << 30)) return hipErrorInvalidValue;
+  const int nchunks = (int)ln_chunks(count);
+  hipLaunchKernelGGL(ln_partial_kernel, dim3(nchunks, batch), dim3(kLnThreads), 0, st, x, nullptr, count, nchunks,
+                     part);
+  hipLaunchKernelGGL(ln_combine_kernel, dim3((batch + 63) / 64), dim3(64), 0, st, part, batch, count, nchunks, eps, 0,
+                     stats);
+  hipLaunchKernelGGL(ln_apply_kernel, dim3(ln_apply_blocks((size_t)batch * count)), dim3(256), 0, st, x, nullptr,
+                     stats, nullptr, batch, count, y);
+  return hipGetLastError();
+}
+
+hipError_t launch_layer_norm_backward(const float* g, const float* y, const float2* stats, int batch,
+                                      long long count, float* dx, float2* part, float2* stats2, hipStream_t st) {
+  if (batch < 1 || batch > 65535 || count < 1 || ln_chunks(count) > (1 << 30)) return hipErrorInvalidValue;
+  const int nchunks = (int)ln_chunks(count);
+  hipLaunchKernelGGL(ln_partial_kernel, dim3(nchunks, batch), dim3(kLnThreads), 0, st, y, g, count, nchunks, part);
+  hipLaunchKernelGGL(ln_combine_kernel, dim3((batch + 63) / 64), dim3(64), 0, st, part, batch, count, nchunks, 0.f, 1,
+                     stats2);
+  hipLaunchKernelGGL(ln_apply_kernel, dim3(ln_apply_blocks((size_t)batch * count)), dim3(256), 0, st, y, g, stats,
+                     stats2, batch, count, dx);
+  return hipGetLastError();
+}
+
 hipError_t launch_prep_layers(const float* phi, int layers, int n, float gamma, const int* orient_host, float2* mod,
                               const Regions* regions, int2* dst, unsigned long long* row_mask,
                               unsigned long long* col_mask, int* row_perm, int* col_perm, const float2* H, int nfft,

@@ -73,6 +73,9 @@ struct PassArgs {
   float2* field_out;
   float2* saved_ud;     // angular-spectrum path only
   float* sums_part;     // [B][ntiles][K]
+  // field added to the detector-plane field before any output or seed is
+  // formed (natural [B][n][n]; nullable): an optical skip connection
+  const float2* skip;
   // backward seed
   const float* grad_sums;  // [B][K]
   const float* grad_int;   // [B][n][n]
@@ -151,5 +154,16 @@ hipError_t launch_prep_layers(const float* phi, int layers, int n, float gamma, 
                               unsigned long long* col_mask, int* row_perm, int* col_perm, const float2* H, int nfft,
                               float2* chirp_x, float2* chirp_y, hipStream_t st);
 hipError_t launch_readout(const float2* field, int batch, int n, const Regions& r, float* sums, hipStream_t st);
+// Layer normalisation of batch maps of count values over fixed chunks of
+// kLnChunk values: part holds batch * ln_chunks(count) float2 partials and
+// stats2 batch float2.  Forward: stats[b] = (mean, 1/sqrt(var + eps)),
+// y = (x - mean) * rstd.  Backward (y the normalised maps, g = dL/dy):
+// dx = rstd * (g - mean(g) - y * mean(g * y)).
+constexpr int kLnChunk = 4096;
+inline long long ln_chunks(long long count) { return (count + kLnChunk - 1) / kLnChunk; }
+hipError_t launch_layer_norm(const float* x, int batch, long long count, float eps, float* y, float2* stats,
+                             float2* part, hipStream_t st);
+hipError_t launch_layer_norm_backward(const float* g, const float* y, const float2* stats, int batch,
+                                      long long count, float* dx, float2* part, float2* stats2, hipStream_t st);
 
 }  // namespace lr

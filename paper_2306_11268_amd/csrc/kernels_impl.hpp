@@ -483,6 +483,22 @@ __device__ __forceinline__ void for_a_elems(int off, int n, int pitch, int vec, 
   });
 }
 
+// Add the skip field of sample b (natural layout) to this thread's A-item of
+// detector-plane values along vector vec (a row for row passes, a column for
+// column passes); positions outside the aperture are left as they are.
+template <class C, int AXIS>
+__device__ __forceinline__ void add_skip(const PassArgs& a, int b, int vec, bool vok, float2 (&x)[C::N1]) {
+  if (!a.skip) return;
+  const int n = a.n;
+  const float2* __restrict__ sk = a.skip + (size_t)b * n * n;
+  for_a_elems<C>(a.off, n, 1, 0, vok, [&](auto k, int q, bool in) {
+    if (in) {
+      const float2 s = ld(sk, AXIS == kRow ? vec * n + q : q * n + vec);
+      x[k.value] = c2(x[k.value].x + s.x, x[k.value].y + s.y);
+    }
+  });
+}
+
 // (in / out: n rows of pitch elements, wave-uniform)
 template <class C>
 __device__ __forceinline__ void load_a_direct(const float2* __restrict__ in, int pitch, int n, int off, int vec,
@@ -840,6 +856,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES) detector_pass(PassArgs a) {
     __syncthreads();
     read_a(t, j, x);
     Dft<N1, 1>::run(x);
+    add_skip<C, AXIS>(a, b, vec, vok, x);
 
     if constexpr (KIND == kFwdLast) {
       write_a(t, j, x);
@@ -1109,6 +1126,7 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
       __syncthreads();
       store_spec_rows<C>(lds, a.out + (size_t)b * n * N, vec0, nvalid);
     } else {
+      if constexpr (KIND == kAsRowLast) add_skip<C, kRow>(a, b, vec, vok, x);
       write_a(t, j, x);  // positions, cropped on output
       __syncthreads();
       if constexpr (KIND == kAsRowIfft) {

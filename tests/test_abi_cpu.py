@@ -192,3 +192,44 @@ def test_codesign_rejects_bad_arguments_without_touching_the_gpu():
     assert lib.lr_codesign_backward(a, b, c, 16, 10, 1.0, d, None, None) == 1
     assert lib.lr_codesign_backward(a, b, c, 16, 10, 1.0, d, d, None) == 7
     assert lib.lr_codesign_backward(a, b, c, 16, 10, -2.0, d, P(0x5000), None) == 3
+
+
+@needs_lib
+def test_layer_norm_rejects_bad_arguments_without_touching_the_gpu():
+    lib = lb.load()
+    P = ctypes.c_void_p
+    count = 200 * 200
+    ws = lib.lr_layer_norm_workspace_size(4, count)
+    assert ws == 4 * (((count + 4095) // 4096) + 1) * 8
+    assert lib.lr_layer_norm_workspace_size(-1, count) == -2
+    assert lib.lr_layer_norm_workspace_size(4, 0) == -2
+    assert lib.lr_layer_norm_workspace_size(4, (1 << 28) + 1) == -2
+    x, y, st, w = P(0x10000000), P(0x20000000), P(0x30000000), P(0x40000000)
+    assert lib.lr_layer_norm(x, -1, count, 1e-5, y, st, w, ws, None) == 2
+    assert lib.lr_layer_norm(x, 4, 0, 1e-5, y, st, w, ws, None) == 2
+    assert lib.lr_layer_norm(x, 4, count, float("nan"), y, st, w, ws, None) == 3
+    assert lib.lr_layer_norm(x, 4, count, -1.0, y, st, w, ws, None) == 3
+    assert lib.lr_layer_norm(None, 4, count, 1e-5, y, st, w, ws, None) == 1
+    assert lib.lr_layer_norm(x, 4, count, 1e-5, y, st, w, ws - 1, None) == 6
+    assert lib.lr_layer_norm(x, 4, count, 1e-5, y, P(0x10000000 + 64), w, ws, None) == 7    # stats inside x
+    assert lib.lr_layer_norm(x, 4, count, 1e-5, P(0x10000000 + 8), st, w, ws, None) == 7    # y overlaps x
+    assert lib.lr_layer_norm(None, 0, count, 1e-5, None, None, None, 0, None) == 0
+    g = P(0x50000000)
+    assert lib.lr_layer_norm_backward(g, y, st, 4, count, None, w, ws, None) == 1
+    assert lib.lr_layer_norm_backward(g, y, st, 4, count, x, w, ws - 8, None) == 6
+    assert lib.lr_layer_norm_backward(g, y, st, 4, count, y, w, ws, None) == 7     # dx over the normalised maps
+    assert lib.lr_layer_norm_backward(g, y, st, 4, count, P(0x50000000 + 4), w, ws, None) == 7
+    assert lib.lr_layer_norm_backward(g, y, st, 4, 0, x, w, ws, None) == 2
+
+
+@needs_lib
+def test_skip_field_must_not_alias_the_field_output():
+    lib = lb.load()
+    P = ctypes.c_void_p
+    net = _net()
+    net.d_skip = 0x3000
+    dummy = P(0x1000)
+    need = lib.lr_workspace_size(ctypes.byref(net), 2, lb.LR_OP_FORWARD)
+    assert need > 0
+    assert lib.lr_donn_forward(ctypes.byref(net), 2, dummy, dummy, None, None, None, P(0x3000), dummy, need,
+                               None) == 7
