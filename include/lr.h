@@ -30,8 +30,8 @@
  *     Device-side faults surface at the caller's next synchronisation.
  *   - No C++ exception crosses the ABI.  Calls on distinct streams are
  *     thread safe; calls that share a workspace must be ordered by the caller.
- *   - Supported FFT grid sizes n_fft: 64, 100, 128, 200, 256, 400, 500,
- *     512, 1000, 1024.  The layer size n satisfies 1 <= n <= n_fft with n_fft - n
+ *   - Supported FFT grid sizes n_fft: 64, 100, 128, 200, 256, 350, 400,
+ *     500, 512, 1000, 1024 (350 is the segmentation DONN's grid of §5.6.2).  The layer size n satisfies 1 <= n <= n_fft with n_fft - n
  *     even; the layer sits centred in the n_fft grid and is cropped back
  *     after every hop.
  */

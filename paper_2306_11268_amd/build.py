@@ -24,7 +24,7 @@ LIB = os.path.join(PKG, "liblr.so")
 # standalone measurement program (practical HBM ceiling of the passes' traffic mixes)
 PROBE = os.path.join(PKG, "membw_probe")
 BUILD_DIR = os.path.join(PKG, "_build")
-FFT_SIZES = (64, 100, 128, 200, 256, 400, 500, 512, 1000, 1024)
+FFT_SIZES = (64, 100, 128, 200, 256, 350, 400, 500, 512, 1000, 1024)
 # (source, object name, extra flags)
 UNITS = [("kernels.hip", "kernels", []), ("api.hip", "api", [])] + [
     ("kern_size.hip", f"kern_n{n}", [f"-DLR_FFT_N={n}"]) for n in FFT_SIZES]

@@ -354,6 +354,7 @@ bool fft_size_supported(int N) {
     case 128:
     case 200:
     case 256:
+    case 350:
     case 400:
     case 500:
     case 512:
@@ -372,6 +373,7 @@ TileShape tile_shape(int N, int) {
     case 128: return shape_n<128>();
     case 200: return shape_n<200>();
     case 256: return shape_n<256>();
+    case 350: return shape_n<350>();
     case 400: return shape_n<400>();
     case 500: return shape_n<500>();
     case 512: return shape_n<512>();
@@ -388,6 +390,7 @@ hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& 
     case 128: return launch_fr_n<128>(kind, axis, a, st);
     case 200: return launch_fr_n<200>(kind, axis, a, st);
     case 256: return launch_fr_n<256>(kind, axis, a, st);
+    case 350: return launch_fr_n<350>(kind, axis, a, st);
     case 400: return launch_fr_n<400>(kind, axis, a, st);
     case 500: return launch_fr_n<500>(kind, axis, a, st);
     case 512: return launch_fr_n<512>(kind, axis, a, st);
@@ -404,6 +407,7 @@ int fresnel_pass_tile(int N, PassKind kind, Axis axis) {
     case 128: return tile_fr_n<128>(kind, axis);
     case 200: return tile_fr_n<200>(kind, axis);
     case 256: return tile_fr_n<256>(kind, axis);
+    case 350: return tile_fr_n<350>(kind, axis);
     case 400: return tile_fr_n<400>(kind, axis);
     case 500: return tile_fr_n<500>(kind, axis);
     case 512: return tile_fr_n<512>(kind, axis);
@@ -420,6 +424,7 @@ int fresnel_pass_slots(int N, PassKind kind, Axis axis) {
     case 128: return slots_fr_n<128>(kind, axis);
     case 200: return slots_fr_n<200>(kind, axis);
     case 256: return slots_fr_n<256>(kind, axis);
+    case 350: return slots_fr_n<350>(kind, axis);
     case 400: return slots_fr_n<400>(kind, axis);
     case 500: return slots_fr_n<500>(kind, axis);
     case 512: return slots_fr_n<512>(kind, axis);
@@ -436,6 +441,7 @@ hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t
     case 128: return launch_as_n<128>(kind, a, st);
     case 200: return launch_as_n<200>(kind, a, st);
     case 256: return launch_as_n<256>(kind, a, st);
+    case 350: return launch_as_n<350>(kind, a, st);
     case 400: return launch_as_n<400>(kind, a, st);
     case 500: return launch_as_n<500>(kind, a, st);
     case 512: return launch_as_n<512>(kind, a, st);
@@ -453,6 +459,7 @@ hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, float scale,
     case 128: return prep_as_n<128>(H, Hp, scale, st);
     case 200: return prep_as_n<200>(H, Hp, scale, st);
     case 256: return prep_as_n<256>(H, Hp, scale, st);
+    case 350: return prep_as_n<350>(H, Hp, scale, st);
     case 400: return prep_as_n<400>(H, Hp, scale, st);
     case 500: return prep_as_n<500>(H, Hp, scale, st);
     case 512: return prep_as_n<512>(H, Hp, scale, st);

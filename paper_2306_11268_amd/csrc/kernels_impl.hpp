@@ -1178,6 +1178,7 @@ template <> struct TileT<100>  { static constexpr int T = 16; };
 template <> struct TileT<128>  { static constexpr int T = 16; };
 template <> struct TileT<200>  { static constexpr int T = 16; };
 template <> struct TileT<256>  { static constexpr int T = 8; };
+template <> struct TileT<350>  { static constexpr int T = 32; };  // 14 slots: T * 14 threads must be whole waves
 template <> struct TileT<400>  { static constexpr int T = 8; };
 template <> struct TileT<500>  { static constexpr int T = 16; };  // 20 slots: T * 20 threads must be whole waves
 template <> struct TileT<512>  { static constexpr int T = 8; };

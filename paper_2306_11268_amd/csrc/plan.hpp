@@ -101,6 +101,7 @@ template <> struct PlanFor<100>  { using type = Plan2<25, 4, true>; };
 template <> struct PlanFor<128>  { using type = Plan2<16, 8, false>; };
 template <> struct PlanFor<200>  { using type = Plan2<25, 8, true>; };
 template <> struct PlanFor<256>  { using type = Plan2<16, 16, false>; };
+template <> struct PlanFor<350>  { using type = Plan2<25, 14, true>; };
 template <> struct PlanFor<400>  { using type = Plan2<25, 16, true>; };
 template <> struct PlanFor<500>  { using type = Plan2<25, 20, false>; };
 template <> struct PlanFor<512>  { using type = Plan2<32, 16, false>; };

@@ -149,9 +149,10 @@ int main() {
   ok &= check_codelet<2>(g); ok &= check_codelet<3>(g); ok &= check_codelet<4>(g);
   ok &= check_codelet<5>(g); ok &= check_codelet<8>(g); ok &= check_codelet<10>(g);
   ok &= check_codelet<16>(g); ok &= check_codelet<20>(g); ok &= check_codelet<25>(g);
-  ok &= check_codelet<32>(g); ok &= check_codelet<40>(g);
+  ok &= check_codelet<32>(g); ok &= check_codelet<40>(g); ok &= check_codelet<7>(g);
+  ok &= check_codelet<14>(g);
   ok &= check_plan<64>(g); ok &= check_plan<100>(g); ok &= check_plan<128>(g);
-  ok &= check_plan<200>(g); ok &= check_plan<256>(g); ok &= check_plan<400>(g);
+  ok &= check_plan<200>(g); ok &= check_plan<256>(g); ok &= check_plan<350>(g); ok &= check_plan<400>(g);
   ok &= check_plan<500>(g); ok &= check_plan<512>(g); ok &= check_plan<1000>(g);
   ok &= check_plan<1024>(g);
   std::printf(ok ? "ALL OK\n" : "FAILURES\n");

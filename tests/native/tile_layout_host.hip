@@ -69,7 +69,7 @@ static bool check_size() {
 int main() {
   bool ok = true;
   ok &= check_size<64>(); ok &= check_size<100>(); ok &= check_size<128>(); ok &= check_size<200>();
-  ok &= check_size<256>(); ok &= check_size<400>(); ok &= check_size<500>(); ok &= check_size<512>();
+  ok &= check_size<256>(); ok &= check_size<350>(); ok &= check_size<400>(); ok &= check_size<500>(); ok &= check_size<512>();
   ok &= check_size<1000>(); ok &= check_size<1024>();
   ok &= check_cfg<lr::PlanFor<200>::type, 24>();
   std::printf(ok ? "ALL OK\n" : "FAILURES\n");

@@ -173,3 +173,28 @@ def test_segmentation_training_step(lrb):
     rgi = od.layer_norm_backward(G, ry, rrstd)
     ref_grad = od.donn_backward(ref, phi, h, 1.0, grad_intensity=rgi)
     assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+def test_segmentation_training_step_at_the_papers_grid(lrb):
+    # the paper's segmentation system: 5 layers on a 350 x 350 grid (§5.6.2),
+    # the optics of the validation setup
+    w = wl.scaled(wl.WORKLOADS[3], n=350)
+    b = 2
+    net = network(lrb, w, det=False)
+    amp = wl.amplitudes(w, b)
+    phi = wl.phases(w)
+    skip = input_skip(amp)
+    G = np.random.default_rng(75).standard_normal((b, w.n, w.n)).astype(np.float32)
+    saved = net.new_saved(b)
+    out = lrb.lr_donn_forward(net, dev(amp), dev(phi), saved=saved, sums=False, intensity=True, skip=dev(skip))
+    y, stats = lrb.lr_layer_norm(out["intensity"], eps=1e-5)
+    gi = lrb.lr_layer_norm_backward(dev(G), y, stats)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_intensity=gi, skip=dev(skip))
+
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
+    ref = od.donn_forward(amp, phi, h, 1.0, None, skip=skip)
+    assert rel(host(out["intensity"]), ref["intensity"]) < TOL_FIELD
+    ry, _, rrstd = od.layer_norm(ref["intensity"], 1e-5)
+    assert rel(host(y), ry) < TOL_FIELD
+    ref_grad = od.donn_backward(ref, phi, h, 1.0, grad_intensity=od.layer_norm_backward(G, ry, rrstd))
+    assert rel(host(grad), ref_grad) < TOL_GRAD

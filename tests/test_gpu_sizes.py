@@ -19,7 +19,7 @@ pytestmark = pytest.mark.gpu
 
 TOL_FIELD = 1e-4
 TOL_GRAD = 1e-3
-SIZES = (64, 100, 128, 200, 256, 400, 500, 512, 1000, 1024)
+SIZES = (64, 100, 128, 200, 256, 350, 400, 500, 512, 1000, 1024)
 
 
 def rel(a, b):
