@@ -629,6 +629,7 @@ hipError_t launch_loss(int kind, const float* sums, const int32_t* labels, int b
 
 hipError_t launch_codesign(const float* logits, const float* noise, const float* levels, int K, long long count,
                            float tau, int hard, const float* grad_phi, float* phi_or_grad, hipStream_t st) {
+  if (K < 1 || K > kCodesignMaxLevels) return hipErrorInvalidValue;
   if (count <= 0) return hipSuccess;
   long long blocks = (count + 3) / 4;  // four pixels (waves) per workgroup
   if (blocks > 65536) blocks = 65536;
