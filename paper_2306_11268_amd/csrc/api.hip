@@ -268,6 +268,7 @@ PassArgs base_args(const lr_donn* net, int batch) {
   a.off = (net->n_fft - net->n) / 2;
   a.batch = batch;
   a.spg = 1;
+  a.tab_sym = net->approx == LR_ANGULAR_SPECTRUM ? 1 : 0;
   return a;
 }
 

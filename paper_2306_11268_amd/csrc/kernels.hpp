@@ -73,6 +73,10 @@ struct PassArgs {
   float2* field_out;
   float2* saved_ud;     // angular-spectrum path only
   float* sums_part;     // [B][ntiles][K]
+  // angular-spectrum column pass: the table is even in ky (H[N - ky] =
+  // H[ky], exact for the analytic angular-spectrum transfer function), so
+  // only its rows ky <= N/2 are read
+  int tab_sym;
   // field added to the detector-plane field before any output or seed is
   // formed (natural [B][n][n]; nullable): an optical skip connection
   const float2* skip;

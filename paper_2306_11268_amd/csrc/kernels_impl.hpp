@@ -1024,7 +1024,9 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
       write_a(t, j, x);
       __syncthreads();
       // B-step with the 2-D table: element k2 of item k1 is ky = freq(k1, k2);
-      // scheduling barriers keep the twiddle and table loads next to their use
+      // scheduling barriers keep the twiddle and table loads next to their use.
+      // An even table is read at min(ky, N - ky): half the rows, so half the
+      // table traffic of a launch (each sample reads the whole table)
       const bool cj = a.conj_tab != 0;
       int s_op = t.s;
       asm volatile("" : "+v"(s_op));
@@ -1039,7 +1041,8 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
         if (vok) {
           static_for<0, C::N2>([&](auto kc) {
             constexpr int k2 = decltype(kc)::value;
-            const float2 h = ld(a.tab, PL::freq(k1, k2) * N + vec);
+            const int ky = PL::freq(k1, k2);
+            const float2 h = ld(a.tab, (a.tab_sym && ky > N / 2 ? N - ky : ky) * N + vec);
             y[k2] = cj ? cmulc(y[k2], h) : cmul(y[k2], h);
           });
         }

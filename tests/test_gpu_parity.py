@@ -266,3 +266,14 @@ def test_tiny_aperture_in_padded_grid(lrb):
     out = host(lrb.lr_propagate(net, dev(u)))
     ref = od.propagate(u.astype(np.complex128), od.transfer_function(532e-9, 36e-6, 0.01, od.FRESNEL, 64))
     assert rel(out, ref) < TOL_FIELD
+
+
+@pytest.mark.parametrize("m,lam,dx,z", [(1024, 1550e-9, 8e-6, 0.05), (200, 532e-9, 4e-6, 0.01),
+                                        (100, 1550e-9, 1e-6, 0.001), (350, 532e-9, 36e-6, 0.3)])
+def test_angular_spectrum_table_is_even(lrb, m, lam, dx, z):
+    # the angular-spectrum column pass reads H at min(ky, m - ky): the table
+    # lr_tf_build writes must be even in ky (and in kx) bit for bit
+    h = host(lrb.lr_tf_build(lam, dx, z, od.ANGULAR_SPECTRUM, m))
+    k = np.arange(1, m)
+    assert np.array_equal(h[k, :], h[m - k, :])
+    assert np.array_equal(h[:, k], h[:, m - k])
