@@ -999,7 +999,8 @@ int lr_layer_norm(const float* d_x, int32_t batch, int64_t count, float eps, flo
   const size_t stat_bytes = static_cast<size_t>(batch) * 2 * sizeof(float);
   if (d_y != d_x && overlaps(d_y, map_bytes, d_x, map_bytes)) return LR_E_ALIAS;
   if (overlaps(d_stats, stat_bytes, d_x, map_bytes) || overlaps(d_stats, stat_bytes, d_y, map_bytes) ||
-      overlaps(d_work, work_bytes, d_x, map_bytes) || overlaps(d_work, work_bytes, d_y, map_bytes))
+      overlaps(d_work, work_bytes, d_x, map_bytes) || overlaps(d_work, work_bytes, d_y, map_bytes) ||
+      overlaps(d_work, work_bytes, d_stats, stat_bytes))
     return LR_E_ALIAS;
   hipStream_t st = static_cast<hipStream_t>(stream);
   float2* part = static_cast<float2*>(d_work);

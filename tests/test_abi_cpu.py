@@ -233,3 +233,13 @@ def test_skip_field_must_not_alias_the_field_output():
     assert need > 0
     assert lib.lr_donn_forward(ctypes.byref(net), 2, dummy, dummy, None, None, None, P(0x3000), dummy, need,
                                None) == 7
+
+
+@needs_lib
+def test_layer_norm_stats_outside_the_workspace():
+    lib = lb.load()
+    P = ctypes.c_void_p
+    count = 4096 * 3
+    ws = lib.lr_layer_norm_workspace_size(2, count)
+    x, y, w = P(0x10000000), P(0x20000000), P(0x40000000)
+    assert lib.lr_layer_norm(x, 2, count, 1e-5, y, P(0x40000000 + 8), w, ws, None) == 7
