@@ -345,7 +345,8 @@ int prep_tables(const lr_donn* net, const Layout& L, void* w, hipStream_t st) {
     });
   }
   return run_timed("prep_as_table", st, [&] {
-    return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), as_table_scale(net), st);
+    return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), as_table_scale(net),
+                                    net->approx == LR_FRAUNHOFER ? 1 : 0, st);
   });
 }
 
@@ -361,7 +362,8 @@ int prep_layers(const lr_donn* net, const float* d_phi, bool regions, const Layo
   const float2* H = reinterpret_cast<const float2*>(net->d_H);
   if (!fresnel) {
     LR_TRY(run_timed("prep_as_table", st, [&] {
-      return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), as_table_scale(net), st);
+      return lr::launch_prep_as_table(net->n_fft, H, at<float2>(w, L.hp), as_table_scale(net),
+                                    net->approx == LR_FRAUNHOFER ? 1 : 0, st);
     }));
   }
   return run_timed("prep_layers", st, [&] {
@@ -620,7 +622,9 @@ int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* 
   a.nvec = net->n;
   a.ntiles = L.ntiles_vec;
   a.out = at<float2>(d_work, L.w0);
+  a.spec_centred = net->approx == LR_FRAUNHOFER ? 1 : 0;
   LR_TRY(as_pass(N, lr::kAsRowFirst, a, st));
+  a.spec_centred = 0;
   if (net->approx == LR_FRAUNHOFER) {
     // far field: the column DFT with the output factors, straight into d_out ([batch][N][N])
     a.in = at<float2>(d_work, L.w0);

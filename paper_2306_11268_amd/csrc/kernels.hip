@@ -11,7 +11,7 @@ template <int N> hipError_t launch_fr_n(PassKind, Axis, const PassArgs&, hipStre
 template <int N> int slots_fr_n(PassKind, Axis);
 template <int N> int tile_fr_n(PassKind, Axis);
 template <int N> hipError_t launch_as_n(AsPassKind, const PassArgs&, hipStream_t);
-template <int N> hipError_t prep_as_n(const float2*, float2*, float, hipStream_t);
+template <int N> hipError_t prep_as_n(const float2*, float2*, float, int, hipStream_t);
 template <int N> TileShape shape_n();
 
 // ---------------------------------------------------------------------------
@@ -452,19 +452,19 @@ hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t
 }
 
 
-hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, float scale, hipStream_t st) {
+hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, float scale, int centred, hipStream_t st) {
   switch (N) {
-    case 64: return prep_as_n<64>(H, Hp, scale, st);
-    case 100: return prep_as_n<100>(H, Hp, scale, st);
-    case 128: return prep_as_n<128>(H, Hp, scale, st);
-    case 200: return prep_as_n<200>(H, Hp, scale, st);
-    case 256: return prep_as_n<256>(H, Hp, scale, st);
-    case 350: return prep_as_n<350>(H, Hp, scale, st);
-    case 400: return prep_as_n<400>(H, Hp, scale, st);
-    case 500: return prep_as_n<500>(H, Hp, scale, st);
-    case 512: return prep_as_n<512>(H, Hp, scale, st);
-    case 1000: return prep_as_n<1000>(H, Hp, scale, st);
-    case 1024: return prep_as_n<1024>(H, Hp, scale, st);
+    case 64: return prep_as_n<64>(H, Hp, scale, centred, st);
+    case 100: return prep_as_n<100>(H, Hp, scale, centred, st);
+    case 128: return prep_as_n<128>(H, Hp, scale, centred, st);
+    case 200: return prep_as_n<200>(H, Hp, scale, centred, st);
+    case 256: return prep_as_n<256>(H, Hp, scale, centred, st);
+    case 350: return prep_as_n<350>(H, Hp, scale, centred, st);
+    case 400: return prep_as_n<400>(H, Hp, scale, centred, st);
+    case 500: return prep_as_n<500>(H, Hp, scale, centred, st);
+    case 512: return prep_as_n<512>(H, Hp, scale, centred, st);
+    case 1000: return prep_as_n<1000>(H, Hp, scale, centred, st);
+    case 1024: return prep_as_n<1024>(H, Hp, scale, centred, st);
     default: return hipErrorInvalidValue;
   }
 }

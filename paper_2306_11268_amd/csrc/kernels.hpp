@@ -73,6 +73,10 @@ struct PassArgs {
   float2* field_out;
   float2* saved_ud;     // angular-spectrum path only
   float* sums_part;     // [B][ntiles][K]
+  // far field: row passes store each x-spectrum in centred natural order
+  // (position p holds frequency (p + N/2) mod N), so that the column pass
+  // reads and writes whole output columns
+  int spec_centred;
   // angular-spectrum column pass: the table is even in ky (H[N - ky] =
   // H[ky], exact for the analytic angular-spectrum transfer function), so
   // only its rows ky <= N/2 are read
@@ -124,7 +128,7 @@ hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t
 
 // Small helper kernels.
 // Hp[ky][c] = scale * H[ky][kx(c)] (columns in the row plan's slot order).
-hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, float scale, hipStream_t st);
+hipError_t launch_prep_as_table(int N, const float2* H, float2* Hp, float scale, int centred, hipStream_t st);
 // sums[b][k] = (accumulate ? sums[b][k] : 0) + the per-tile partial sums, in tile order.
 hipError_t launch_finish_sums(const float* part, int batch, int ntiles, int K, float* sums, int accumulate,
                               hipStream_t st);

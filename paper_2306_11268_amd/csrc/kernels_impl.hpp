@@ -960,15 +960,21 @@ __device__ __forceinline__ void load_spec_rows(float2* lds, const float2* __rest
     if (e < total) lds[(e - v * C::N) * C::TP + v] = buf[i.value];
   });
 }
+// With centred, position p of a stored row holds frequency (p + N/2) mod N
+// instead of slot p (N even).
 template <class C>
-__device__ __forceinline__ void store_spec_rows(const float2* lds, float2* __restrict__ out, int vec0, int nvalid) {
+__device__ __forceinline__ void store_spec_rows(const float2* lds, float2* __restrict__ out, int vec0, int nvalid,
+                                                bool centred) {
+  using PL = typename C::Plan;
   float2 buf[C::N1];
   const int total = nvalid * C::N;
   const int tid = opaque_tid();
   static_for<0, C::N1>([&](auto i) {
     const int e = tid + i.value * C::P;
     const int v = e / C::N;
-    if (e < total) buf[i.value] = lds[(e - v * C::N) * C::TP + v];
+    const int p = e - v * C::N;
+    const int slot = centred ? PL::slot_of_freq(p + C::N / 2 < C::N ? p + C::N / 2 : p - C::N / 2) : p;
+    if (e < total) buf[i.value] = lds[slot * C::TP + v];
   });
   static_for<0, C::N1>([&](auto i) {
     const int e = tid + i.value * C::P;
@@ -1058,9 +1064,11 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
       continue;
     }
     if constexpr (KIND == kAsColFar) {
-      // unnormalised DFT along y of the x-spectrum column vec (row-plan slot
-      // order); frequency (ky, kx) goes to [(ky + N/2) mod N][(kx + N/2) mod N]
-      // times the table (which carries the far-field factors)
+      // unnormalised DFT along y of x-spectrum column vec, stored by the row
+      // pass in centred order (column vec holds kx = (vec + N/2) mod N);
+      // frequency (ky, kx) goes to [(ky + N/2) mod N][vec] times the table
+      // (in the same column order, carrying the far-field factors), so a
+      // tile writes whole runs of consecutive output columns
       const float2* __restrict__ in = static_cast<const float2*>(a.in) + (size_t)b * n * N;
       __syncthreads();
       load_a_direct<C>(in, N, n, off, vec, vok, x);
@@ -1070,9 +1078,7 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
       b_forward_all<C>(t);
       __syncthreads();
       if (vok) {
-        using RPL = typename RowPlanFor<N>::type;
-        const int kx = RPL::freq(vec / RPL::N2, vec % RPL::N2);
-        const int ocol = kx + N / 2 < N ? kx + N / 2 : kx - N / 2;
+        const int ocol = vec;
         float2* __restrict__ out = a.out + (size_t)b * N * N;
 #pragma unroll 4
         for (int ky = t.s; ky < N; ky += C::S) {
@@ -1127,7 +1133,7 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
       __syncthreads();
       b_forward_all<C>(t);
       __syncthreads();
-      store_spec_rows<C>(lds, a.out + (size_t)b * n * N, vec0, nvalid);
+      store_spec_rows<C>(lds, a.out + (size_t)b * n * N, vec0, nvalid, a.spec_centred != 0);
     } else {
       if constexpr (KIND == kAsRowLast) add_skip<C, kRow>(a, b, vec, vok, x);
       write_a(t, j, x);  // positions, cropped on output
@@ -1156,16 +1162,22 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
 // far-field table), c the slot of frequency kx in the row plan (the layout
 // in which row passes store x-spectra).
 template <class PL>
-__global__ void prep_as_table_kernel(const float2* __restrict__ H, float2* __restrict__ Hp, float inv) {
+__global__ void prep_as_table_kernel(const float2* __restrict__ H, float2* __restrict__ Hp, float inv, int centred) {
   constexpr int N = PL::N;
   const size_t total = (size_t)N * N;
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
     const int ky = (int)(i / N);
     const int c = (int)(i - (size_t)ky * N);
-    // slot c holds element k2 of B-item k1
-    const int k1 = c / PL::N2;
-    const int k2 = c - k1 * PL::N2;
-    const int kx = PL::freq(k1, k2);
+    int kx;
+    if (centred) {
+      // column c holds frequency (c + N/2) mod N (the far field's centred order)
+      kx = c + N / 2 < N ? c + N / 2 : c - N / 2;
+    } else {
+      // slot c holds element k2 of B-item k1
+      const int k1 = c / PL::N2;
+      const int k2 = c - k1 * PL::N2;
+      kx = PL::freq(k1, k2);
+    }
     Hp[i] = cscale(H[(size_t)ky * N + kx], inv);
   }
 }
@@ -1341,10 +1353,11 @@ hipError_t launch_as_n(AsPassKind kind, const PassArgs& a, hipStream_t st) {
 }
 
 template <int N>
-hipError_t prep_as_n(const float2* H, float2* Hp, float scale, hipStream_t st) {
+hipError_t prep_as_n(const float2* H, float2* Hp, float scale, int centred, hipStream_t st) {
+  if (centred && (N & 1)) return hipErrorInvalidValue;
   const int blocks = (int)(((size_t)N * N + 255) / 256);
   hipLaunchKernelGGL((prep_as_table_kernel<typename RowPlanFor<N>::type>), dim3(blocks < 4096 ? blocks : 4096), dim3(256),
-                     0, st, H, Hp, scale);
+                     0, st, H, Hp, scale, centred);
   return hipGetLastError();
 }
 

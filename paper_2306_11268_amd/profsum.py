@@ -28,7 +28,8 @@ import sys
 from collections import defaultdict
 
 FR_KINDS = ("prop", "fwd_mid", "fwd_last", "bwd_first", "bwd_mid", "bwd_last")
-AS_KINDS = ("row_first", "col", "row_mid", "row_last", "row_bwd_first", "row_bwd_mid", "row_bwd_last", "row_ifft")
+AS_KINDS = ("row_first", "col", "row_mid", "row_last", "row_bwd_first", "row_bwd_mid", "row_bwd_last", "row_ifft",
+            "col_far")
 AXES = ("row", "col")
 
 
