@@ -119,44 +119,63 @@ __device__ __forceinline__ int wave_min_int(int x) {
 
 // Per-pixel softmax statistics: max of y = (logits + noise) / tau, the first
 // level index reaching the largest logits + noise, and sum_k exp(y_k - max).
+// The scores of a pixel are read once into registers: lane l holds
+// s[i] = logits + noise of level l + 64 i, i < NI = ceil(K / 64) (-inf past K).
 struct CodesignStats {
   float ymax;
   int kbest;
   float esum;
 };
-__device__ __forceinline__ CodesignStats codesign_stats(const float* __restrict__ lg, const float* __restrict__ nz, int K,
-                                                        float inv_tau, int lane) {
+template <int NI>
+__device__ __forceinline__ void codesign_load(const float* __restrict__ lg, const float* __restrict__ nz, int K,
+                                              int lane, float (&sc)[NI]) {
+#pragma unroll
+  for (int i = 0; i < NI; ++i) {
+    const int k = lane + 64 * i;
+    sc[i] = k < K ? lg[k] + nz[k] : -INFINITY;
+  }
+}
+template <int NI>
+__device__ __forceinline__ CodesignStats codesign_stats(const float (&sc)[NI], int K, float inv_tau, int lane) {
   float smax = -INFINITY;
-  for (int k = lane; k < K; k += 64) smax = fmaxf(smax, lg[k] + nz[k]);
+#pragma unroll
+  for (int i = 0; i < NI; ++i) smax = fmaxf(smax, sc[i]);
   smax = wave_max(smax);
   int kb = K;
-  for (int k = lane; k < K; k += 64)
-    if (lg[k] + nz[k] == smax) {
-      kb = k;
-      break;
-    }
+#pragma unroll
+  for (int i = NI - 1; i >= 0; --i) {
+    const int k = lane + 64 * i;
+    if (k < K && sc[i] == smax) kb = k;  // the lowest level of this lane reaching the maximum
+  }
   kb = wave_min_int(kb);
   const float ymax = smax * inv_tau;
   float es = 0.f;
-  for (int k = lane; k < K; k += 64) es += expf((lg[k] + nz[k]) * inv_tau - ymax);
+#pragma unroll
+  for (int i = 0; i < NI; ++i)
+    if (lane + 64 * i < K) es += expf(sc[i] * inv_tau - ymax);
   return CodesignStats{ymax, kb, wave_sum(es)};
 }
 
+template <int NI>
 __global__ void __launch_bounds__(256) codesign_kernel(const float* __restrict__ logits, const float* __restrict__ noise,
                                                        const float* __restrict__ levels, int K, long long count,
                                                        float inv_tau, int hard, float* __restrict__ phi) {
   const int lane = threadIdx.x & 63;
   const long long waves = (long long)gridDim.x * (blockDim.x >> 6);
   for (long long p = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); p < count; p += waves) {
-    const float* lg = logits + p * K;
-    const float* nz = noise + p * K;
-    const CodesignStats cs = codesign_stats(lg, nz, K, inv_tau, lane);
+    float sc[NI];
+    codesign_load<NI>(logits + p * K, noise + p * K, K, lane, sc);
+    const CodesignStats cs = codesign_stats<NI>(sc, K, inv_tau, lane);
     float out;
     if (hard) {
       out = levels[cs.kbest < K ? cs.kbest : 0];  // (no index reaches the maximum only for NaN scores)
     } else {
       float acc = 0.f;
-      for (int k = lane; k < K; k += 64) acc += expf((lg[k] + nz[k]) * inv_tau - cs.ymax) * levels[k];
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int k = lane + 64 * i;
+        if (k < K) acc += expf(sc[i] * inv_tau - cs.ymax) * levels[k];
+      }
       out = wave_sum(acc) / cs.esum;
     }
     if (lane == 0) phi[p] = out;
@@ -165,6 +184,7 @@ __global__ void __launch_bounds__(256) codesign_kernel(const float* __restrict__
 
 // dL/dlogit_j = w_j (levels_j - sum_k w_k levels_k) dL/dphi / tau (the soft
 // Jacobian, also the straight-through gradient of the hard layer).
+template <int NI>
 __global__ void __launch_bounds__(256) codesign_bwd_kernel(const float* __restrict__ logits,
                                                            const float* __restrict__ noise,
                                                            const float* __restrict__ levels, int K, long long count,
@@ -173,19 +193,42 @@ __global__ void __launch_bounds__(256) codesign_bwd_kernel(const float* __restri
   const int lane = threadIdx.x & 63;
   const long long waves = (long long)gridDim.x * (blockDim.x >> 6);
   for (long long p = (long long)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6); p < count; p += waves) {
-    const float* lg = logits + p * K;
-    const float* nz = noise + p * K;
-    const CodesignStats cs = codesign_stats(lg, nz, K, inv_tau, lane);
+    float sc[NI];
+    codesign_load<NI>(logits + p * K, noise + p * K, K, lane, sc);
+    const CodesignStats cs = codesign_stats<NI>(sc, K, inv_tau, lane);
     const float inv_s = 1.f / cs.esum;
     float acc = 0.f;
-    for (int k = lane; k < K; k += 64) acc += expf((lg[k] + nz[k]) * inv_tau - cs.ymax) * levels[k];
+    float lv[NI];
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int k = lane + 64 * i;
+      lv[i] = k < K ? levels[k] : 0.f;
+      if (k < K) acc += expf(sc[i] * inv_tau - cs.ymax) * lv[i];
+    }
     const float mean = wave_sum(acc) * inv_s;
     const float gs = grad_phi[p] * inv_tau;
     float* gl = grad_logits + p * K;
-    for (int k = lane; k < K; k += 64) {
-      const float w = expf((lg[k] + nz[k]) * inv_tau - cs.ymax) * inv_s;
-      gl[k] = w * (levels[k] - mean) * gs;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int k = lane + 64 * i;
+      if (k < K) {
+        const float w = expf(sc[i] * inv_tau - cs.ymax) * inv_s;
+        gl[k] = w * (lv[i] - mean) * gs;
+      }
     }
+  }
+}
+
+template <int NI>
+static void launch_codesign_ni(const float* logits, const float* noise, const float* levels, int K, long long count,
+                               float tau, int hard, const float* grad_phi, float* phi_or_grad, unsigned blocks,
+                               hipStream_t st) {
+  if (grad_phi) {
+    hipLaunchKernelGGL(codesign_bwd_kernel<NI>, dim3(blocks), dim3(256), 0, st, logits, noise, levels, K, count,
+                       1.f / tau, grad_phi, phi_or_grad);
+  } else {
+    hipLaunchKernelGGL(codesign_kernel<NI>, dim3(blocks), dim3(256), 0, st, logits, noise, levels, K, count, 1.f / tau,
+                       hard, phi_or_grad);
   }
 }
 
@@ -633,12 +676,18 @@ hipError_t launch_codesign(const float* logits, const float* noise, const float*
   if (count <= 0) return hipSuccess;
   long long blocks = (count + 3) / 4;  // four pixels (waves) per workgroup
   if (blocks > 65536) blocks = 65536;
-  if (grad_phi) {
-    hipLaunchKernelGGL(codesign_bwd_kernel, dim3((unsigned)blocks), dim3(256), 0, st, logits, noise, levels, K, count,
-                       1.f / tau, grad_phi, phi_or_grad);
-  } else {
-    hipLaunchKernelGGL(codesign_kernel, dim3((unsigned)blocks), dim3(256), 0, st, logits, noise, levels, K, count,
-                       1.f / tau, hard, phi_or_grad);
+  const unsigned nb = (unsigned)blocks;
+  // registers per lane for the scores: ceil(K / 64) (K <= 1024)
+  switch ((K + 63) / 64) {
+    case 1: launch_codesign_ni<1>(logits, noise, levels, K, count, tau, hard, grad_phi, phi_or_grad, nb, st); break;
+    case 2: launch_codesign_ni<2>(logits, noise, levels, K, count, tau, hard, grad_phi, phi_or_grad, nb, st); break;
+    case 3:
+    case 4: launch_codesign_ni<4>(logits, noise, levels, K, count, tau, hard, grad_phi, phi_or_grad, nb, st); break;
+    case 5:
+    case 6:
+    case 7:
+    case 8: launch_codesign_ni<8>(logits, noise, levels, K, count, tau, hard, grad_phi, phi_or_grad, nb, st); break;
+    default: launch_codesign_ni<16>(logits, noise, levels, K, count, tau, hard, grad_phi, phi_or_grad, nb, st); break;
   }
   return hipGetLastError();
 }
