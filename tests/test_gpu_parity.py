@@ -277,3 +277,38 @@ def test_angular_spectrum_table_is_even(lrb, m, lam, dx, z):
     k = np.arange(1, m)
     assert np.array_equal(h[k, :], h[m - k, :])
     assert np.array_equal(h[:, k], h[:, m - k])
+
+
+@pytest.mark.parametrize("approx", [od.FRESNEL, od.ANGULAR_SPECTRUM])
+def test_maximum_layer_count(lrb, approx):
+    # LR_MAX_LAYERS = 64 layers (65 hops), 64 x 64 centred in 128, forward and
+    # full-map backward against the oracle
+    n, m, L, b = 64, 128, 64, 2
+    lam, dx, z = 532e-9, 36e-6, 0.02
+    g = np.random.default_rng(91)
+    amp = g.uniform(0, 1, (b, n, n)).astype(np.float32)
+    phi = g.uniform(0, 2 * np.pi, (L, n, n)).astype(np.float32)
+    gi = g.standard_normal((b, n, n)).astype(np.float32)
+    net = lrb.Network(lam, dx, z, approx, n, m, L)
+    saved = net.new_saved(b)
+    out = lrb.lr_donn_forward(net, dev(amp), dev(phi), saved=saved, sums=False, intensity=True)
+    grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_intensity=dev(gi))
+    h = od.transfer_function(lam, dx, z, approx, m)
+    ref = od.donn_forward(amp, phi, h, 1.0, None)
+    assert rel(host(out["intensity"]), ref["intensity"]) < TOL_FIELD
+    assert rel(host(grad), od.donn_backward(ref, phi, h, 1.0, grad_intensity=gi)) < TOL_GRAD
+
+
+def test_large_batch_sampled(lrb):
+    # 4096 samples of workload 2's optics at 64 x 64 (in a 64 grid): region
+    # sums of the first and last samples against the oracle one by one
+    w = wl.scaled(wl.WORKLOADS[2], n=64)
+    b = 4096
+    net = make_net(lrb, w)
+    amp = wl.amplitudes(w, b)
+    phi = wl.phases(w)
+    out = host(lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True)["sums"])
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, w.n_fft)
+    for s in (0, b - 1):
+        ref = od.donn_forward(amp[s:s + 1], phi, h, 1.0, oracle_det(w.detector))
+        assert rel(out[s:s + 1], ref["sums"]) < TOL_FIELD
