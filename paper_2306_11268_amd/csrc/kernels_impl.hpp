@@ -622,12 +622,13 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
       });
     }
   }
-  // At N >= 1000 an A-item is 25-32 values: the prefetch buffer and a
-  // modulation loaded during the B-step no longer fit next to the
-  // propagating item in 256 registers (they spilled), so these sizes load
-  // each input when it is needed and rely on the other resident waves (the
-  // forward layer pass likewise loads its modulation after the B-step).
-  constexpr bool BIG = C::N >= 1000;
+  // From N = 500 on (B-items of 16-40 values next to A-items of 25-32) the
+  // prefetch buffer and a modulation loaded during the B-step no longer fit
+  // next to the propagating item in 256 registers (they spilled 12-122
+  // registers), so these sizes load each input when it is needed and rely
+  // on the other resident waves (the forward layer pass likewise loads its
+  // modulation after the B-step).
+  constexpr bool BIG = C::N >= 500;
   constexpr bool PREFETCH = ACC && (DIRECT || KIND == kBwdMid) && !BIG;
   constexpr bool G_FIRST = DIRECT && KIND == kBwdLast;
   float2 pf[PREFETCH && DIRECT ? N1 : 1];
@@ -712,7 +713,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
         read_a(t, j, x);
       }
       // G_l = adjoint of the first-axis half of hop l+1; the modulation is
-      // loaded during its B-step (after it at N >= 1000)
+      // loaded during its B-step (after it from N = 500 on)
       float2 m[N1];
       if constexpr (BIG) {
         prop(x, true, nothing);
