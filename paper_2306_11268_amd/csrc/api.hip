@@ -234,7 +234,7 @@ std::string as_name(int N, int kind) {
 // hardware dispatcher then balances them, which measured faster than a
 // persistent schedule with prefetching for them.
 int schedule_layer_pass(int N, lr::PassKind kind, Axis ax, int max_lanes, PassArgs& a) {
-  const int slots = lr::fresnel_pass_slots(N, kind, ax);
+  const int slots = lr::fresnel_pass_slots(N, kind, ax, a.full != 0);
   const int tile_t = lr::fresnel_pass_tile(N, kind, ax);
   if (slots <= 0 || tile_t <= 0) return LR_E_HIP;
   a.ntiles = ceil_div(a.nvec, tile_t);
@@ -332,6 +332,14 @@ float as_table_scale(const lr_donn* net) {
   return net->approx == LR_FRAUNHOFER ? 1.0f : static_cast<float>(1.0 / (N * N));
 }
 
+// The separable passes of a network whose layer fills the FFT grid keep
+// their fields, modulation tables and dphi partials in the plan's slot order
+// (no index arithmetic in the passes); padded layers use natural order.
+bool slot_ordered(const lr_donn* net) { return net->approx == LR_FRESNEL && net->n == net->n_fft; }
+lr::SlotMap slot_map_of(const lr_donn* net) {
+  return slot_ordered(net) ? lr::slot_map(net->n_fft) : lr::SlotMap{0, 0, 0};
+}
+
 // Transfer-function tables of the passes: the separable Fresnel chirps (in
 // natural frequency order; each pass stages them in its own plan order) or the
 // column-permuted copy of H the angular-spectrum passes read.
@@ -339,8 +347,8 @@ int prep_tables(const lr_donn* net, const Layout& L, void* w, hipStream_t st) {
   const float2* H = reinterpret_cast<const float2*>(net->d_H);
   if (net->approx == LR_FRESNEL) {
     return run_timed("prep_layers", st, [&] {
-      return lr::launch_prep_layers(nullptr, 0, net->n, 1.0f, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
-                                    nullptr, nullptr, H, net->n_fft, at<float2>(w, L.chirp_x),
+      return lr::launch_prep_layers(nullptr, 0, net->n, 1.0f, nullptr, lr::SlotMap{0, 0, 0}, nullptr, nullptr,
+                                    nullptr, nullptr, nullptr, nullptr, nullptr, H, net->n_fft, at<float2>(w, L.chirp_x),
                                     at<float2>(w, L.chirp_y), st);
     });
   }
@@ -367,7 +375,8 @@ int prep_layers(const lr_donn* net, const float* d_phi, bool regions, const Layo
     }));
   }
   return run_timed("prep_layers", st, [&] {
-    return lr::launch_prep_layers(d_phi, net->num_layers, net->n, net->gamma, orient, at<float2>(w, L.mod),
+    return lr::launch_prep_layers(d_phi, net->num_layers, net->n, net->gamma, orient, slot_map_of(net),
+                                  at<float2>(w, L.mod),
                                   with_regions ? &r : nullptr, at<int2>(w, L.regions),
                                   at<unsigned long long>(w, L.row_mask), at<unsigned long long>(w, L.col_mask),
                                   at<int>(w, L.row_perm), at<int>(w, L.col_perm), fresnel ? H : nullptr,
@@ -688,6 +697,7 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
 
   PassArgs a = base_args(net, batch);
   a.accumulate = accumulate ? 1 : 0;
+  a.full = slot_ordered(net) ? 1 : 0;
   const int tile_t = lr::tile_shape(N, 0).T;
   int sum_tiles = L.ntiles_vec;  // tiles that wrote partial detector sums
   if (net->approx == LR_FRESNEL) {
@@ -807,7 +817,10 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
     // an empty batch has a zero gradient: a fixed-order sum over no groups
     int none[LR_MAX_LAYERS] = {};
     return run_timed("reduce_dphi", st,
-                     [&] { return lr::launch_reduce_dphi(nullptr, 0, none, none, Lyr, n, d_grad_phi, st); });
+                     [&] {
+                       return lr::launch_reduce_dphi(nullptr, 0, none, none, Lyr, n, lr::SlotMap{0, 0, 0}, d_grad_phi,
+                                                     st);
+                     });
   }
   const float2* saved = static_cast<const float2*>(d_saved);
   float2* ws_mod = at<float2>(d_work, L.mod);
@@ -826,6 +839,7 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
   PassArgs a = base_args(net, batch);
   a.conj_tab = 1;
   a.conj_mod = 1;
+  a.full = slot_ordered(net) ? 1 : 0;
   a.nvec = n;
   a.ntiles = L.ntiles_vec;
   // layer l accumulates into its own partials; one launch reduces all layers at the end
@@ -836,7 +850,8 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
   for (int l = 1; l <= Lyr; ++l) orient_of[l - 1] = layer_transposed(net, l);
   auto reduce_all = [&]() {
     return run_timed("reduce_dphi", st, [&] {
-      return lr::launch_reduce_dphi(part, layer_stride, groups_of, orient_of, Lyr, n, d_grad_phi, st);
+      return lr::launch_reduce_dphi(part, layer_stride, groups_of, orient_of, Lyr, n, slot_map_of(net), d_grad_phi,
+                                    st);
     });
   };
 

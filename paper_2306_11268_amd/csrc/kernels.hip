@@ -8,11 +8,12 @@ namespace lr {
 
 // Per-size entry points, defined in kern_size.hip (one object per size).
 template <int N> hipError_t launch_fr_n(PassKind, Axis, const PassArgs&, hipStream_t);
-template <int N> int slots_fr_n(PassKind, Axis);
+template <int N> int slots_fr_n(PassKind, Axis, bool);
 template <int N> int tile_fr_n(PassKind, Axis);
 template <int N> hipError_t launch_as_n(AsPassKind, const PassArgs&, hipStream_t);
 template <int N> hipError_t prep_as_n(const float2*, float2*, float, int, hipStream_t);
 template <int N> TileShape shape_n();
+template <int N> SlotMap slot_map_n();
 
 // ---------------------------------------------------------------------------
 // Helper kernels
@@ -20,20 +21,24 @@ template <int N> TileShape shape_n();
 
 struct OrientArg { int o[64]; };
 
-// mod[l][q][vec] = gamma * exp(j*phi_l[y][x]); (y, x) = (q, vec) or (vec, q) when transposed.
+// mod[l][sq][sv] = gamma * exp(j*phi_l[y][x]) with (q, vec) = (sm.pos(sq),
+// sm.pos(sv)) and (y, x) = (q, vec), or (vec, q) when transposed.
 __device__ __forceinline__ void prep_mod_body(const float* __restrict__ phi, int layers, int n, float gamma,
-                                              const OrientArg& orient, float2* __restrict__ mod) {
+                                              const OrientArg& orient, SlotMap sm, float2* __restrict__ mod) {
   const size_t nn = (size_t)n * n;
   const size_t total = nn * layers;
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < total; i += (size_t)gridDim.x * blockDim.x) {
     const int l = (int)(i / nn);
     const size_t r = i - (size_t)l * nn;
-    const int y = (int)(r / n);
-    const int x = (int)(r - (size_t)y * n);
+    const int sq = (int)(r / n);
+    const int q = sm.pos(sq);
+    const int vec = sm.pos((int)(r - (size_t)sq * n));
+    const bool tr = orient.o[l < 64 ? l : 63] != 0;
+    const int y = tr ? vec : q;
+    const int x = tr ? q : vec;
     float s, c;
-    sincosf(phi[i], &s, &c);
-    const size_t o = orient.o[l < 64 ? l : 63] ? (size_t)x * n + y : r;
-    mod[(size_t)l * nn + o] = c2(gamma * c, gamma * s);
+    sincosf(phi[(size_t)l * nn + (size_t)y * n + x], &s, &c);
+    mod[i] = c2(gamma * c, gamma * s);
   }
 }
 
@@ -246,8 +251,9 @@ __global__ void adam_kernel(float* __restrict__ phi, const float* __restrict__ g
   }
 }
 
-// dphi_l[y][x] = sum over groups of part_l[g][q][vec], oriented (transposed:
-// q = x), for every layer l = blockIdx.y in one launch; part_l starts at
+// dphi_l[y][x] = sum over groups of part_l[g][sq][sv], oriented (transposed:
+// q = x) and in the slot order sm ((q, vec) = (sm.pos(sq), sm.pos(sv))), for
+// every layer l = blockIdx.y in one launch; part_l starts at
 // part + l * layer_stride.  A workgroup covers 64 consecutive elements with 4
 // slices of 64 threads; slice s sums groups s, s+4, s+8, ... in order and the
 // four partial sums are added in slice order, so the result does not depend
@@ -257,7 +263,7 @@ struct ReduceArg {
   int transposed[64];
 };
 __global__ void __launch_bounds__(256) reduce_dphi_kernel(const float* __restrict__ part, size_t layer_stride,
-                                                          ReduceArg arg, int n, float* __restrict__ out) {
+                                                          ReduceArg arg, int n, SlotMap sm, float* __restrict__ out) {
   __shared__ float red[4][64];
   const int l = blockIdx.y;
   const int groups = arg.groups[l];
@@ -285,28 +291,36 @@ __global__ void __launch_bounds__(256) reduce_dphi_kernel(const float* __restric
   __syncthreads();
   if (slice == 0 && i < nn) {
     const float r = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
-    const int q = (int)(i / n);
-    const int v = (int)(i - (size_t)q * n);
-    out[(size_t)l * nn + (arg.transposed[l] ? (size_t)v * n + q : i)] = r;
+    const int sq = (int)(i / n);
+    const int q = sm.pos(sq);
+    const int v = sm.pos((int)(i - (size_t)sq * n));
+    out[(size_t)l * nn + (arg.transposed[l] ? (size_t)v * n + q : (size_t)q * n + v)] = r;
   }
 }
 
-// Region corners, per-row / per-column coverage masks and the covered-first
-// permutations of rows and columns: covered indices in ascending order, then
-// the uncovered ones.  Run by one workgroup of 1024 threads, thread i handles
-// row i and column i (n <= 1024).
-__device__ void set_regions_body(const Regions& reg, int n, int2* dst, unsigned long long* row_mask,
+// Region corners, per-row / per-column coverage masks (natural indices) and
+// the covered-first permutations of the stored rows and columns (slot order
+// sm): stored indices whose natural row / column a region covers, in
+// ascending order, then the others.  Run by one workgroup of 1024 threads,
+// thread i handles row i and column i (n <= 1024).
+__device__ void set_regions_body(const Regions& reg, int n, SlotMap sm, int2* dst, unsigned long long* row_mask,
                                  unsigned long long* col_mask, int* row_perm, int* col_perm, int (*wave_count)[16]) {
   const int i = threadIdx.x;
   if (i < reg.K) dst[i] = make_int2(reg.y0[i], reg.x0[i]);
+  auto masks = [&](int p, unsigned long long& rm, unsigned long long& cm) {
+    rm = 0;
+    cm = 0;
+    for (int k = 0; k < reg.K; ++k) {
+      if ((unsigned)(p - reg.y0[k]) < (unsigned)reg.s) rm |= 1ull << k;
+      if ((unsigned)(p - reg.x0[k]) < (unsigned)reg.s) cm |= 1ull << k;
+    }
+  };
   unsigned long long rm = 0, cm = 0;
   if (i < n) {
-    for (int k = 0; k < reg.K; ++k) {
-      if ((unsigned)(i - reg.y0[k]) < (unsigned)reg.s) rm |= 1ull << k;
-      if ((unsigned)(i - reg.x0[k]) < (unsigned)reg.s) cm |= 1ull << k;
-    }
+    masks(i, rm, cm);
     row_mask[i] = rm;
     col_mask[i] = cm;
+    masks(sm.pos(i), rm, cm);  // coverage of stored index i
   }
   const bool rc = i < n && rm != 0;
   const bool cc = i < n && cm != 0;
@@ -354,15 +368,16 @@ __device__ __forceinline__ void prep_chirps_body(const float2* __restrict__ H, i
 // detector regions, the region tables (workgroup 0).  Workgroups of 1024
 // threads.
 __global__ void __launch_bounds__(1024) prep_layers_kernel(const float* __restrict__ phi, int layers, int n, float gamma,
-                                                           OrientArg orient, float2* __restrict__ mod, Regions reg,
+                                                           OrientArg orient, SlotMap sm, float2* __restrict__ mod,
+                                                           Regions reg,
                                                            int2* dst, unsigned long long* row_mask,
                                                            unsigned long long* col_mask, int* row_perm, int* col_perm,
                                                            const float2* __restrict__ H, int nfft,
                                                            float2* __restrict__ cx, float2* __restrict__ cy) {
   __shared__ int wave_count[2][16];
-  if (blockIdx.x == 0 && dst) set_regions_body(reg, n, dst, row_mask, col_mask, row_perm, col_perm, wave_count);
+  if (blockIdx.x == 0 && dst) set_regions_body(reg, n, sm, dst, row_mask, col_mask, row_perm, col_perm, wave_count);
   if (H) prep_chirps_body(H, nfft, cx, cy);
-  if (phi) prep_mod_body(phi, layers, n, gamma, orient, mod);
+  if (phi) prep_mod_body(phi, layers, n, gamma, orient, sm, mod);
 }
 
 // Detector readout from a field: one workgroup per (sample, region).
@@ -426,6 +441,23 @@ TileShape tile_shape(int N, int) {
   }
 }
 
+SlotMap slot_map(int N) {
+  switch (N) {
+    case 64: return slot_map_n<64>();
+    case 100: return slot_map_n<100>();
+    case 128: return slot_map_n<128>();
+    case 200: return slot_map_n<200>();
+    case 256: return slot_map_n<256>();
+    case 350: return slot_map_n<350>();
+    case 400: return slot_map_n<400>();
+    case 500: return slot_map_n<500>();
+    case 512: return slot_map_n<512>();
+    case 1000: return slot_map_n<1000>();
+    case 1024: return slot_map_n<1024>();
+    default: return SlotMap{0, 0, 0};
+  }
+}
+
 hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& a, hipStream_t st) {
   switch (N) {
     case 64: return launch_fr_n<64>(kind, axis, a, st);
@@ -460,19 +492,19 @@ int fresnel_pass_tile(int N, PassKind kind, Axis axis) {
   }
 }
 
-int fresnel_pass_slots(int N, PassKind kind, Axis axis) {
+int fresnel_pass_slots(int N, PassKind kind, Axis axis, bool full) {
   switch (N) {
-    case 64: return slots_fr_n<64>(kind, axis);
-    case 100: return slots_fr_n<100>(kind, axis);
-    case 128: return slots_fr_n<128>(kind, axis);
-    case 200: return slots_fr_n<200>(kind, axis);
-    case 256: return slots_fr_n<256>(kind, axis);
-    case 350: return slots_fr_n<350>(kind, axis);
-    case 400: return slots_fr_n<400>(kind, axis);
-    case 500: return slots_fr_n<500>(kind, axis);
-    case 512: return slots_fr_n<512>(kind, axis);
-    case 1000: return slots_fr_n<1000>(kind, axis);
-    case 1024: return slots_fr_n<1024>(kind, axis);
+    case 64: return slots_fr_n<64>(kind, axis, full);
+    case 100: return slots_fr_n<100>(kind, axis, full);
+    case 128: return slots_fr_n<128>(kind, axis, full);
+    case 200: return slots_fr_n<200>(kind, axis, full);
+    case 256: return slots_fr_n<256>(kind, axis, full);
+    case 350: return slots_fr_n<350>(kind, axis, full);
+    case 400: return slots_fr_n<400>(kind, axis, full);
+    case 500: return slots_fr_n<500>(kind, axis, full);
+    case 512: return slots_fr_n<512>(kind, axis, full);
+    case 1000: return slots_fr_n<1000>(kind, axis, full);
+    case 1024: return slots_fr_n<1024>(kind, axis, full);
     default: return 0;
   }
 }
@@ -635,12 +667,13 @@ hipError_t launch_layer_norm_backward(const float* g, const float* y, const floa
   return hipGetLastError();
 }
 
-hipError_t launch_prep_layers(const float* phi, int layers, int n, float gamma, const int* orient_host, float2* mod,
-                              const Regions* regions, int2* dst, unsigned long long* row_mask,
+hipError_t launch_prep_layers(const float* phi, int layers, int n, float gamma, const int* orient_host, SlotMap sm,
+                              float2* mod, const Regions* regions, int2* dst, unsigned long long* row_mask,
                               unsigned long long* col_mask, int* row_perm, int* col_perm, const float2* H, int nfft,
                               float2* chirp_x, float2* chirp_y, hipStream_t st) {
   if (n < 1 || n > 1024 || layers < 0 || layers > 64 || (H && (nfft < n || !chirp_x || !chirp_y)))
     return hipErrorInvalidValue;
+  if (sm.N1 != 0 && sm.N1 * sm.N2 != n) return hipErrorInvalidValue;
   if (regions && (regions->K < 1 || regions->K > kMaxRegions)) return hipErrorInvalidValue;
   OrientArg o{};
   for (int l = 0; l < layers; ++l) o.o[l] = orient_host[l];
@@ -651,7 +684,7 @@ hipError_t launch_prep_layers(const float* phi, int layers, int n, float gamma, 
   if (blocks > 2048) blocks = 2048;
   if (blocks < 1) blocks = 1;
   hipLaunchKernelGGL(prep_layers_kernel, dim3(blocks), dim3(1024), 0, st, layers > 0 ? phi : nullptr, layers, n,
-                     gamma, o, mod, r, regions ? dst : nullptr, row_mask, col_mask, row_perm, col_perm, H, nfft,
+                     gamma, o, sm, mod, r, regions ? dst : nullptr, row_mask, col_mask, row_perm, col_perm, H, nfft,
                      chirp_x, chirp_y);
   return hipGetLastError();
 }
@@ -703,8 +736,9 @@ hipError_t launch_adam(float* phi, const float* g, float* m, float* v, long long
 }
 
 hipError_t launch_reduce_dphi(const float* part, size_t layer_stride, const int* groups, const int* transposed,
-                              int layers, int n, float* out, hipStream_t st) {
+                              int layers, int n, SlotMap sm, float* out, hipStream_t st) {
   if (layers < 1 || layers > 64) return hipErrorInvalidValue;
+  if (sm.N1 != 0 && sm.N1 * sm.N2 != n) return hipErrorInvalidValue;
   ReduceArg arg{};
   for (int l = 0; l < layers; ++l) {
     arg.groups[l] = groups[l];
@@ -712,7 +746,7 @@ hipError_t launch_reduce_dphi(const float* part, size_t layer_stride, const int*
   }
   const size_t nn = (size_t)n * n;
   const int blocks = (int)((nn + 63) / 64);
-  hipLaunchKernelGGL(reduce_dphi_kernel, dim3(blocks, layers), dim3(256), 0, st, part, layer_stride, arg, n, out);
+  hipLaunchKernelGGL(reduce_dphi_kernel, dim3(blocks, layers), dim3(256), 0, st, part, layer_stride, arg, n, sm, out);
   return hipGetLastError();
 }
 

@@ -36,6 +36,7 @@ enum AsPassKind : int {
 };
 
 struct PassArgs {
+  int full;       // n == N: fields and per-layer tables in slot order (see SlotMap)
   int n;          // layer (aperture) size
   int off;        // (N - n) / 2
   int batch;
@@ -107,6 +108,25 @@ struct PassArgs {
 
 struct TileShape { int T; int S; };
 
+// Slot order of an FFT plan N = N1 * N2 (plan.hpp): stored index s along an
+// axis holds natural position pos(s) = (N2 * (s / N2) + N1 * (s % N2)) mod N
+// for a Good-Thomas plan (pfa != 0) and s otherwise.  The separable passes
+// store the fields they hand to each other, the modulation tables and the
+// dphi partials in this order along both axes when the layer fills the grid.
+// N1 = 0 is the identity (natural order).
+struct SlotMap {
+  int N1;
+  int N2;
+  int pfa;
+  __host__ __device__ int pos(int s) const {
+    if (N1 == 0 || !pfa) return s;
+    const int x = s / N2;
+    const int j = s - x * N2;
+    return (N2 * x + N1 * j) % (N1 * N2);
+  }
+};
+SlotMap slot_map(int N);
+
 // Detector regions passed by value: K squares of side s with corners (y0, x0).
 struct Regions {
   int K;
@@ -122,7 +142,7 @@ TileShape tile_shape(int N, int axis);
 hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& a, hipStream_t st);
 // Workgroups of a separable pass kernel that fit on the current device at
 // once, and the vectors each of its workgroups transforms.
-int fresnel_pass_slots(int N, PassKind kind, Axis axis);
+int fresnel_pass_slots(int N, PassKind kind, Axis axis, bool full);
 int fresnel_pass_tile(int N, PassKind kind, Axis axis);
 hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t st);
 
@@ -146,19 +166,21 @@ hipError_t launch_codesign(const float* logits, const float* noise, const float*
 hipError_t launch_adam(float* phi, const float* g, float* m, float* v, long long count, float lr, float b1, float b2,
                        float eps, float bc1, float bc2, hipStream_t st);
 // dphi of `layers` layers in one launch: layer l sums groups[l] partials
-// (oriented [q][vec], transposed[l] != 0: q = x) starting at
-// part + l * layer_stride floats into out + l * n * n.
+// (oriented [q][vec], transposed[l] != 0: q = x, both indices in the slot
+// order sm) starting at part + l * layer_stride floats into out + l * n * n
+// (natural order).
 hipError_t launch_reduce_dphi(const float* part, size_t layer_stride, const int* groups, const int* transposed,
-                              int layers, int n, float* out, hipStream_t st);
+                              int layers, int n, SlotMap sm, float* out, hipStream_t st);
 // Per-call tables in one launch: mod[l] = gamma * exp(j*phi_l) oriented per
-// layer (orient_host[l] != 0: transposed; none when layers = 0); when regions
-// is not NULL, the region corners (int2 [K]), per-row / per-column coverage
-// masks (uint64 [n]) and covered-first permutations of rows and columns
-// (int [n]); when H is not NULL, the separable Fresnel chirps of the nfft grid
+// layer (orient_host[l] != 0: transposed; none when layers = 0) in the slot
+// order sm along both axes; when regions is not NULL, the region corners
+// (int2 [K]), per-row / per-column coverage masks (uint64 [n], natural
+// indices) and covered-first permutations of the stored rows and columns
+// (int [n], slot order sm); when H is not NULL, the separable Fresnel chirps of the nfft grid
 // in natural frequency order (chirp_x[f] = H[0][f] / nfft, chirp_y[f] =
 // H[f][0] * conj(H[0][0]) / nfft).  n <= 1024.
-hipError_t launch_prep_layers(const float* phi, int layers, int n, float gamma, const int* orient_host, float2* mod,
-                              const Regions* regions, int2* dst, unsigned long long* row_mask,
+hipError_t launch_prep_layers(const float* phi, int layers, int n, float gamma, const int* orient_host, SlotMap sm,
+                              float2* mod, const Regions* regions, int2* dst, unsigned long long* row_mask,
                               unsigned long long* col_mask, int* row_perm, int* col_perm, const float2* H, int nfft,
                               float2* chirp_x, float2* chirp_y, hipStream_t st);
 hipError_t launch_readout(const float2* field, int batch, int n, const Regions& r, float* sums, hipStream_t st);

@@ -78,6 +78,22 @@ __device__ __forceinline__ void bstore(Rsrc r, unsigned off, float2 v) {
 __device__ __forceinline__ void bstore_f(Rsrc r, unsigned off, float v) {
   __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, (int)off, 0, 0);
 }
+// The same with a wave-uniform scalar offset added to the per-lane one.  A
+// per-lane offset at or past kOutOfRange stays out of range with any scalar
+// offset used here (at most a few MB), whether or not the hardware's range
+// check includes the scalar part.
+__device__ __forceinline__ float2 bload_so(Rsrc r, unsigned off, int soff) {
+  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, soff, 2));
+}
+__device__ __forceinline__ float2 bload_keep_so(Rsrc r, unsigned off, int soff) {
+  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, soff, 0));
+}
+__device__ __forceinline__ void bstore_so(Rsrc r, unsigned off, int soff, float2 v) {
+  __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(lr_v2i, v), r, (int)off, soff, 0);
+}
+__device__ __forceinline__ void bstore_f_so(Rsrc r, unsigned off, int soff, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(int, v), r, (int)off, soff, 0);
+}
 
 // threadIdx.x behind an empty asm statement: values derived from it are not
 // hoisted out of the per-sample loop (which would keep dozens of index
@@ -156,6 +172,9 @@ __device__ __forceinline__ void zero_padding(float2* lds, int n, int off) {
 //     (v, q) = (e mod T, e div T): every access of a wave covers T
 //     consecutive columns of a few rows.
 //
+// With ST (a field stored in slot order, n = N, off = 0) position q of a
+// vector is its slot: li = q*(T+1) + v, no Good-Thomas index map.
+//
 // The walk runs in chunks of at most W elements per thread: first() is
 // called for the whole chunk (issue loads), then second() (consume them).
 // Loads use one chunk (every load of the thread in flight before the first
@@ -184,7 +203,7 @@ struct WalkShape {
   static constexpr int BUF = CH;
 };
 
-template <class C, int AXIS, int W, class F1, class F2>
+template <class C, int AXIS, int W, bool ST, class F1, class F2>
 __device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& first, F2&& second) {
   using WS = WalkShape<C, AXIS, W>;
   if constexpr (WS::ROWS) {
@@ -197,7 +216,7 @@ __device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& firs
     static_for<0, RL::NCH>([&](auto m) {
       const int q = lane + 64 * decltype(m)::value;
       qok[m.value] = q < n;
-      lofs[m.value] = q < n ? lds_index<C>(q + off, 0) : C::SPARE;
+      lofs[m.value] = q < n ? (ST ? q * C::TP : lds_index<C>(q + off, 0)) : C::SPARE;
     });
     static_for<0, WS::NCHUNK>([&](auto c) {
       auto visit = [&](auto& f) {
@@ -231,7 +250,7 @@ __device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& firs
         static_for<0, WS::CH>([&](auto i) {
           constexpr int ii = decltype(c)::value * WS::CH + decltype(i)::value;
           if constexpr (ii < C::N1) {
-            if (tid + ii * C::P < total) f(i, v, q, lds_index<C>(q + off, v), true);
+            if (tid + ii * C::P < total) f(i, v, q, ST ? q * C::TP + v : lds_index<C>(q + off, v), true);
             q += dq;
             v += dv;
             if (q >= n) { q -= n; ++v; }
@@ -251,7 +270,7 @@ __device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& firs
             const int e = tid + ii * C::P;
             const int q = e / C::T;
             const int v = e - q * C::T;
-            if (q < n && v < nvalid) f(i, v, q, lds_index<C>(q + off, v), true);
+            if (q < n && v < nvalid) f(i, v, q, ST ? q * C::TP + v : lds_index<C>(q + off, v), true);
           }
         });
       };
@@ -273,23 +292,24 @@ __device__ __forceinline__ unsigned elem_off(bool ok, int n, int vec, int q) {
 // Load a tile of complex (or real) natural-layout rows/columns of an n x n
 // field (src, wave-uniform) into shared memory.  Tile vector v is field
 // row/column vf(v).
-template <class C, int AXIS, class VF>
+// (ST: src is stored in slot order; the real amplitudes are always natural)
+template <class C, int AXIS, bool ST, class VF>
 __device__ __forceinline__ void load_tile(float2* lds, const void* src, bool real, int n, int off, VF&& vf,
                                           int nvalid) {
-  zero_padding<C>(lds, n, off);
+  if constexpr (!ST) zero_padding<C>(lds, n, off);
   constexpr int BUF = WalkShape<C, AXIS, kAll>::BUF;
   if (real) {
     // (real input: loads masked per lane; 4-byte buffer loads over the whole
     // row runs measured slower here)
     const float* __restrict__ in = static_cast<const float*>(src);
     float buf[BUF];
-    tile_walk2<C, AXIS, kAll>(n, off, nvalid,
+    tile_walk2<C, AXIS, kAll, false>(n, off, nvalid,
         [&](auto i, int v, int q, int, bool ok) { buf[i.value] = ok ? ld(in, nat_index<AXIS>(n, vf(v), q)) : 0.f; },
         [&](auto i, int, int, int li, bool) { lds[li] = c2(buf[i.value], 0.f); });
   } else {
     const Rsrc r = make_rsrc(src, (unsigned)(n * n) * 8u);
     float2 buf[BUF];
-    tile_walk2<C, AXIS, kAll>(n, off, nvalid,
+    tile_walk2<C, AXIS, kAll, ST>(n, off, nvalid,
         [&](auto i, int v, int q, int, bool ok) { buf[i.value] = bload(r, elem_off<AXIS, 8>(ok, n, vf(v), q)); },
         [&](auto i, int, int, int li, bool) { lds[li] = buf[i.value]; });
   }
@@ -305,25 +325,25 @@ __device__ __forceinline__ void tile_issue(TileBuf<C, AXIS>& buf, const void* sr
                                            int nvalid) {
   if (real) {
     const float* __restrict__ in = static_cast<const float*>(src);
-    tile_walk2<C, AXIS, kAll>(n, 0, nvalid,
+    tile_walk2<C, AXIS, kAll, false>(n, 0, nvalid,
         [&](auto i, int v, int q, int, bool ok) { buf[i.value].x = ok ? ld(in, nat_index<AXIS>(n, vf(v), q)) : 0.f; },
         [](auto, int, int, int, bool) {});
   } else {
     const Rsrc r = make_rsrc(src, (unsigned)(n * n) * 8u);
-    tile_walk2<C, AXIS, kAll>(n, 0, nvalid,
+    tile_walk2<C, AXIS, kAll, false>(n, 0, nvalid,
         [&](auto i, int v, int q, int, bool ok) { buf[i.value] = bload(r, elem_off<AXIS, 8>(ok, n, vf(v), q)); },
         [](auto, int, int, int, bool) {});
   }
 }
-template <class C, int AXIS>
+template <class C, int AXIS, bool ST>
 __device__ __forceinline__ void tile_commit(float2* lds, const TileBuf<C, AXIS>& buf, bool real, int n, int off,
                                             int nvalid) {
-  zero_padding<C>(lds, n, off);
+  if constexpr (!ST) zero_padding<C>(lds, n, off);
   if (real) {
-    tile_walk2<C, AXIS, kAll>(n, off, nvalid, [](auto, int, int, int, bool) {},
+    tile_walk2<C, AXIS, kAll, ST>(n, off, nvalid, [](auto, int, int, int, bool) {},
         [&](auto i, int, int, int li, bool) { lds[li] = c2(buf[i.value].x, 0.f); });
   } else {
-    tile_walk2<C, AXIS, kAll>(n, off, nvalid, [](auto, int, int, int, bool) {},
+    tile_walk2<C, AXIS, kAll, ST>(n, off, nvalid, [](auto, int, int, int, bool) {},
         [&](auto i, int, int, int li, bool) { lds[li] = buf[i.value]; });
   }
 }
@@ -353,7 +373,7 @@ __device__ __forceinline__ void load_seed(float2* lds, const PassArgs& a, int b,
   constexpr int BUF = WalkShape<C, AXIS, kAll>::BUF;
   float2 buf[BUF];
   float g[BUF];
-  tile_walk2<C, AXIS, kAll>(n, off, nvalid,
+  tile_walk2<C, AXIS, kAll, false>(n, off, nvalid,
       [&](auto i, int v, int q, int, bool ok) {
         float gv = 0.f;
         float2 u = c2(0.f, 0.f);
@@ -380,12 +400,12 @@ __device__ __forceinline__ void load_seed(float2* lds, const PassArgs& a, int b,
 
 // Store a tile from shared memory into natural-layout rows/columns of an
 // n x n field (out, wave-uniform).
-template <class C, int AXIS, class VF>
+template <class C, int AXIS, bool ST, class VF>
 __device__ __forceinline__ void store_tile(const float2* lds, float2* __restrict__ out, int n, int off, VF&& vf,
                                            int nvalid) {
   const Rsrc r = make_rsrc(out, (unsigned)(n * n) * 8u);
   float2 buf[WalkShape<C, AXIS, kStoreChunk>::BUF];
-  tile_walk2<C, AXIS, kStoreChunk>(n, off, nvalid,
+  tile_walk2<C, AXIS, kStoreChunk, ST>(n, off, nvalid,
       [&](auto i, int, int, int li, bool) { buf[i.value] = lds[li]; },
       [&](auto i, int v, int q, int, bool ok) { bstore(r, elem_off<AXIS, 8>(ok, n, vf(v), q), buf[i.value]); });
 }
@@ -394,7 +414,7 @@ __device__ __forceinline__ void store_tile(const float2* lds, float2* __restrict
 template <class C, int AXIS, class VF>
 __device__ __forceinline__ void zero_vectors(float2* __restrict__ out, int n, VF&& vf, int nvalid) {
   const Rsrc r = make_rsrc(out, (unsigned)(n * n) * 8u);
-  tile_walk2<C, AXIS, kStoreChunk>(n, 0, nvalid, [&](auto, int, int, int, bool) {},
+  tile_walk2<C, AXIS, kStoreChunk, false>(n, 0, nvalid, [&](auto, int, int, int, bool) {},
       [&](auto, int v, int q, int, bool ok) { bstore(r, elem_off<AXIS, 8>(ok, n, vf(v), q), c2(0.f, 0.f)); });
 }
 
@@ -416,7 +436,7 @@ __device__ __forceinline__ void tile_outputs(const float2* lds, float* rsum, con
   float* io = a.intensity ? a.intensity + (size_t)b * nn : nullptr;
   if (fo || sv || io) {
     float2 buf[WalkShape<C, AXIS, kStoreChunk>::BUF];
-    tile_walk2<C, AXIS, kStoreChunk>(n, off, nvalid,
+    tile_walk2<C, AXIS, kStoreChunk, false>(n, off, nvalid,
         [&](auto i, int, int, int li, bool) { buf[i.value] = lds[li]; },
         [&](auto i, int v, int q, int, bool ok) {
           if (ok) {
@@ -499,41 +519,77 @@ __device__ __forceinline__ void add_skip(const PassArgs& a, int b, int vec, bool
   });
 }
 
-// (in / out: n rows of pitch elements, wave-uniform)
-template <class C>
+// Stored-order A-item access (ST: an N x N array whose axis positions are
+// slots): element k of this thread's A-item j lies at stored index
+// j + N2*k along the pass axis, a constant stride of N2*N elements, so every
+// element is one per-lane base plus a compile-time scalar offset and costs
+// no vector instructions.  Lanes outside the tile (vok false) take the
+// out-of-range base.
+template <class C, int ES>
+__device__ __forceinline__ unsigned a_base_st(int vec, bool vok) {
+  const int j = opaque_tid() / C::T;
+  return vok ? (unsigned)(j * C::N + vec) * (unsigned)ES : kOutOfRange;
+}
+template <class C, int ES, int K>
+constexpr int a_soff_st() { return K * C::N2 * C::N * ES; }
+
+// (in / out: n rows of pitch elements, wave-uniform; with ST, n = pitch = N)
+template <class C, bool ST = false>
 __device__ __forceinline__ void load_a_direct(const float2* __restrict__ in, int pitch, int n, int off, int vec,
                                               bool vok, float2 (&x)[C::N1]) {
   const Rsrc r = make_rsrc(in, (unsigned)(n * pitch) * 8u);
-  for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
-    x[k.value] = bload(r, valid ? (unsigned)idx * 8u : kOutOfRange);
-  });
+  if constexpr (ST) {
+    const unsigned base = a_base_st<C, 8>(vec, vok);
+    static_for<0, C::N1>([&](auto k) { x[k.value] = bload_so(r, base, a_soff_st<C, 8, k.value>()); });
+  } else {
+    for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
+      x[k.value] = bload(r, valid ? (unsigned)idx * 8u : kOutOfRange);
+    });
+  }
 }
-template <class C>
+template <class C, bool ST = false>
 __device__ __forceinline__ void store_a_direct(float2* __restrict__ out, int pitch, int n, int off, int vec,
                                                bool vok, const float2 (&x)[C::N1]) {
   const Rsrc r = make_rsrc(out, (unsigned)(n * pitch) * 8u);
-  for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
-    bstore(r, valid ? (unsigned)idx * 8u : kOutOfRange, x[k.value]);
-  });
+  if constexpr (ST) {
+    const unsigned base = a_base_st<C, 8>(vec, vok);
+    static_for<0, C::N1>([&](auto k) { bstore_so(r, base, a_soff_st<C, 8, k.value>(), x[k.value]); });
+  } else {
+    for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
+      bstore(r, valid ? (unsigned)idx * 8u : kOutOfRange, x[k.value]);
+    });
+  }
 }
 // As load_a_direct, reading only the elements k with bit k of mask set (the
 // others are zero).
-template <class C>
+template <class C, bool ST = false>
 __device__ __forceinline__ void load_a_direct_masked(const float2* __restrict__ in, int pitch, int n, int off,
                                                      int vec, bool vok, unsigned mask, float2 (&x)[C::N1]) {
   const Rsrc r = make_rsrc(in, (unsigned)(n * pitch) * 8u);
-  for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
-    x[k.value] = bload(r, valid && ((mask >> k.value) & 1u) ? (unsigned)idx * 8u : kOutOfRange);
-  });
+  if constexpr (ST) {
+    const unsigned base = a_base_st<C, 8>(vec, vok);
+    static_for<0, C::N1>([&](auto k) {
+      x[k.value] = bload_so(r, ((mask >> k.value) & 1u) ? base : kOutOfRange, a_soff_st<C, 8, k.value>());
+    });
+  } else {
+    for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
+      x[k.value] = bload(r, valid && ((mask >> k.value) & 1u) ? (unsigned)idx * 8u : kOutOfRange);
+    });
+  }
 }
 // Per-layer [q][vec] table of n x n entries at this thread's A-item.
-template <class C>
+template <class C, bool ST = false>
 __device__ __forceinline__ void load_a_table(const float2* __restrict__ tab, int n, int off, int vec, bool vok,
                                              float2 (&m)[C::N1]) {
   const Rsrc r = make_rsrc(tab, (unsigned)(n * n) * 8u);
-  for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool valid) {
-    m[k.value] = bload_keep(r, valid ? (unsigned)idx * 8u : kOutOfRange);
-  });
+  if constexpr (ST) {
+    const unsigned base = a_base_st<C, 8>(vec, vok);
+    static_for<0, C::N1>([&](auto k) { m[k.value] = bload_keep_so(r, base, a_soff_st<C, 8, k.value>()); });
+  } else {
+    for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool valid) {
+      m[k.value] = bload_keep(r, valid ? (unsigned)idx * 8u : kOutOfRange);
+    });
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -556,8 +612,14 @@ __device__ __forceinline__ void load_a_table(const float2* __restrict__ tab, int
 // ntiles, so a workgroup keeps one tile and strides through the batch.  The
 // ranks are XCD-contiguous: the workgroups of one XCD work on neighbouring
 // items at the same time.
+//
+// FULL (the layer fills the FFT grid, n = N): the fields the passes hand to
+// each other, the modulation tables and the dphi partials are stored in slot
+// order along both axes (plan.hpp), so A-items are read and written at a
+// constant stride with no index arithmetic; only the input amplitudes of the
+// first pass are natural.  Otherwise everything is in natural order.
 // ---------------------------------------------------------------------------
-template <class C, int KIND, int AXIS>
+template <class C, int KIND, int AXIS, bool FULL>
 __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
     fresnel_pass(PassArgs a) {
   static_assert(KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid || KIND == kBwdLast,
@@ -580,9 +642,35 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
   const bool conj_tab = a.conj_tab != 0;
   const bool real = a.in_real != 0;
 
-  float acc[ACC ? N1 : 1];
+  // dphi accumulators, one per A-item element: registers, or (column kinds)
+  // this thread's private shared-memory slots, which leaves the registers to
+  // the two A-items, the modulation and the prefetch buffer that are live at
+  // once in the adjoint passes
+  constexpr bool ACC_LDS = ACC && DIRECT;
+  __shared__ float acc_lds[ACC_LDS ? N1 * C::P : 1];
+  float acc[ACC && !ACC_LDS ? N1 : 1];
+  auto acc_add = [&](auto k, float v) {
+    if constexpr (ACC_LDS) {
+      acc_lds[k.value * C::P + threadIdx.x] += v;
+    } else {
+      acc[k.value] += v;
+    }
+  };
+  auto acc_get = [&](auto k) {
+    if constexpr (ACC_LDS) {
+      return acc_lds[k.value * C::P + threadIdx.x];
+    } else {
+      return acc[k.value];
+    }
+  };
   if constexpr (ACC) {
-    static_for<0, N1>([&](auto k) { acc[k.value] = 0.f; });
+    static_for<0, N1>([&](auto k) {
+      if constexpr (ACC_LDS) {
+        acc_lds[k.value * C::P + threadIdx.x] = 0.f;
+      } else {
+        acc[k.value] = 0.f;
+      }
+    });
   }
   stage_table_by_freq<C>(lds, a.tab);  // visible after the first barrier below
 
@@ -595,7 +683,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
     write_a(t, j, v);
     mid();
     __syncthreads();
-    b_spectral(t, cj);
+    b_spectral<C, ACC>(t, cj);
     __syncthreads();
     read_a(t, j, v);
     Dft<N1, 1>::run(v);
@@ -639,8 +727,8 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
       const int nv = live ? min(C::T, a.nvec - v0) : 0;
       const float2* src = G_FIRST ? static_cast<const float2*>(a.in) : a.act_in;
       if constexpr (DIRECT) {
-        load_a_direct_masked<C>(src + (size_t)(item / a.ntiles) * nn, n, n, off, v0 + t.v, t.v < nv,
-                                G_FIRST ? gmask : ~0u, pf);
+        load_a_direct_masked<C, FULL>(src + (size_t)(item / a.ntiles) * nn, n, n, off, v0 + t.v, t.v < nv,
+                                      G_FIRST ? gmask : ~0u, pf);
       } else {
         tile_issue<C, AXIS>(pft, src + (size_t)(item / a.ntiles) * nn, false, n, Consecutive{v0}, nv);
       }
@@ -671,20 +759,20 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
       if constexpr (PREFETCH) {
         static_for<0, N1>([&](auto k) { x[k.value] = pf[k.value]; });
       } else {
-        load_a_direct_masked<C>(fin, n, n, off, vec, vok, gmask, x);
+        load_a_direct_masked<C, FULL>(fin, n, n, off, vec, vok, gmask, x);
       }
-      load_a_direct<C>(a.act_in + (size_t)b * nn, n, n, off, vec, vok, ar);
+      load_a_direct<C, FULL>(a.act_in + (size_t)b * nn, n, n, off, vec, vok, ar);
       float2 m[N1];
       if constexpr (BIG) {
         prop(x, true, nothing);
-        load_a_table<C>(a.mod, n, off, vec, vok, m);
+        load_a_table<C, FULL>(a.mod, n, off, vec, vok, m);
       } else {
-        prop(x, true, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+        prop(x, true, [&] { load_a_table<C, FULL>(a.mod, n, off, vec, vok, m); });
       }
       static_for<0, N1>([&](auto k) { x[k.value] = cmulc(x[k.value], m[k.value]); });
       // A_1, then dphi_1 += Im(conj(A_1) conj(M_1) G_1)
       prop(ar, false, prefetch);
-      static_for<0, N1>([&](auto k) { acc[k.value] += ar[k.value].x * x[k.value].y - ar[k.value].y * x[k.value].x; });
+      static_for<0, N1>([&](auto k) { acc_add(k, ar[k.value].x * x[k.value].y - ar[k.value].y * x[k.value].x); });
     } else if constexpr (ACC) {
       // A_l from the saved input of the forward pass, while G (the gradient
       // with respect to W_l) is in flight
@@ -693,22 +781,22 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
         if constexpr (PREFETCH) {
           static_for<0, N1>([&](auto k) { ar[k.value] = pf[k.value]; });
         } else {
-          load_a_direct<C>(a.act_in + (size_t)b * nn, n, n, off, vec, vok, ar);
+          load_a_direct<C, FULL>(a.act_in + (size_t)b * nn, n, n, off, vec, vok, ar);
         }
-        load_a_direct_masked<C>(fin, n, n, off, vec, vok, gmask, x);
+        load_a_direct_masked<C, FULL>(fin, n, n, off, vec, vok, gmask, x);
         prop(ar, false, nothing);
       } else {
         __syncthreads();  // shared memory reuse across items
         if constexpr (PREFETCH) {
-          tile_commit<C, AXIS>(lds, pft, false, n, off, nvalid);
+          tile_commit<C, AXIS, FULL>(lds, pft, false, n, off, nvalid);
         } else {
-          load_tile<C, AXIS>(lds, a.act_in + (size_t)b * nn, false, n, off, Consecutive{vec0}, nvalid);
+          load_tile<C, AXIS, FULL>(lds, a.act_in + (size_t)b * nn, false, n, off, Consecutive{vec0}, nvalid);
         }
         __syncthreads();
         read_a(t, j, ar);
         prop(ar, false, nothing);
         __syncthreads();
-        load_tile<C, AXIS>(lds, fin, false, n, off, Consecutive{vec0}, nvalid);
+        load_tile<C, AXIS, FULL>(lds, fin, false, n, off, Consecutive{vec0}, nvalid);
         __syncthreads();
         read_a(t, j, x);
       }
@@ -717,14 +805,14 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
       float2 m[N1];
       if constexpr (BIG) {
         prop(x, true, nothing);
-        load_a_table<C>(a.mod, n, off, vec, vok, m);
+        load_a_table<C, FULL>(a.mod, n, off, vec, vok, m);
       } else {
-        prop(x, true, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+        prop(x, true, [&] { load_a_table<C, FULL>(a.mod, n, off, vec, vok, m); });
       }
       // conj(M_l) G_l (zero outside the aperture) and dphi_l += Im(conj(U_l) G_l) = Im(conj(A_l) conj(M_l) G_l)
       static_for<0, N1>([&](auto k) {
         const float2 h = cmulc(x[k.value], m[k.value]);
-        acc[k.value] += ar[k.value].x * h.y - ar[k.value].y * h.x;
+        acc_add(k, ar[k.value].x * h.y - ar[k.value].y * h.x);
         x[k.value] = h;
       });
       if constexpr (KIND == kBwdMid && DIRECT) {
@@ -736,11 +824,17 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
       }
     } else {
       if constexpr (DIRECT) {
-        load_a_direct<C>(fin, n, n, off, vec, vok, x);
+        load_a_direct<C, FULL>(fin, n, n, off, vec, vok, x);
       } else {
         __syncthreads();  // shared memory reuse across items
-        load_tile<C, AXIS>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * (real ? 4 : 8), real, n, off,
-                           Consecutive{vec0}, nvalid);
+        const void* src = static_cast<const char*>(a.in) + (size_t)b * nn * (real ? 4 : 8);
+        if (FULL && real) {
+          // natural amplitudes: stored row vec0 + v is natural row pos_of_slot(vec0 + v)
+          load_tile<C, AXIS, false>(lds, src, true, n, off,
+                                    [&](int v) { return C::Plan::pos_of_slot(vec0 + v); }, nvalid);
+        } else {
+          load_tile<C, AXIS, FULL>(lds, src, real, n, off, Consecutive{vec0}, nvalid);
+        }
         __syncthreads();
         read_a(t, j, x);
       }
@@ -748,9 +842,9 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
         float2 m[N1];
         if constexpr (BIG) {
           prop(x, conj_tab, nothing);
-          load_a_table<C>(a.mod, n, off, vec, vok, m);
+          load_a_table<C, FULL>(a.mod, n, off, vec, vok, m);
         } else {
-          prop(x, conj_tab, [&] { load_a_table<C>(a.mod, n, off, vec, vok, m); });
+          prop(x, conj_tab, [&] { load_a_table<C, FULL>(a.mod, n, off, vec, vok, m); });
         }
         // U_l = M_l A_l, zero outside the aperture (crop)
         static_for<0, N1>([&](auto k) { x[k.value] = cmul(x[k.value], m[k.value]); });
@@ -760,11 +854,11 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
 
     if constexpr (KIND != kBwdLast) {
       if constexpr (DIRECT) {
-        store_a_direct<C>(a.out + (size_t)b * nn, n, n, off, vec, vok, x);
+        store_a_direct<C, FULL>(a.out + (size_t)b * nn, n, n, off, vec, vok, x);
       } else {
         write_a(t, j, x);
         __syncthreads();
-        store_tile<C, AXIS>(lds, a.out + (size_t)b * nn, n, off, Consecutive{vec0}, nvalid);
+        store_tile<C, AXIS, FULL>(lds, a.out + (size_t)b * nn, n, off, Consecutive{vec0}, nvalid);
         if constexpr (ACC) prefetch();
       }
     }
@@ -775,9 +869,14 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
     const int vec = vec0 + t.v;
     const bool vok = t.v < min(C::T, a.nvec - vec0);
     const Rsrc dp = make_rsrc(a.dphi_part + (size_t)(rank / a.ntiles) * nn, (unsigned)nn * 4u);
-    for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
-      bstore_f(dp, in ? (unsigned)idx * 4u : kOutOfRange, acc[k.value]);
-    });
+    if constexpr (FULL) {
+      const unsigned base = a_base_st<C, 4>(vec, vok);
+      static_for<0, N1>([&](auto k) { bstore_f_so(dp, base, a_soff_st<C, 4, k.value>(), acc_get(k)); });
+    } else {
+      for_a_elems<C>(off, n, n, vec, vok, [&](auto k, int idx, bool in) {
+        bstore_f(dp, in ? (unsigned)idx * 4u : kOutOfRange, acc_get(k));
+      });
+    }
   }
 }
 
@@ -793,12 +892,13 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
 // a.vperm only those vectors are transformed, and the seed pass writes zero
 // vectors for the rest.
 // ---------------------------------------------------------------------------
-template <class C, int KIND, int AXIS>
+template <class C, int KIND, int AXIS, bool FULL>
 __global__ void __launch_bounds__(C::P, C::WAVES) detector_pass(PassArgs a) {
   static_assert(KIND == kFwdLast || KIND == kBwdFirst, "detector-plane kinds only");
   __shared__ float2 lds[C::LDS_ELEMS];
   __shared__ float rsum[KIND == kFwdLast ? C::T * kMaxRegions : 1];
-  __shared__ int vmap[C::T];
+  __shared__ int vmap[C::T];  // natural index of tile vector v
+  __shared__ int vst[C::T];   // its index in the stored (input / gradient) layout
   constexpr int N1 = C::N1;
   const Tile<C> t{lds, (int)(threadIdx.x % C::T), (int)(threadIdx.x / C::T)};
   const int j = t.s;
@@ -828,14 +928,18 @@ __global__ void __launch_bounds__(C::P, C::WAVES) detector_pass(PassArgs a) {
     first = wi.tile * C::T;
     nvalid = min(C::T, n - first);
   }
+  // (with FULL, vperm lists stored indices)
   if ((int)threadIdx.x < C::T) {
     const int v = (int)threadIdx.x;
-    vmap[v] = v < nvalid ? (a.vperm ? a.vperm[first + v] : first + v) : 0;
+    const int sv = v < nvalid ? (a.vperm ? a.vperm[first + v] : first + v) : 0;
+    vst[v] = sv;
+    vmap[v] = FULL ? C::Plan::pos_of_slot(sv) : sv;
   }
   const Mapped vf{vmap};
+  const Mapped vfs{vst};
   if (KIND == kBwdFirst && zero_tile) {
     __syncthreads();
-    for (int b = b0; b < b1; ++b) zero_vectors<C, AXIS>(a.out + (size_t)b * nn, n, vf, nvalid);
+    for (int b = b0; b < b1; ++b) zero_vectors<C, AXIS>(a.out + (size_t)b * nn, n, vfs, nvalid);
     return;
   }
   stage_table_by_freq<C>(lds, a.tab);
@@ -846,7 +950,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES) detector_pass(PassArgs a) {
   for (int b = b0; b < b1; ++b) {
     float2 x[N1];
     __syncthreads();
-    load_tile<C, AXIS>(lds, static_cast<const float2*>(a.in) + (size_t)b * nn, false, n, off, vf, nvalid);
+    load_tile<C, AXIS, FULL>(lds, static_cast<const float2*>(a.in) + (size_t)b * nn, false, n, off, vfs, nvalid);
     __syncthreads();
     read_a(t, j, x);
     // rest of the last hop: U_D
@@ -868,7 +972,7 @@ __global__ void __launch_bounds__(C::P, C::WAVES) detector_pass(PassArgs a) {
       if (a.grad_int) {
         float2 g[N1];
         __syncthreads();  // every read of U_D from shared memory is done
-        load_tile<C, AXIS>(lds, a.grad_int + (size_t)b * nn, true, n, off, vf, nvalid);
+        load_tile<C, AXIS, false>(lds, a.grad_int + (size_t)b * nn, true, n, off, vf, nvalid);
         __syncthreads();
         read_a(t, j, g);
         static_for<0, N1>([&](auto k) { x[k.value] = cscale(x[k.value], 2.f * g[k.value].x); });
@@ -898,11 +1002,11 @@ __global__ void __launch_bounds__(C::P, C::WAVES) detector_pass(PassArgs a) {
       read_a(t, j, x);
       Dft<N1, 1>::run(x);
       if constexpr (AXIS == kCol) {
-        store_a_direct<C>(a.out + (size_t)b * nn, n, n, off, vec, vok, x);
+        store_a_direct<C, FULL>(a.out + (size_t)b * nn, n, n, off, vst[t.v], vok, x);
       } else {
         write_a(t, j, x);
         __syncthreads();
-        store_tile<C, AXIS>(lds, a.out + (size_t)b * nn, n, off, vf, nvalid);
+        store_tile<C, AXIS, FULL>(lds, a.out + (size_t)b * nn, n, off, vfs, nvalid);
       }
     }
   }
@@ -1121,7 +1225,7 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
         load_seed<C, kRow>(lds, a, b, vec0, nvalid);
       } else {
         const size_t es = a.in_real ? sizeof(float) : sizeof(float2);
-        load_tile<C, kRow>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * es, a.in_real != 0, n, off,
+        load_tile<C, kRow, false>(lds, static_cast<const char*>(a.in) + (size_t)b * nn * es, a.in_real != 0, n, off,
                            Consecutive{vec0}, nvalid);
       }
       __syncthreads();
@@ -1140,7 +1244,7 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
       write_a(t, j, x);  // positions, cropped on output
       __syncthreads();
       if constexpr (KIND == kAsRowIfft) {
-        store_tile<C, kRow>(lds, a.out + (size_t)b * nn, n, off, Consecutive{vec0}, nvalid);
+        store_tile<C, kRow, false>(lds, a.out + (size_t)b * nn, n, off, Consecutive{vec0}, nvalid);
       } else {  // kAsRowLast
         tile_outputs<C, kRow>(lds, rsum, a, b, Consecutive{vec0}, nvalid, wi.tile);
       }
@@ -1223,17 +1327,17 @@ template <int N, int KIND, int AXIS>
 using LayerCfg = Cfg<std::conditional_t<AXIS == kRow, typename RowPlanFor<N>::type, typename PlanFor<N>::type>,
                      LayerTile<N, KIND, AXIS>::T>;
 
-template <int N, int KIND, int AXIS>
+template <int N, int KIND, int AXIS, bool FULL>
 hipError_t launch_fr(const PassArgs& a, hipStream_t st) {
   if constexpr (KIND == kFwdLast || KIND == kBwdFirst) {
     using C = std::conditional_t<AXIS == kRow, RowCfgFor<N>, CfgFor<N>>;
     const dim3 grid(work_grid(a.ntiles, (a.batch + a.spg - 1) / a.spg));
-    hipLaunchKernelGGL((detector_pass<C, KIND, AXIS>), grid, dim3(C::P), 0, st, a);
+    hipLaunchKernelGGL((detector_pass<C, KIND, AXIS, FULL>), grid, dim3(C::P), 0, st, a);
   } else {
     using C = LayerCfg<N, KIND, AXIS>;
     if (a.workers < 1) return hipErrorInvalidValue;
     const dim3 grid(8 * ((a.workers + 7) / 8));
-    hipLaunchKernelGGL((fresnel_pass<C, KIND, AXIS>), grid, dim3(C::P), 0, st, a);
+    hipLaunchKernelGGL((fresnel_pass<C, KIND, AXIS, FULL>), grid, dim3(C::P), 0, st, a);
   }
   return hipGetLastError();
 }
@@ -1270,17 +1374,19 @@ inline int resident_per_cu(const void* kernel, int block) {
   return nb;
 }
 
-template <int N, int KIND, int AXIS>
+template <int N, int KIND, int AXIS, bool FULL>
 int slots_fr() {
   using C = LayerCfg<N, KIND, AXIS>;
   static int per_cu = 0;
-  if (per_cu == 0) per_cu = resident_per_cu(reinterpret_cast<const void*>(&fresnel_pass<C, KIND, AXIS>), C::P);
+  if (per_cu == 0)
+    per_cu = resident_per_cu(reinterpret_cast<const void*>(&fresnel_pass<C, KIND, AXIS, FULL>), C::P);
   return per_cu * device_cus();
 }
 
 template <int N, int KIND>
-int slots_fr_axis(Axis axis) {
-  return axis == kRow ? slots_fr<N, KIND, kRow>() : slots_fr<N, KIND, kCol>();
+int slots_fr_axis(Axis axis, bool full) {
+  if (full) return axis == kRow ? slots_fr<N, KIND, kRow, true>() : slots_fr<N, KIND, kCol, true>();
+  return axis == kRow ? slots_fr<N, KIND, kRow, false>() : slots_fr<N, KIND, kCol, false>();
 }
 
 template <int N, int KIND>
@@ -1301,23 +1407,25 @@ int tile_fr_n(PassKind kind, Axis axis) {
 }
 
 template <int N>
-int slots_fr_n(PassKind kind, Axis axis) {
+int slots_fr_n(PassKind kind, Axis axis, bool full) {
   switch (kind) {
-    case kPropOnce: return slots_fr_axis<N, kPropOnce>(axis);
-    case kFwdMid: return slots_fr_axis<N, kFwdMid>(axis);
-    case kBwdMid: return slots_fr_axis<N, kBwdMid>(axis);
-    case kBwdLast: return slots_fr_axis<N, kBwdLast>(axis);
+    case kPropOnce: return slots_fr_axis<N, kPropOnce>(axis, full);
+    case kFwdMid: return slots_fr_axis<N, kFwdMid>(axis, full);
+    case kBwdMid: return slots_fr_axis<N, kBwdMid>(axis, full);
+    case kBwdLast: return slots_fr_axis<N, kBwdLast>(axis, full);
     default: return 0;
   }
 }
 
 template <int N, int KIND>
 hipError_t launch_fr_axis(Axis axis, const PassArgs& a, hipStream_t st) {
-  return axis == kRow ? launch_fr<N, KIND, kRow>(a, st) : launch_fr<N, KIND, kCol>(a, st);
+  if (a.full) return axis == kRow ? launch_fr<N, KIND, kRow, true>(a, st) : launch_fr<N, KIND, kCol, true>(a, st);
+  return axis == kRow ? launch_fr<N, KIND, kRow, false>(a, st) : launch_fr<N, KIND, kCol, false>(a, st);
 }
 
 template <int N>
 hipError_t launch_fr_n(PassKind kind, Axis axis, const PassArgs& a, hipStream_t st) {
+  if (a.full && a.n != N) return hipErrorInvalidValue;
   switch (kind) {
     case kPropOnce: return launch_fr_axis<N, kPropOnce>(axis, a, st);
     case kFwdMid: return launch_fr_axis<N, kFwdMid>(axis, a, st);
@@ -1364,5 +1472,14 @@ hipError_t prep_as_n(const float2* H, float2* Hp, float scale, int centred, hipS
 
 template <int N>
 TileShape shape_n() { return TileShape{CfgFor<N>::T, CfgFor<N>::S}; }
+
+// The slot order of the separable passes' stored fields: rows and columns
+// use the same plan, so one map serves both axes.
+template <int N>
+SlotMap slot_map_n() {
+  using PL = typename PlanFor<N>::type;
+  static_assert(std::is_same_v<PL, typename RowPlanFor<N>::type>, "stored slot order needs one plan for both axes");
+  return SlotMap{PL::N1, PL::N2, PL::PFA ? 1 : 0};
+}
 
 }  // namespace lr

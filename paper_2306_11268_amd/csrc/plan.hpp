@@ -18,6 +18,12 @@
 // CT  (Cooley-Tukey):   pos(x, j) = j + N2*x (the slot itself),  freq = k1 + N1*k2
 // PFA (Good-Thomas, gcd(N1,N2) = 1, no twiddles):
 //                       pos(x, j) = (N2*x + N1*j) mod N,        freq = CRT(k1 mod N1, k2 mod N2)
+//
+// Slot order as a storage order: a field whose rows and columns are both
+// stored in slot order (stored index s along an axis holds natural position
+// pos_of_slot(s)) has the elements of A-item j at the stored indices
+// j + N2*x, a constant stride, for either plan; in natural order the
+// Good-Thomas positions wrap around N once per item.
 #pragma once
 
 #include "codelets.hpp"
@@ -56,6 +62,8 @@ struct Plan2 {
     return base + N2 * x;
   }
   LR_HD static int pos(int x, int j) { return pos_at(pos_base(j), x); }
+  // Natural position held by slot s (inverse of slot_of_pos).
+  LR_HD static int pos_of_slot(int s) { return pos(s / N2, s % N2); }
   // Slot holding natural position p.
   LR_HD static int slot_of_pos(int p) {
     if (PFA) return ((p % N1) * U1 % N1) * N2 + (p % N2) * U2 % N2;

@@ -189,7 +189,7 @@ __device__ __forceinline__ void b_spectral_item(const Tile<C>& t, int k1, bool c
   fence();
   write_b(t, k1, y);
 }
-template <class C>
+template <class C, bool SERIAL = false>
 __device__ __forceinline__ void b_spectral(const Tile<C>& t, bool conj_tab) {
   // The B-item index behind an empty asm statement: twiddle offsets derived
   // from it are formed here, not hoisted out of the caller's loops.
@@ -206,6 +206,9 @@ __device__ __forceinline__ void b_spectral(const Tile<C>& t, bool conj_tab) {
     static_for<0, C::IB>([&](auto ic) {
       const int k1 = s + C::S * decltype(ic)::value;
       if (C::B_FULL || k1 < C::N1) b_spectral_item(t, k1, conj_tab);
+      // SERIAL: one item's registers at a time (for kernels that hold other
+      // arrays across the B-step)
+      if constexpr (SERIAL) __builtin_amdgcn_sched_barrier(0);
     });
   }
 }
