@@ -235,12 +235,16 @@ std::string as_name(int N, int kind) {
 // persistent schedule with prefetching for them.
 int schedule_layer_pass(int N, lr::PassKind kind, Axis ax, int max_lanes, PassArgs& a) {
   const int slots = lr::fresnel_pass_slots(N, kind, ax, a.full != 0);
-  const int tile_t = lr::fresnel_pass_tile(N, kind, ax);
+  const int tile_t = lr::fresnel_pass_tile(N, kind, ax, a.full != 0);
   if (slots <= 0 || tile_t <= 0) return LR_E_HIP;
   a.ntiles = ceil_div(a.nvec, tile_t);
   if (kind == lr::kBwdMid || kind == lr::kBwdLast) {
     int lanes = std::max(1, slots / std::max(1, a.ntiles));
     lanes = std::min(lanes, std::max(1, std::min(max_lanes, a.batch)));
+    // the same number of samples for every lane (the last round of a
+    // persistent pass is as long as its longest lane)
+    const int per = ceil_div(a.batch, lanes);
+    lanes = ceil_div(a.batch, per);
     a.lanes = lanes;
     a.workers = lanes * a.ntiles;
   } else {

@@ -9,7 +9,7 @@
 namespace lr {
 template hipError_t launch_fr_n<LR_FFT_N>(PassKind, Axis, const PassArgs&, hipStream_t);
 template int slots_fr_n<LR_FFT_N>(PassKind, Axis, bool);
-template int tile_fr_n<LR_FFT_N>(PassKind, Axis);
+template int tile_fr_n<LR_FFT_N>(PassKind, Axis, bool);
 template hipError_t launch_as_n<LR_FFT_N>(AsPassKind, const PassArgs&, hipStream_t);
 template hipError_t prep_as_n<LR_FFT_N>(const float2*, float2*, float, int, hipStream_t);
 template TileShape shape_n<LR_FFT_N>();

@@ -9,7 +9,7 @@ namespace lr {
 // Per-size entry points, defined in kern_size.hip (one object per size).
 template <int N> hipError_t launch_fr_n(PassKind, Axis, const PassArgs&, hipStream_t);
 template <int N> int slots_fr_n(PassKind, Axis, bool);
-template <int N> int tile_fr_n(PassKind, Axis);
+template <int N> int tile_fr_n(PassKind, Axis, bool);
 template <int N> hipError_t launch_as_n(AsPassKind, const PassArgs&, hipStream_t);
 template <int N> hipError_t prep_as_n(const float2*, float2*, float, int, hipStream_t);
 template <int N> TileShape shape_n();
@@ -475,19 +475,19 @@ hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& 
   }
 }
 
-int fresnel_pass_tile(int N, PassKind kind, Axis axis) {
+int fresnel_pass_tile(int N, PassKind kind, Axis axis, bool full) {
   switch (N) {
-    case 64: return tile_fr_n<64>(kind, axis);
-    case 100: return tile_fr_n<100>(kind, axis);
-    case 128: return tile_fr_n<128>(kind, axis);
-    case 200: return tile_fr_n<200>(kind, axis);
-    case 256: return tile_fr_n<256>(kind, axis);
-    case 350: return tile_fr_n<350>(kind, axis);
-    case 400: return tile_fr_n<400>(kind, axis);
-    case 500: return tile_fr_n<500>(kind, axis);
-    case 512: return tile_fr_n<512>(kind, axis);
-    case 1000: return tile_fr_n<1000>(kind, axis);
-    case 1024: return tile_fr_n<1024>(kind, axis);
+    case 64: return tile_fr_n<64>(kind, axis, full);
+    case 100: return tile_fr_n<100>(kind, axis, full);
+    case 128: return tile_fr_n<128>(kind, axis, full);
+    case 200: return tile_fr_n<200>(kind, axis, full);
+    case 256: return tile_fr_n<256>(kind, axis, full);
+    case 350: return tile_fr_n<350>(kind, axis, full);
+    case 400: return tile_fr_n<400>(kind, axis, full);
+    case 500: return tile_fr_n<500>(kind, axis, full);
+    case 512: return tile_fr_n<512>(kind, axis, full);
+    case 1000: return tile_fr_n<1000>(kind, axis, full);
+    case 1024: return tile_fr_n<1024>(kind, axis, full);
     default: return 0;
   }
 }

@@ -143,7 +143,7 @@ hipError_t launch_fresnel_pass(int N, PassKind kind, Axis axis, const PassArgs& 
 // Workgroups of a separable pass kernel that fit on the current device at
 // once, and the vectors each of its workgroups transforms.
 int fresnel_pass_slots(int N, PassKind kind, Axis axis, bool full);
-int fresnel_pass_tile(int N, PassKind kind, Axis axis);
+int fresnel_pass_tile(int N, PassKind kind, Axis axis, bool full);
 hipError_t launch_as_pass(int N, AsPassKind kind, const PassArgs& a, hipStream_t st);
 
 // Small helper kernels.

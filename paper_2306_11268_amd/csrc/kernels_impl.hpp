@@ -1259,6 +1259,211 @@ __global__ void __launch_bounds__(C::P, (KIND == kAsRowBwdMid || KIND == kAsRowB
 }
 
 // ---------------------------------------------------------------------------
+// Wave-tile layer passes: the layer kinds of the separable path for a field
+// stored in slot order (FULL) with a plan whose B-step has N2 = 8 points
+// (N = 64, 128, 200).
+//
+// A workgroup is one wave and transforms 8 vectors.  Lane (v, j) holds A-item
+// j of vector vec0 + v in registers: its N1 elements at the stored indices
+// j + 8k, one per-lane base plus a compile-time offset each.  The B-step
+// exchange stays inside the wave, 8 B-item indices at a time, through a
+// private shared-memory buffer: the lanes write elements k1 = 8c .. 8c+7 of
+// their A-items, lane (v, s) transforms B-item 8c + s of vector v, and the
+// lanes read their elements back.  Against the workgroup tiles this needs no
+// cross-wave barrier, has no partial tiles (N is a multiple of 8) and holds
+// about 5 KB of shared memory per wave instead of the wave's share of a whole
+// tile (13 KB at N = 200), so more waves stay resident to hide latency.
+// Columns take lanes v-fastest (each load covers 64 contiguous bytes of 8
+// rows), rows j-fastest (64 contiguous bytes of each of 8 rows).
+// ---------------------------------------------------------------------------
+template <class PL, int AXIS>
+struct WaveTile {
+  static constexpr int N = PL::N;
+  static constexpr int N1 = PL::N1;
+  static_assert(PL::N2 == 8, "wave tiles pair 8 A-items with 8 vectors");
+  static constexpr int NC = (N1 + 7) / 8;  // exchange chunks
+  static __device__ __forceinline__ int v_of(int lane) { return AXIS == kCol ? (lane & 7) : (lane >> 3); }
+  static __device__ __forceinline__ int j_of(int lane) { return AXIS == kCol ? (lane >> 3) : (lane & 7); }
+  // Exchange buffer index of (B-item offset s, A-item j, vector v), in
+  // complex entries: s*PS + j*PJ + v*PV.  Each half wave's 32 lanes hit 32
+  // distinct 8-byte bank slots on both sides of the exchange.
+  static constexpr int PJ = AXIS == kCol ? 8 : 1;
+  static constexpr int PV = AXIS == kCol ? 1 : 8;
+  static constexpr int PS = AXIS == kCol ? 72 : 65;
+  static constexpr int XCH = 7 * PS + 64;
+};
+
+// Byte offset of element (stored index j, vector vec) of an N x N array
+// oriented [q][vec] (tables, dphi partials, column fields) or [vec][q] (row
+// fields); element k of the A-item adds wt_soff<...k>.
+template <int N, int ES, bool QMAJOR>
+__device__ __forceinline__ unsigned wt_base(int j, int vec, bool vok) {
+  const unsigned e = QMAJOR ? (unsigned)(j * N + vec) : (unsigned)(vec * N + j);
+  return vok ? e * (unsigned)ES : kOutOfRange;
+}
+template <int N, int ES, bool QMAJOR, int K>
+constexpr int wt_soff() { return QMAJOR ? K * 8 * N * ES : K * 8 * ES; }
+
+template <class PL, int KIND, int AXIS>
+__global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 : 4) wave_pass(PassArgs a) {
+  using WT = WaveTile<PL, AXIS>;
+  constexpr int N = PL::N;
+  constexpr int N1 = PL::N1;
+  constexpr bool ACC = (KIND == kBwdMid || KIND == kBwdLast);
+  constexpr bool FQ = AXIS == kCol;  // field arrays q-major along this pass
+  static_assert(KIND == kFwdMid || ACC, "wave tiles run the layer kinds");
+  __shared__ float2 tab[N];
+  __shared__ float2 xch[WT::XCH];
+  __shared__ float acc_lds[ACC ? N1 * 64 : 1];  // per-lane dphi accumulators
+
+  const int G = (int)gridDim.x;
+  const int l = (int)blockIdx.x;
+  const int rank = (l & 7) * (G >> 3) + (l >> 3);
+  if (rank >= a.workers) return;
+  const int lane = (int)threadIdx.x;
+  const int total = a.ntiles * a.batch;
+  const size_t nn = (size_t)N * N;
+
+  // chirp in B-item order: entry 8*k1 + k2 is frequency freq(k1, k2)
+  for (int i = lane; i < N; i += 64) tab[i] = a.tab[PL::freq(i >> 3, i & 7)];
+  if constexpr (ACC) {
+    static_for<0, N1>([&](auto k) { acc_lds[k.value * 64 + lane] = 0.f; });
+  }
+
+  // One 1-D propagation of this lane's A-item: A-step DFT, B-step (DFT,
+  // x chirp, inverse DFT) in chunks of 8 B-items through the exchange
+  // buffer, inverse A-step DFT.  mid() runs once the first chunk is written
+  // (loads issued there arrive during the B-step).
+  auto prop = [&](float2(&x)[N1], bool cj, auto&& mid) {
+    Dft<N1, -1>::run(x);
+    int vv = WT::v_of(opaque_tid() & 63);
+    int jj = WT::j_of(opaque_tid() & 63);
+    const int wb = jj * WT::PJ + vv * WT::PV;  // A side: + s * PS
+    const int bb = jj * WT::PS + vv * WT::PV;  // B side: + j' * PJ
+    static_for<0, WT::NC>([&](auto cc) {
+      constexpr int c = decltype(cc)::value;
+      static_for<0, 8>([&](auto sc) {
+        constexpr int k1 = 8 * c + decltype(sc)::value;
+        if constexpr (k1 < N1) xch[decltype(sc)::value * WT::PS + wb] = x[k1];
+      });
+      __syncthreads();
+      if constexpr (c == 0) {
+        // loads issued here arrive during the B-step; the scheduling
+        // barriers keep them from being hoisted over the A-step
+        __builtin_amdgcn_sched_barrier(0);
+        mid();
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      const int k1 = 8 * c + jj;
+      if (8 * c + 8 <= N1 || k1 < N1) {
+        float2 y[8];
+        static_for<0, 8>([&](auto jp) { y[jp.value] = xch[bb + jp.value * WT::PJ]; });
+        if constexpr (!PL::PFA) {
+          static_for<1, 8>([&](auto jp) { y[jp.value] = cmul(y[jp.value], root_at<N>((unsigned)(k1 * jp.value))); });
+        }
+        Dft<8, -1>::run(y);
+        const float2* tk = tab + 8 * k1;
+        if (cj) {
+          static_for<0, 8>([&](auto k2) { y[k2.value] = cmulc(y[k2.value], tk[k2.value]); });
+        } else {
+          static_for<0, 8>([&](auto k2) { y[k2.value] = cmul(y[k2.value], tk[k2.value]); });
+        }
+        Dft<8, 1>::run(y);
+        if constexpr (!PL::PFA) {
+          static_for<1, 8>(
+              [&](auto jp) { y[jp.value] = cmul(y[jp.value], root_at<N>((unsigned)(N - k1 * jp.value))); });
+        }
+        static_for<0, 8>([&](auto jp) { xch[bb + jp.value * WT::PJ] = y[jp.value]; });
+      }
+      __syncthreads();
+      static_for<0, 8>([&](auto sc) {
+        constexpr int k1r = 8 * c + decltype(sc)::value;
+        if constexpr (k1r < N1) x[k1r] = xch[decltype(sc)::value * WT::PS + wb];
+      });
+    });
+    Dft<N1, 1>::run(x);
+  };
+  auto nothing = [] {};
+
+  // rows of G that can be nonzero (layer L of a region loss, column passes)
+  unsigned gmask = ~0u;
+  if constexpr (ACC && AXIS == kCol) {
+    if (a.live) {
+      gmask = 0u;
+      const int j = WT::j_of(lane);
+      static_for<0, N1>([&](auto k) {
+        if (ld(a.live, PL::pos_of_slot(j + 8 * k.value)) != 0ull) gmask |= 1u << k.value;
+      });
+    }
+  }
+
+  for (int it = rank; it < total; it += a.workers) {
+    const int tile = it % a.ntiles;
+    const int b = it / a.ntiles;
+    const int vec = tile * 8 + WT::v_of(opaque_tid() & 63);
+    const int j = WT::j_of(opaque_tid() & 63);
+    const bool vok = vec < a.nvec;
+    const unsigned fb = wt_base<N, 8, FQ>(j, vec, vok);    // field arrays
+    const unsigned tb = wt_base<N, 8, true>(j, vec, vok);  // [q][vec] tables
+    const Rsrc rin = make_rsrc(static_cast<const float2*>(a.in) + (size_t)b * nn, (unsigned)nn * 8u);
+    const Rsrc rmod = make_rsrc(a.mod, (unsigned)nn * 8u);
+    auto load_field = [&](Rsrc r, unsigned mask, float2(&x)[N1]) {
+      static_for<0, N1>([&](auto k) {
+        x[k.value] = bload_so(r, ((mask >> k.value) & 1u) ? fb : kOutOfRange, wt_soff<N, 8, FQ, k.value>());
+      });
+    };
+    auto load_mod = [&](float2(&m)[N1]) {
+      static_for<0, N1>([&](auto k) { m[k.value] = bload_keep_so(rmod, tb, wt_soff<N, 8, true, k.value>()); });
+    };
+    float2 x[N1];
+    if constexpr (KIND == kFwdMid) {
+      load_field(rin, ~0u, x);
+      float2 m[N1];
+      prop(x, a.conj_tab != 0, nothing);
+      load_mod(m);
+      static_for<0, N1>([&](auto k) { x[k.value] = cmul(x[k.value], m[k.value]); });
+      prop(x, a.conj_tab != 0, nothing);
+    } else {
+      const Rsrc rw = make_rsrc(a.act_in + (size_t)b * nn, (unsigned)nn * 8u);
+      float2 ar[N1];
+      float2 m[N1];
+      if constexpr (KIND == kBwdMid) {
+        // A_l from the saved input of the forward pass, then the gradient
+        load_field(rw, ~0u, ar);
+        load_field(rin, gmask, x);
+        prop(ar, false, nothing);
+        prop(x, true, nothing);
+      } else {
+        load_field(rin, gmask, x);
+        load_field(rw, ~0u, ar);
+        prop(x, true, nothing);
+        prop(ar, false, nothing);
+      }
+      load_mod(m);
+      // h = conj(M_l) G_l and dphi_l += Im(conj(A_l) h)
+      static_for<0, N1>([&](auto k) {
+        const float2 h = cmulc(x[k.value], m[k.value]);
+        acc_lds[k.value * 64 + lane] += ar[k.value].x * h.y - ar[k.value].y * h.x;
+        x[k.value] = h;
+      });
+      if constexpr (KIND == kBwdMid) prop(x, true, nothing);
+    }
+    if constexpr (KIND != kBwdLast) {
+      const Rsrc rout = make_rsrc(a.out + (size_t)b * nn, (unsigned)nn * 8u);
+      static_for<0, N1>([&](auto k) { bstore_so(rout, fb, wt_soff<N, 8, FQ, k.value>(), x[k.value]); });
+    }
+  }
+  if constexpr (ACC) {
+    // one partial per lane for the tile this wave kept
+    const int vec = (rank % a.ntiles) * 8 + WT::v_of(lane);
+    const unsigned base = wt_base<N, 4, true>(WT::j_of(lane), vec, vec < a.nvec);
+    const Rsrc dp = make_rsrc(a.dphi_part + (size_t)(rank / a.ntiles) * nn, (unsigned)nn * 4u);
+    static_for<0, N1>(
+        [&](auto k) { bstore_f_so(dp, base, wt_soff<N, 4, true, k.value>(), acc_lds[k.value * 64 + lane]); });
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Helper kernels
 // ---------------------------------------------------------------------------
 
@@ -1327,9 +1532,25 @@ template <int N, int KIND, int AXIS>
 using LayerCfg = Cfg<std::conditional_t<AXIS == kRow, typename RowPlanFor<N>::type, typename PlanFor<N>::type>,
                      LayerTile<N, KIND, AXIS>::T>;
 
+// Layer kinds of a slot-ordered field run as wave tiles where the plan allows,
+// along rows: there each wave's loads cover 8 whole 64-byte runs of its rows.
+// Along columns a wave covers half of each 128-byte line and the other half
+// is fetched again by the next tile (counters: 450 against 348 MB per
+// forward layer pass at N = 200), so columns keep the workgroup tiles.
+template <int N, int KIND, int AXIS>
+constexpr bool wave_tile_kind() {
+  using PL = typename PlanFor<N>::type;
+  return AXIS == kRow && PL::N2 == 8 && std::is_same_v<PL, typename RowPlanFor<N>::type> &&
+         (KIND == kFwdMid || KIND == kBwdMid || KIND == kBwdLast);
+}
+
 template <int N, int KIND, int AXIS, bool FULL>
 hipError_t launch_fr(const PassArgs& a, hipStream_t st) {
-  if constexpr (KIND == kFwdLast || KIND == kBwdFirst) {
+  if constexpr (FULL && wave_tile_kind<N, KIND, AXIS>()) {
+    if (a.workers < 1) return hipErrorInvalidValue;
+    const dim3 grid(8 * ((a.workers + 7) / 8));
+    hipLaunchKernelGGL((wave_pass<typename PlanFor<N>::type, KIND, AXIS>), grid, dim3(64), 0, st, a);
+  } else if constexpr (KIND == kFwdLast || KIND == kBwdFirst) {
     using C = std::conditional_t<AXIS == kRow, RowCfgFor<N>, CfgFor<N>>;
     const dim3 grid(work_grid(a.ntiles, (a.batch + a.spg - 1) / a.spg));
     hipLaunchKernelGGL((detector_pass<C, KIND, AXIS, FULL>), grid, dim3(C::P), 0, st, a);
@@ -1376,10 +1597,15 @@ inline int resident_per_cu(const void* kernel, int block) {
 
 template <int N, int KIND, int AXIS, bool FULL>
 int slots_fr() {
-  using C = LayerCfg<N, KIND, AXIS>;
   static int per_cu = 0;
-  if (per_cu == 0)
-    per_cu = resident_per_cu(reinterpret_cast<const void*>(&fresnel_pass<C, KIND, AXIS, FULL>), C::P);
+  if (per_cu == 0) {
+    if constexpr (FULL && wave_tile_kind<N, KIND, AXIS>()) {
+      per_cu = resident_per_cu(reinterpret_cast<const void*>(&wave_pass<typename PlanFor<N>::type, KIND, AXIS>), 64);
+    } else {
+      using C = LayerCfg<N, KIND, AXIS>;
+      per_cu = resident_per_cu(reinterpret_cast<const void*>(&fresnel_pass<C, KIND, AXIS, FULL>), C::P);
+    }
+  }
   return per_cu * device_cus();
 }
 
@@ -1390,18 +1616,19 @@ int slots_fr_axis(Axis axis, bool full) {
 }
 
 template <int N, int KIND>
-int tile_fr_axis(Axis axis) {
-  return axis == kRow ? LayerTile<N, KIND, kRow>::T : LayerTile<N, KIND, kCol>::T;
+int tile_fr_axis(Axis axis, bool full) {
+  if (axis == kRow) return full && wave_tile_kind<N, KIND, kRow>() ? 8 : LayerTile<N, KIND, kRow>::T;
+  return full && wave_tile_kind<N, KIND, kCol>() ? 8 : LayerTile<N, KIND, kCol>::T;
 }
 
 // Vectors per workgroup of a separable pass.
 template <int N>
-int tile_fr_n(PassKind kind, Axis axis) {
+int tile_fr_n(PassKind kind, Axis axis, bool full) {
   switch (kind) {
-    case kPropOnce: return tile_fr_axis<N, kPropOnce>(axis);
-    case kFwdMid: return tile_fr_axis<N, kFwdMid>(axis);
-    case kBwdMid: return tile_fr_axis<N, kBwdMid>(axis);
-    case kBwdLast: return tile_fr_axis<N, kBwdLast>(axis);
+    case kPropOnce: return tile_fr_axis<N, kPropOnce>(axis, full);
+    case kFwdMid: return tile_fr_axis<N, kFwdMid>(axis, full);
+    case kBwdMid: return tile_fr_axis<N, kBwdMid>(axis, full);
+    case kBwdLast: return tile_fr_axis<N, kBwdLast>(axis, full);
     default: return TileT<N>::T;  // detector-plane passes
   }
 }
