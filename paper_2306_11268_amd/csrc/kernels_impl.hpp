@@ -633,7 +633,10 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
 
   const int G = (int)gridDim.x;
   const int l = (int)blockIdx.x;
-  const int rank = (l & 7) * (G >> 3) + (l >> 3);
+  // XCD-contiguous ranks let neighbouring column tiles share cache lines in
+  // one XCD's L2; row tiles read whole rows and stream faster in dispatch
+  // order (a memory-only probe of the row pattern: 6.4 against 5.8 TB/s)
+  const int rank = AXIS == kCol ? (l & 7) * (G >> 3) + (l >> 3) : l;
   if (rank >= a.workers) return;
   const int n = a.n;
   const int off = a.off;
@@ -1318,7 +1321,10 @@ __global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 
 
   const int G = (int)gridDim.x;
   const int l = (int)blockIdx.x;
-  const int rank = (l & 7) * (G >> 3) + (l >> 3);
+  // XCD-contiguous ranks let neighbouring column tiles share cache lines in
+  // one XCD's L2; row tiles read whole rows and stream faster in dispatch
+  // order (a memory-only probe of the row pattern: 6.4 against 5.8 TB/s)
+  const int rank = AXIS == kCol ? (l & 7) * (G >> 3) + (l >> 3) : l;
   if (rank >= a.workers) return;
   const int lane = (int)threadIdx.x;
   const int total = a.ntiles * a.batch;
