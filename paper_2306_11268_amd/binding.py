@@ -285,12 +285,13 @@ def lr_donn_forward(net: Network, amp, phi, saved=None, sums: bool = True, inten
     w = net.workspace(b, LR_OP_FORWARD)
     if saved is not None and saved.numel() < net.saved_size(b):
         raise ValueError("saved buffer too small")
+    k = net.detector.num
     _check(load().lr_donn_forward(
         ctypes.byref(desc), b,
         _ptr(amp, torch.float32, (b, n, n), "amp"), _ptr(phi, torch.float32, (L, n, n), "phi"),
         _ptr(saved, torch.uint8, None, "saved"),
-        _ptr(out_sums, torch.float32, None, "sums"), _ptr(out_intensity, torch.float32, None, "intensity"),
-        _ptr(out_field, torch.complex64, None, "field"),
+        _ptr(out_sums, torch.float32, (b, k), "sums"), _ptr(out_intensity, torch.float32, (b, n, n), "intensity"),
+        _ptr(out_field, torch.complex64, (b, n, n), "field"),
         _ptr(w), w.numel(), _stream(dev)), "lr_donn_forward")
     return {"sums": out_sums, "intensity": out_intensity, "field": out_field, "saved": saved}
 
@@ -307,12 +308,16 @@ def lr_donn_backward(net: Network, phi, saved, sums=None, labels=None, grad_sums
     if out_grad_phi is None:
         out_grad_phi = torch.empty((L, n, n), dtype=torch.float32, device=dev)
     loss = torch.empty((), dtype=torch.float32, device=dev) if (labels is not None and want_loss) else None
+    if saved is None or saved.numel() < net.saved_size(b):
+        raise ValueError("saved buffer missing or smaller than the forward pass of this batch fills")
+    k = net.detector.num
     w = net.workspace(b, LR_OP_BACKWARD)
     desc = _with_skip(net.c, skip, b, n)
     _check(load().lr_donn_backward(
         ctypes.byref(desc), b, _ptr(phi, torch.float32, (L, n, n), "phi"), _ptr(saved, torch.uint8, None, "saved"),
-        _ptr(sums, torch.float32, None, "sums"), _ptr(labels, torch.int32, None, "labels"),
-        _ptr(grad_sums, torch.float32, None, "grad_sums"), _ptr(grad_intensity, torch.float32, None, "grad_intensity"),
+        _ptr(sums, torch.float32, (b, k), "sums"), _ptr(labels, torch.int32, (b,), "labels"),
+        _ptr(grad_sums, torch.float32, (b, k), "grad_sums"),
+        _ptr(grad_intensity, torch.float32, (b, n, n), "grad_intensity"),
         _ptr(loss, torch.float32, None, "loss"), _ptr(out_grad_phi, torch.float32, (L, n, n), "grad_phi"),
         _ptr(w), w.numel(), _stream(dev)), "lr_donn_backward")
     return out_grad_phi, loss

@@ -10,6 +10,7 @@
 #include <cstring>
 #include <map>
 #include <mutex>
+#include <initializer_list>
 #include <string>
 #include <vector>
 
@@ -93,13 +94,36 @@ int run_timed(const std::string& name, hipStream_t st, F&& launch) {
 // ---------------------------------------------------------------------------
 bool finite_pos(double v) { return std::isfinite(v) && v > 0.0; }
 
+// Byte ranges [p, p + bytes) of two buffers overlap (empty or null ranges never do).
+bool overlaps(const void* p, size_t bytes, const void* q, size_t qbytes) {
+  if (!p || !q || bytes == 0 || qbytes == 0) return false;
+  const char* a = static_cast<const char*>(p);
+  const char* b = static_cast<const char*>(q);
+  return a < b + qbytes && b < a + bytes;
+}
+struct Span {
+  const void* p;
+  size_t bytes;
+};
+// Some output range overlaps another buffer of the call (an input or another output).
+bool outputs_alias(std::initializer_list<Span> outputs, std::initializer_list<Span> inputs) {
+  for (auto o = outputs.begin(); o != outputs.end(); ++o) {
+    for (const Span& i : inputs)
+      if (overlaps(o->p, o->bytes, i.p, i.bytes)) return true;
+    for (auto q = o + 1; q != outputs.end(); ++q)
+      if (overlaps(o->p, o->bytes, q->p, q->bytes)) return true;
+  }
+  return false;
+}
+
 int validate_detector(const lr_detector& d, int n) {
   if (d.num < 0 || d.num > LR_MAX_REGIONS) return LR_E_ARG;
   if (d.num == 0) return LR_OK;
   if (!d.y0 || !d.x0) return LR_E_NULL;
   if (d.size < 1 || d.size > n) return LR_E_ARG;
+  // (size <= n, so n - size does not overflow; y0 + size could)
   for (int k = 0; k < d.num; ++k) {
-    if (d.y0[k] < 0 || d.x0[k] < 0 || d.y0[k] + d.size > n || d.x0[k] + d.size > n) return LR_E_ARG;
+    if (d.y0[k] < 0 || d.x0[k] < 0 || d.y0[k] > n - d.size || d.x0[k] > n - d.size) return LR_E_ARG;
   }
   return LR_OK;
 }
@@ -190,6 +214,11 @@ Layout make_layout(const lr_donn* net, int batch, int op) {
   }
   L.total = off;
   return L;
+}
+
+// Bytes of the saved state (L + 1 complex64 fields of [batch][n][n]).
+size_t saved_bytes(const lr_donn* net, int batch) {
+  return static_cast<size_t>(net->num_layers + 1) * static_cast<size_t>(batch) * net->n * net->n * 8;
 }
 
 template <class T>
@@ -601,7 +630,7 @@ int64_t lr_saved_size(const lr_donn* net, int32_t batch) {
   const int r = validate_net(net, true);
   if (r != LR_OK) return -r;
   if (batch < 0) return -LR_E_SIZE;
-  return static_cast<int64_t>(net->num_layers + 1) * batch * net->n * net->n * 8;
+  return static_cast<int64_t>(saved_bytes(net, batch));
 }
 
 int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* d_out, int32_t adjoint,
@@ -610,10 +639,15 @@ int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* 
   if (batch < 0) return LR_E_SIZE;
   if (batch == 0) return LR_OK;
   if (!d_in || !d_out) return LR_E_NULL;
-  if (static_cast<const void*>(d_in) == static_cast<const void*>(d_out)) return LR_E_ALIAS;
   if (net->approx == LR_FRAUNHOFER && adjoint) return LR_E_ARG;
   Layout L;
   LR_TRY(check_work(net, batch, LR_OP_PROPAGATE, d_work, work_bytes, &L));
+  {
+    const size_t m = static_cast<size_t>(net->approx == LR_FRAUNHOFER ? net->n_fft : net->n);
+    const size_t in_bytes = static_cast<size_t>(batch) * net->n * net->n * 8;
+    if (outputs_alias({{d_out, static_cast<size_t>(batch) * m * m * 8}, {d_work, L.total}}, {{d_in, in_bytes}}))
+      return LR_E_ALIAS;
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int N = net->n_fft;
   LR_TRY(prep_tables(net, L, d_work, st));
@@ -684,10 +718,20 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   if (d_sums && net->det.num == 0) return LR_E_ARG;
   const bool accumulate = (net->flags & LR_ACCUMULATE) != 0;
   if (accumulate && d_field_out) return LR_E_ARG;  // fields of separate channels do not add
-  if (net->d_skip && static_cast<const void*>(net->d_skip) == static_cast<const void*>(d_field_out))
-    return LR_E_ALIAS;
   Layout L;
   LR_TRY(check_work(net, batch, LR_OP_FORWARD, d_work, work_bytes, &L));
+  {
+    const size_t nn4 = static_cast<size_t>(batch) * net->n * net->n * 4;
+    if (outputs_alias({{d_saved, saved_bytes(net, batch)},
+                       {d_sums, static_cast<size_t>(batch) * net->det.num * 4},
+                       {d_intensity, nn4},
+                       {d_field_out, 2 * nn4},
+                       {d_work, L.total}},
+                      {{d_amp, nn4},
+                       {d_phi, static_cast<size_t>(net->num_layers) * net->n * net->n * 4},
+                       {net->d_skip, 2 * nn4}}))
+      return LR_E_ALIAS;
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int N = net->n_fft;
   const int n = net->n;
@@ -817,6 +861,21 @@ int lr_donn_backward(const lr_donn* net, int32_t batch, const float* d_phi, cons
   }
   Layout L;
   LR_TRY(check_work(net, batch, LR_OP_BACKWARD, d_work, work_bytes, &L));
+  {
+    const size_t nn4 = static_cast<size_t>(std::max(batch, 0)) * net->n * net->n * 4;
+    const size_t bk4 = static_cast<size_t>(std::max(batch, 0)) * net->det.num * 4;
+    if (outputs_alias({{d_grad_phi, static_cast<size_t>(net->num_layers) * net->n * net->n * 4},
+                       {d_loss, 4},
+                       {d_work, L.total}},
+                      {{d_phi, static_cast<size_t>(net->num_layers) * net->n * net->n * 4},
+                       {d_saved, batch > 0 ? saved_bytes(net, batch) : 0},
+                       {d_sums, bk4},
+                       {d_labels, static_cast<size_t>(std::max(batch, 0)) * 4},
+                       {d_grad_sums, bk4},
+                       {d_grad_intensity, nn4},
+                       {net->d_skip, 2 * nn4}}))
+      return LR_E_ALIAS;
+  }
   if (batch == 0) {
     // an empty batch has a zero gradient: a fixed-order sum over no groups
     int none[LR_MAX_LAYERS] = {};
@@ -948,7 +1007,11 @@ int lr_loss(int32_t kind, const float* d_sums, const int32_t* d_labels, int32_t 
   if (!d_loss && !d_grad_sums) return LR_E_NULL;
   if (batch == 0) return LR_OK;
   if (!d_sums || !d_labels) return LR_E_NULL;
-  if (static_cast<const void*>(d_grad_sums) == static_cast<const void*>(d_sums)) return LR_E_ALIAS;
+  {
+    const size_t bk4 = static_cast<size_t>(batch) * classes * 4;
+    if (outputs_alias({{d_grad_sums, bk4}, {d_loss, 4}}, {{d_sums, bk4}, {d_labels, static_cast<size_t>(batch) * 4}}))
+      return LR_E_ALIAS;
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   return run_timed(kind == LR_LOSS_SOFTMAX_CE ? "ce_loss" : "mse_loss", st, [&] {
     return lr::launch_loss(kind, d_sums, d_labels, batch, classes, d_grad_sums, d_loss, st);
@@ -961,8 +1024,12 @@ int lr_codesign_phase(const float* d_logits, const float* d_noise, const float* 
   if (!(tau > 0.f) || !std::isfinite(tau)) return LR_E_ARG;
   if (count == 0) return LR_OK;
   if (!d_logits || !d_noise || !d_levels || !d_phi) return LR_E_NULL;
-  const void* out = d_phi;
-  if (out == d_logits || out == d_noise || out == d_levels) return LR_E_ALIAS;
+  {
+    const size_t sc = static_cast<size_t>(count) * levels * 4;
+    if (outputs_alias({{d_phi, static_cast<size_t>(count) * 4}},
+                      {{d_logits, sc}, {d_noise, sc}, {d_levels, static_cast<size_t>(levels) * 4}}))
+      return LR_E_ALIAS;
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   return run_timed("codesign", st, [&] {
     return lr::launch_codesign(d_logits, d_noise, d_levels, levels, static_cast<long long>(count), tau, hard ? 1 : 0,
@@ -976,8 +1043,14 @@ int lr_codesign_backward(const float* d_logits, const float* d_noise, const floa
   if (!(tau > 0.f) || !std::isfinite(tau)) return LR_E_ARG;
   if (count == 0) return LR_OK;
   if (!d_logits || !d_noise || !d_levels || !d_grad_phi || !d_grad_logits) return LR_E_NULL;
-  const void* out = d_grad_logits;
-  if (out == d_logits || out == d_noise || out == d_levels || out == d_grad_phi) return LR_E_ALIAS;
+  {
+    const size_t sc = static_cast<size_t>(count) * levels * 4;
+    if (outputs_alias({{d_grad_logits, sc}}, {{d_logits, sc},
+                                              {d_noise, sc},
+                                              {d_levels, static_cast<size_t>(levels) * 4},
+                                              {d_grad_phi, static_cast<size_t>(count) * 4}}))
+      return LR_E_ALIAS;
+  }
   hipStream_t st = static_cast<hipStream_t>(stream);
   return run_timed("codesign_bwd", st, [&] {
     return lr::launch_codesign(d_logits, d_noise, d_levels, levels, static_cast<long long>(count), tau, 0,
@@ -998,11 +1071,6 @@ size_t ln_work_bytes(int32_t batch, int64_t count) {
 }
 
 // [p, p + bytes) and [q, q + qbytes) overlap
-bool overlaps(const void* p, size_t bytes, const void* q, size_t qbytes) {
-  const char* a = static_cast<const char*>(p);
-  const char* b = static_cast<const char*>(q);
-  return a < b + qbytes && b < a + bytes;
-}
 }  // namespace
 
 int64_t lr_layer_norm_workspace_size(int32_t batch, int64_t count) {
@@ -1064,10 +1132,10 @@ int lr_adam_update(float* d_phi, const float* d_grad, float* d_m, float* d_v, in
     return LR_E_ARG;
   if (count == 0) return LR_OK;
   if (!d_phi || !d_grad || !d_m || !d_v) return LR_E_NULL;
-  const void* p[4] = {d_phi, d_grad, d_m, d_v};
-  for (int i = 0; i < 4; ++i)
-    for (int k = i + 1; k < 4; ++k)
-      if (p[i] == p[k]) return LR_E_ALIAS;
+  {
+    const size_t b4 = static_cast<size_t>(count) * 4;
+    if (outputs_alias({{d_phi, b4}, {d_m, b4}, {d_v, b4}}, {{d_grad, b4}})) return LR_E_ALIAS;
+  }
   const double bc1 = 1.0 - std::pow(static_cast<double>(beta1), step);
   const double bc2 = 1.0 - std::pow(static_cast<double>(beta2), step);
   if (!(bc1 > 0.0) || !(bc2 > 0.0)) return LR_E_ARG;

@@ -243,3 +243,56 @@ def test_layer_norm_stats_outside_the_workspace():
     ws = lib.lr_layer_norm_workspace_size(2, count)
     x, y, w = P(0x10000000), P(0x20000000), P(0x40000000)
     assert lib.lr_layer_norm(x, 2, count, 1e-5, y, P(0x40000000 + 8), w, ws, None) == 7
+
+
+@needs_lib
+def test_detector_origins_near_int_max_are_rejected():
+    """Region origins whose end overflows int32 must fail validation, not wrap."""
+    lib = lb.load()
+    P = ctypes.POINTER(ctypes.c_int32)
+    big = 2147483642
+    for ys, xs in (((big,), (0,)), ((0,), (big,)), ((-big,), (0,))):
+        y = (ctypes.c_int32 * 1)(*ys)
+        x = (ctypes.c_int32 * 1)(*xs)
+        det = lb.LrDetector(1, 20, ctypes.cast(y, P), ctypes.cast(x, P))
+        assert _ws(_net(det=det)) == -3
+        assert lib.lr_detector_readout(ctypes.c_void_p(0x1000), 2, 200, ctypes.byref(det), ctypes.c_void_p(0x9000000),
+                                       None) == 3
+        net = _net(det=det)
+        assert lib.lr_donn_forward(ctypes.byref(net), 2, ctypes.c_void_p(0x1000), ctypes.c_void_p(0x1000), None,
+                                   None, None, None, ctypes.c_void_p(0x40000000), 1 << 30, None) == 3
+
+
+@needs_lib
+def test_partially_overlapping_buffers_are_rejected():
+    """Outputs overlapping an input (or another output) by part of their range
+    are aliasing errors, not only equal pointers; nothing is launched."""
+    lib = lb.load()
+    P = ctypes.c_void_p
+    net = _net()
+    ref = ctypes.byref(net)
+    field = 2 * 200 * 200 * 8
+    a, w = 0x10000000, 0x40000000
+    ws = lib.lr_workspace_size(ref, 2, lb.LR_OP_PROPAGATE)
+    # propagate: output starting inside the input, or the workspace over either
+    assert lib.lr_propagate(ref, 2, P(a), P(a + field - 8), 0, P(w), ws, None) == 7
+    assert lib.lr_propagate(ref, 2, P(a), P(a + field), 0, P(a + 2 * field - 64), ws, None) == 7
+    # forward: intensity over the amplitudes, field output over the phases
+    wf = lib.lr_workspace_size(ref, 2, lb.LR_OP_FORWARD)
+    amp, phi = 0x10000000, 0x20000000
+    assert lib.lr_donn_forward(ref, 2, P(amp), P(phi), None, None, P(amp + 4096), None, P(w), wf, None) == 7
+    assert lib.lr_donn_forward(ref, 2, P(amp), P(phi), None, None, None, P(phi + 8), P(w), wf, None) == 7
+    # backward: dphi over the saved state
+    det_y = (ctypes.c_int32 * 1)(0)
+    det = lb.LrDetector(1, 20, ctypes.cast(det_y, ctypes.POINTER(ctypes.c_int32)),
+                        ctypes.cast(det_y, ctypes.POINTER(ctypes.c_int32)))
+    nd = _net(det=det)
+    wb = lib.lr_workspace_size(ctypes.byref(nd), 2, lb.LR_OP_BACKWARD)
+    saved = 0x30000000
+    gi = 0x50000000
+    assert lib.lr_donn_backward(ctypes.byref(nd), 2, P(phi), P(saved), None, None, None, P(gi), None,
+                                P(saved + 800), P(w), wb, None) == 7
+    # Adam: a moment buffer starting inside the phases
+    f = ctypes.c_float
+    assert lib.lr_adam_update(P(0x1000), P(0x9000), P(0x1000 + 16), P(0x5000), 8, 1, f(0.5), f(0.9), f(0.999),
+                              f(1e-8), None) == 7
