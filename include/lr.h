@@ -190,6 +190,23 @@ int64_t lr_saved_size(const lr_donn* net, int32_t batch);
 int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* d_out,
                  int32_t adjoint, void* d_work, size_t work_bytes, void* stream);
 
+/* lr_propagate for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same hop, with the workspace taken from a fixed array of
+ * LR_NOALLOC_SCRATCH_BYTES bytes that the library keeps in device memory on
+ * every GPU it runs on until the process ends.  The call itself allocates
+ * nothing (no hipMalloc, no events: kernel timing skips it).  Arguments,
+ * results and errors as lr_propagate; additionally LR_E_WORKSPACE when
+ * lr_workspace_size(net, batch, LR_OP_PROPAGATE) exceeds the array
+ * (lr_propagate_noalloc_limit() returns its size), checked before anything
+ * is enqueued.  All calls on one GPU share that GPU's array: calls that can
+ * overlap on one GPU (different streams or host threads without ordering)
+ * race, and the caller must order them. */
+#define LR_NOALLOC_SCRATCH_BYTES (32u << 20)
+int lr_propagate_noalloc(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* d_out, int32_t adjoint,
+                         void* stream);
+int64_t lr_propagate_noalloc_limit(void);
+
 /* Detector readout (§2.1): d_sums[b][k] = sum over region k of |d_field[b]|^2.
  * d_field: complex64 [batch][n][n]; d_sums: float32 [batch][det->num].
  * Regions must lie inside the n x n plane. */

@@ -29,7 +29,8 @@ LR_LOSS_SOFTMAX_MSE = 1
 
 EXPORTS = (
     "lr_tf_build", "lr_workspace_size", "lr_saved_size",
-    "lr_propagate", "lr_detector_readout", "lr_donn_forward", "lr_donn_backward",
+    "lr_propagate", "lr_propagate_noalloc", "lr_propagate_noalloc_limit",
+    "lr_detector_readout", "lr_donn_forward", "lr_donn_backward",
     "lr_loss", "lr_adam_update", "lr_codesign_phase", "lr_codesign_backward",
     "lr_layer_norm_workspace_size", "lr_layer_norm", "lr_layer_norm_backward",
     "lr_status_string", "lr_kernel_timing", "lr_kernel_timing_report", "lr_version",
@@ -73,6 +74,9 @@ def load() -> ctypes.CDLL:
     lib.lr_saved_size.argtypes = [POINTER(LrDonn), c_int32]
     lib.lr_saved_size.restype = c_int64
     lib.lr_propagate.argtypes = [POINTER(LrDonn), c_int32, P, P, c_int32, P, c_size_t, P]
+    lib.lr_propagate_noalloc.argtypes = [POINTER(LrDonn), c_int32, P, P, c_int32, P]
+    lib.lr_propagate_noalloc_limit.argtypes = []
+    lib.lr_propagate_noalloc_limit.restype = c_int64
     lib.lr_detector_readout.argtypes = [P, c_int32, c_int32, POINTER(LrDetector), P, P]
     lib.lr_donn_forward.argtypes = [POINTER(LrDonn), c_int32, P, P, P, P, P, P, P, c_size_t, P]
     lib.lr_donn_backward.argtypes = [POINTER(LrDonn), c_int32, P, P, P, P, P, P, P, P, P, c_size_t, P]
@@ -234,6 +238,28 @@ def lr_propagate(net: Network, field, adjoint: bool = False, out=None):
                                _ptr(out, torch.complex64, (b, m, m), "out"),
                                1 if adjoint else 0, _ptr(w), w.numel(), _stream(net.device)), "lr_propagate")
     return out
+
+
+def lr_propagate_noalloc(net: Network, field, adjoint: bool = False, out=None):
+    """lr_propagate with the library's fixed device scratch array as the
+    workspace (no allocation inside the call; batches whose workspace exceeds
+    lr_propagate_noalloc_limit() bytes are rejected).  Calls that overlap on
+    one GPU share that array: order them."""
+    torch = _torch()
+    b = int(field.shape[0])
+    m = net.n_fft if net.c.approx == LR_FRAUNHOFER else net.n
+    if out is None:
+        out = torch.empty((b, m, m), dtype=torch.complex64, device=field.device)
+    _check(load().lr_propagate_noalloc(ctypes.byref(net.c), b,
+                                       _ptr(field, torch.complex64, (b, net.n, net.n), "field"),
+                                       _ptr(out, torch.complex64, (b, m, m), "out"),
+                                       1 if adjoint else 0, _stream(net.device)), "lr_propagate_noalloc")
+    return out
+
+
+def lr_propagate_noalloc_limit() -> int:
+    """Bytes of the device scratch array lr_propagate_noalloc uses as its workspace."""
+    return int(load().lr_propagate_noalloc_limit())
 
 
 def lr_detector_readout(field, detector: Detector, out=None):

@@ -63,13 +63,17 @@ hipEvent_t take_event(TimingState& s) {
   return e;
 }
 
+// Calls that must not allocate (lr_propagate_noalloc) launch untimed: the
+// timing records create HIP events.
+thread_local bool g_untimed = false;
+
 template <class F>
 int run_timed(const std::string& name, hipStream_t st, F&& launch) {
   TimingState& s = timing();
   bool on;
   {
     std::lock_guard<std::mutex> g(s.mu);
-    on = s.on;
+    on = s.on && !g_untimed;
   }
   if (!on) return launch() == hipSuccess ? LR_OK : LR_E_HIP;
   hipEvent_t a, b;
@@ -692,6 +696,60 @@ int lr_propagate(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* 
   a.nvec = net->n;
   a.ntiles = L.ntiles_vec;
   return as_pass(N, lr::kAsRowIfft, a, st);
+}
+
+// ---------------------------------------------------------------------------
+// lr_propagate without a caller workspace: the workspace is a fixed array in
+// device memory, one per GPU (each device holds its own copy of the array
+// while the library is loaded).  In host code the array's name is not a
+// device address; its address on the current device comes from
+// hipGetSymbolAddress, taken once per device and kept.
+// ---------------------------------------------------------------------------
+namespace {
+constexpr size_t kScratchBytes = static_cast<size_t>(LR_NOALLOC_SCRATCH_BYTES);
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+int scratch_on_current_device(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return LR_E_HIP;
+  std::lock_guard<std::mutex> g(g_scratch_mu);
+  if (g_scratch_ptr[dev] == nullptr) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return LR_E_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return LR_OK;
+}
+
+struct UntimedScope {
+  bool prev;
+  UntimedScope() : prev(g_untimed) { g_untimed = true; }
+  ~UntimedScope() { g_untimed = prev; }
+};
+}  // namespace
+
+int64_t lr_propagate_noalloc_limit(void) { return static_cast<int64_t>(kScratchBytes); }
+
+int lr_propagate_noalloc(const lr_donn* net, int32_t batch, const lr_c64* d_in, lr_c64* d_out, int32_t adjoint,
+                         void* stream) {
+  LR_TRY(validate_net(net, false));
+  if (batch < 0) return LR_E_SIZE;
+  if (batch == 0) return LR_OK;
+  // the same checks as lr_propagate, before the scratch size
+  if (!d_in || !d_out) return LR_E_NULL;
+  const Layout L = make_layout(net, batch, LR_OP_PROPAGATE);
+  if (L.total > kScratchBytes) return LR_E_WORKSPACE;
+  void* work = nullptr;
+  LR_TRY(scratch_on_current_device(&work));
+  UntimedScope untimed;
+  // every part of the workspace a propagation uses is written before it is
+  // read, so nothing left by an earlier call needs clearing
+  return lr_propagate(net, batch, d_in, d_out, adjoint, work, kScratchBytes, stream);
 }
 
 int lr_detector_readout(const lr_c64* d_field, int32_t batch, int32_t n, const lr_detector* det, float* d_sums,

@@ -296,3 +296,23 @@ def test_partially_overlapping_buffers_are_rejected():
     f = ctypes.c_float
     assert lib.lr_adam_update(P(0x1000), P(0x9000), P(0x1000 + 16), P(0x5000), 8, 1, f(0.5), f(0.9), f(0.999),
                               f(1e-8), None) == 7
+
+
+@needs_lib
+def test_noalloc_propagate_limits_without_touching_the_gpu():
+    lib = lb.load()
+    P = ctypes.c_void_p
+    limit = lib.lr_propagate_noalloc_limit()
+    assert limit == 32 << 20
+    net = _net(num_layers=1)
+    ref = ctypes.byref(net)
+    # a batch whose workspace exceeds the scratch array is rejected before any launch
+    per = lib.lr_workspace_size(ref, 1, lb.LR_OP_PROPAGATE)
+    big = limit // (200 * 200 * 8) + 2
+    assert lib.lr_workspace_size(ref, big, lb.LR_OP_PROPAGATE) > limit > per
+    assert lib.lr_propagate_noalloc(ref, big, P(0x1000), P(0x40000000), 0, None) == 6
+    assert lib.lr_propagate_noalloc(ref, 2, None, P(0x40000000), 0, None) == 1
+    assert lib.lr_propagate_noalloc(ref, -1, P(0x1000), P(0x40000000), 0, None) == 2
+    assert lib.lr_propagate_noalloc(ref, 0, None, None, 0, None) == 0
+    bad = _net(d_H=ctypes.c_void_p(0))
+    assert lib.lr_propagate_noalloc(ctypes.byref(bad), 2, P(0x1000), P(0x40000000), 0, None) == 1
