@@ -4,8 +4,7 @@
 
 Compiles the HIP sources with hipcc, the pass kernels once per supported FFT
 size (csrc/kern_size.hip with -DLR_FFT_N=<size>), all translation units in
-parallel, and links paper_2306_11268_amd/liblr.so; also builds the standalone
-memory-ceiling probe paper_2306_11268_amd/membw_probe.  Packed fp32 VALU
+parallel, and links paper_2306_11268_amd/liblr.so.  Packed fp32 VALU
 instructions are disabled for all device code.
 """
 
@@ -21,8 +20,6 @@ from concurrent.futures import ThreadPoolExecutor
 PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "liblr.so")
-# standalone measurement program (practical HBM ceiling of the passes' traffic mixes)
-PROBE = os.path.join(PKG, "membw_probe")
 BUILD_DIR = os.path.join(PKG, "_build")
 FFT_SIZES = (64, 100, 128, 200, 256, 350, 400, 500, 512, 1000, 1024)
 # (source, object name, extra flags)
@@ -90,10 +87,6 @@ def build(verbose: bool = True) -> str:
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr[-8000:]}")
     os.replace(tmp, LIB)
-    r = subprocess.run([hipcc(), *[f for f in COMMON if f != "-fPIC"], os.path.join(CSRC, "membw_probe.hip"),
-                        "-o", PROBE], capture_output=True, text=True)
-    if r.returncode != 0:
-        raise RuntimeError(f"hipcc failed for membw_probe.hip:\n{r.stderr[-8000:]}")
     if verbose:
         print(f"built {LIB} in {time.time() - t0:.1f}s")
     return LIB
