@@ -562,6 +562,31 @@ def codesign_limits():
     return max(e1, e2, e3, e4)
 
 
+def codesign_hard_near_ties():
+    """The hard choice is the device's float32 decision (reading R10): scores
+    that differ below float32 resolution tie, and the first level wins.  The
+    expected levels are worked out by hand from float32 rounding:
+      - logits (1, 1), noise (0, 2^-30): 1 + 2^-30 rounds to 1 in float32 (ulp
+        2^-23), so the scores tie and level 0 wins, where the float64 sums
+        would pick level 1;
+      - logits (1, 1), noise (0, 2^-22): 1 + 2^-22 is a float32 number, level 1;
+      - logits (0.5, 0.5, 0.5), noise (0, 0, 0): an exact three-way tie, level 0;
+      - logits (-3, 2, 2 + 2^-21), noise (0, 0, 0): level 2 by one float32 step.
+    Returns the number of wrong choices."""
+    levels = np.array([0.25, 1.5, 2.75])
+    cases = [
+        (np.array([1.0, 1.0, -9.0]), np.array([0.0, 2.0 ** -30, 0.0]), 0),
+        (np.array([1.0, 1.0, -9.0]), np.array([0.0, 2.0 ** -22, 0.0]), 1),
+        (np.array([0.5, 0.5, 0.5]), np.zeros(3), 0),
+        (np.array([-3.0, 2.0, 2.0 + 2.0 ** -21]), np.zeros(3), 2),
+    ]
+    wrong = 0
+    for logits, noise, k in cases:
+        phi, _ = od.codesign_phase(logits, noise, levels, 1.0, hard=True)
+        wrong += int(float(phi) != levels[k])
+    return wrong
+
+
 def codesign_grad_fd(tau=0.7):
     """Central finite differences of L = sum c * phi against codesign_backward."""
     logits, noise, levels = _codesign_case(K=6, shape=(2, 3))

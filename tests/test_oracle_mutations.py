@@ -199,6 +199,23 @@ def _codesign_no_temperature(logits, noise, levels, tau, hard=False):
     return _orig["codesign_phase"](logits, noise, levels, 1.0, hard)
 
 
+def _codesign_hard_in_float64(logits, noise, levels, tau, hard=False):
+    phi, w = _orig["codesign_phase"](logits, noise, levels, tau, False)
+    if hard:
+        s = np.asarray(logits, np.float64) + np.asarray(noise, np.float64)
+        phi = np.asarray(levels, np.float64)[np.argmax(s, axis=-1)]
+    return phi, w
+
+
+def _codesign_hard_last_on_ties(logits, noise, levels, tau, hard=False):
+    phi, w = _orig["codesign_phase"](logits, noise, levels, tau, False)
+    if hard:
+        s = (np.asarray(logits, np.float32) + np.asarray(noise, np.float32))[..., ::-1]
+        k = s.shape[-1] - 1 - np.argmax(s, axis=-1)
+        phi = np.asarray(levels, np.float64)[k]
+    return phi, w
+
+
 def _codesign_backward_no_centering(w, levels, tau, grad_phi):
     lv = np.asarray(levels, np.float64)
     return w * lv * (np.asarray(grad_phi, np.float64)[..., None] / tau)
@@ -265,6 +282,9 @@ MUTANTS = [
     ("multichannel_grad_split", "multichannel_backward", _multichannel_grad_split,
      lambda: c.multichannel_grad_fd() > 1e-3),
     ("codesign_no_temperature", "codesign_phase", _codesign_no_temperature, lambda: c.codesign_limits() > 1e-3),
+    ("codesign_hard_float64", "codesign_phase", _codesign_hard_in_float64, lambda: c.codesign_hard_near_ties() > 0),
+    ("codesign_hard_last_on_ties", "codesign_phase", _codesign_hard_last_on_ties,
+     lambda: c.codesign_hard_near_ties() > 0),
     ("codesign_grad_not_centred", "codesign_backward", _codesign_backward_no_centering,
      lambda: c.codesign_grad_fd() > 1e-3),
     ("adam_no_bias_correction", "adam_update", _adam_no_bias_correction, lambda: c.adam_first_step() > 1e-3),

@@ -173,6 +173,10 @@ def test_codesign_limits_and_shift_invariance():
     assert c.codesign_limits() < 1e-9
 
 
+def test_codesign_hard_choice_on_float32_near_ties():
+    assert c.codesign_hard_near_ties() == 0
+
+
 def test_codesign_gradient_by_finite_differences():
     assert c.codesign_grad_fd() < 1e-8
 
