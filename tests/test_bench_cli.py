@@ -42,3 +42,25 @@ def test_traffic_reported_only_for_matching_sources(tmp_path, monkeypatch):
     doc["source_digest"] = "0" * 16
     (prof / f"fresnel_passes__{name}__traffic.json").write_text(json.dumps(doc))
     assert bench.recorded_traffic(name, "k") is None
+
+
+def test_step_byte_models():
+    """Per-sample step bytes: the method's one-pass bound (40 L - 10.4) n^2 at
+    the 4-3-3 layout, and this path's passes counted by hand for L = 5 at
+    200 x 200 with 60 covered rows."""
+    from paper_2306_11268_amd import workloads as wl
+
+    w = wl.WORKLOADS[3]
+
+    class Det:
+        num = len(w.detector.y0)
+        size = w.detector.size
+        y0 = w.detector.y0
+        x0 = w.detector.x0
+
+    one_pass, path = bench.step_bytes_per_sample(w, Det)
+    nn = 200 * 200
+    assert abs(one_pass - 189.6 * nn) < 1e-6 * nn
+    # prop 12, five forward layers 80, detector read 2.4, seed 4.8, layer 5 adjoint 2.4 + 16,
+    # layers 4..2 adjoint 72, layer 1 adjoint 16 (units of n^2)
+    assert abs(path - (12 + 80 + 2.4 + 4.8 + 18.4 + 72 + 16) * nn) < 1e-6 * nn
