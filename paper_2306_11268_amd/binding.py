@@ -66,6 +66,9 @@ def load() -> ctypes.CDLL:
         return _lib
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is not built; run paper_2306_11268_amd.build.build() first")
+    # torch first: its HIP runtime is then the one the library binds to, so
+    # device pointers and streams from torch are valid in the library's calls
+    _torch()
     lib = ctypes.CDLL(LIB_PATH)
     P = c_void_p
     lib.lr_tf_build.argtypes = [c_double, c_double, c_double, c_int32, c_int32, P, P]

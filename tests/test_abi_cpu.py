@@ -316,3 +316,19 @@ def test_noalloc_propagate_limits_without_touching_the_gpu():
     assert lib.lr_propagate_noalloc(ref, 0, None, None, 0, None) == 0
     bad = _net(d_H=ctypes.c_void_p(0))
     assert lib.lr_propagate_noalloc(ctypes.byref(bad), 2, P(0x1000), P(0x40000000), 0, None) == 1
+
+
+@needs_lib
+def test_binding_shares_torchs_hip_runtime():
+    """Loading the library through the binding maps one HIP runtime, torch's:
+    loaded first on its own, the library would bind a second copy from the
+    ROCm install, and torch's device pointers and streams would be foreign to
+    it."""
+    import subprocess
+    import sys
+    code = ("import paper_2306_11268_amd.binding as lb; lb.load(); "
+            "m = open('/proc/self/maps').read(); "
+            "print(len({l.split()[-1] for l in m.splitlines() if 'libamdhip64' in l}))")
+    r = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, cwd=ROOT, timeout=300)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert r.stdout.strip().splitlines()[-1] == "1"
