@@ -1315,7 +1315,10 @@ __global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 
   constexpr bool ACC = (KIND == kBwdMid || KIND == kBwdLast);
   constexpr bool FQ = AXIS == kCol;  // field arrays q-major along this pass
   static_assert(KIND == kFwdMid || ACC, "wave tiles run the layer kinds");
-  __shared__ float2 tab[N];
+  // chirp entries of B-item k1 at 9*k1 + k2: the 8 B-items a wave reads at
+  // once then start in 8 different bank pairs (a pitch of 8 put two of them
+  // on each pair)
+  __shared__ float2 tab[9 * N1];
   __shared__ float2 xch[WT::XCH];
   __shared__ float acc_lds[ACC ? N1 * 64 : 1];  // per-lane dphi accumulators
 
@@ -1330,8 +1333,8 @@ __global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 
   const int total = a.ntiles * a.batch;
   const size_t nn = (size_t)N * N;
 
-  // chirp in B-item order: entry 8*k1 + k2 is frequency freq(k1, k2)
-  for (int i = lane; i < N; i += 64) tab[i] = a.tab[PL::freq(i >> 3, i & 7)];
+  // chirp in B-item order: entry 9*k1 + k2 is frequency freq(k1, k2)
+  for (int i = lane; i < N; i += 64) tab[i + (i >> 3)] = a.tab[PL::freq(i >> 3, i & 7)];
   if constexpr (ACC) {
     static_for<0, N1>([&](auto k) { acc_lds[k.value * 64 + lane] = 0.f; });
   }
@@ -1368,7 +1371,7 @@ __global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 
           static_for<1, 8>([&](auto jp) { y[jp.value] = cmul(y[jp.value], root_at<N>((unsigned)(k1 * jp.value))); });
         }
         Dft<8, -1>::run(y);
-        const float2* tk = tab + 8 * k1;
+        const float2* tk = tab + 9 * k1;
         if (cj) {
           static_for<0, 8>([&](auto k2) { y[k2.value] = cmulc(y[k2.value], tk[k2.value]); });
         } else {

@@ -93,3 +93,25 @@ def test_training_step_every_size(lrb, m, layers):
     grad, _ = lrb.lr_donn_backward(net, dev(phi), saved, grad_sums=dev(gs))
     ref_grad = od.donn_backward(ref, phi, h, 0.95, odet, grad_sums=gs)
     assert rel(host(grad), ref_grad) < TOL_GRAD
+
+
+@pytest.mark.parametrize("m,b", [(100, 5), (200, 7), (200, 9)])
+def test_forward_ragged_column_tiles_full_map(lrb, m, b):
+    """Full-grid forward passes whose column tiles end ragged (100 = 6*16 + 4
+    and 200 = 6*32 + 8 columns) at odd batch sizes: every output pixel of
+    every sample is checked through the full intensity map, with two layers
+    so that a column layer pass feeds a row layer pass."""
+    det = wl.layout_grid(m, 4, max(2, m // 10))
+    w = wl.Workload(93, "test", 532e-9, 36e-6, 0.3, od.FRESNEL, m, m, 2, b, "forward", det, "sums", "uniform")
+    net = lrb.Network(w.wavelength, w.pixel_pitch, w.distance, w.approx, m, m, 2, 1.0,
+                      lrb.Detector(det.size, det.y0, det.x0))
+    amp = wl.amplitudes(w, b)
+    phi = wl.phases(w)
+    out = lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True, intensity=True)
+    h = od.transfer_function(w.wavelength, w.pixel_pitch, w.distance, w.approx, m)
+    odet = od.Detector(det.size, tuple(det.y0), tuple(det.x0))
+    ref = od.donn_forward(amp, phi, h, 1.0, odet)
+    got = host(out["intensity"])
+    for s in range(b):
+        assert rel(got[s], ref["intensity"][s]) < TOL_FIELD
+    assert rel(host(out["sums"]), ref["sums"]) < TOL_FIELD
