@@ -80,6 +80,28 @@ def recorded_traffic(workload: str, kernel: str):
     return doc["kernels"][kernel]["hbm_bytes_per_dispatch"]
 
 
+# Vector-ALU issue ceiling of the chip without packed FP32 instructions: 256
+# CUs x 4 SIMDs, one wave64 FP32 instruction per SIMD every 4 cycles (16
+# lanes per cycle) at the 2.4 GHz peak engine clock, in wave instructions/s.
+VALU_PEAK_WAVE_INSTR_PER_S = 256 * 4 * 2.4e9 / 4
+
+
+def recorded_valu(workload: str, kernel: str):
+    """Wave-level VALU instructions per launch of `kernel` (SQ_INSTS_VALU) from
+    the committed counter summary of this workload, or None when there is none
+    or the device sources have changed since the counters were taken."""
+    from paper_2306_11268_amd.build import source_digest
+
+    path = os.path.join(ROOT, "profiles", f"fresnel_passes__{workload}__valu.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        doc = json.load(fh)
+    if doc.get("source_digest") != source_digest() or kernel not in doc.get("kernels", {}):
+        return None
+    return doc["kernels"][kernel]["valu_instr_per_dispatch"]
+
+
 def algorithmic_bytes_per_sample(kind: str, n: int) -> float:
     """Bytes one sample must move through HBM in one launch of each kernel kind.
 
@@ -326,6 +348,19 @@ def main():
                 "avg_launch_us": round(avg_s * 1e6, 2), "algorithmic_bytes_per_launch": int(bytes_launch),
                 "traffic_unit": "HBM bytes per launch (FETCH_SIZE, WRITE_SIZE scaled by a copy calibration)",
                 "traffic_gbps": round(traffic / avg_s / 1e9, 1) if traffic else None}
+    # what actually bounds the layer passes: vector-ALU issue (counted
+    # instructions of the same kernel over its measured launch time)
+    valu = None
+    if kind is not None:
+        instr = recorded_valu(w.name, dom) if batch == w.batch else None
+        if instr:
+            rate = instr / avg_s
+            valu = {"kernel": dom, "instr_per_launch": int(instr), "achieved": round(rate / 1e9, 1),
+                    "peak": round(VALU_PEAK_WAVE_INSTR_PER_S / 1e9, 1), "unit": "G wave instructions/s",
+                    "frac": round(rate / VALU_PEAK_WAVE_INSTR_PER_S, 4),
+                    "floor_us": round(instr / VALU_PEAK_WAVE_INSTR_PER_S * 1e6, 1),
+                    "peak_basis": "256 CUs x 4 SIMDs x 2.4 GHz / 4 cycles per wave64 FP32 instruction "
+                                  "(no packed FP32)"}
 
     nn = w.n * w.n
     step_one_pass, step_path = step_bytes_per_sample(w, det)
@@ -348,6 +383,7 @@ def main():
                    "wavelength_m": w.wavelength, "pixel_pitch_m": w.pixel_pitch, "distance_m": w.distance,
                    "loss": "softmax_cross_entropy", "detector_regions": det.num},
         "roofline": roof,
+        "valu_issue": valu,
         "fields_per_s": round(value * (2 * w.layers + 1), 1),
         # whole-step GB/s under two byte counts: the one-pass lower bound of the
         # method and the bytes this path's passes move by design

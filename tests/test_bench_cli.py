@@ -44,6 +44,24 @@ def test_traffic_reported_only_for_matching_sources(tmp_path, monkeypatch):
     assert bench.recorded_traffic(name, "k") is None
 
 
+def test_valu_counts_reported_only_for_matching_sources(tmp_path, monkeypatch):
+    from paper_2306_11268_amd import build as lb
+
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    name = "wl"
+    doc = {"source_digest": lb.source_digest(), "kernels": {"k": {"valu_instr_per_dispatch": 4.5e7}}}
+    (prof / f"fresnel_passes__{name}__valu.json").write_text(json.dumps(doc))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.recorded_valu(name, "k") == 4.5e7
+    assert bench.recorded_valu(name, "other") is None
+    doc["source_digest"] = "0" * 16
+    (prof / f"fresnel_passes__{name}__valu.json").write_text(json.dumps(doc))
+    assert bench.recorded_valu(name, "k") is None
+    # 1024 SIMDs, one wave64 instruction per 4 cycles at 2.4 GHz
+    assert bench.VALU_PEAK_WAVE_INSTR_PER_S == 614.4e9
+
+
 def test_step_byte_models():
     """Per-sample step bytes: the method's one-pass bound (40 L - 10.4) n^2 at
     the 4-3-3 layout, and this path's passes counted by hand for L = 5 at
