@@ -41,6 +41,9 @@ def parse():
                     help="grid size of a runtime-study variant of the workload (unpadded n x n)")
     ap.add_argument("--layers", type=int, default=None, help="depth of a runtime-study variant")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--layer-passes", action="store_true",
+                    help="forward workloads: one pass per layer even where the whole-field kernel applies "
+                         "(Fresnel, n = n_fft <= 128, sums only)")
     ap.add_argument("--graph", action="store_true",
                     help="record the step once as a HIP graph and time its replays (measured slower than "
                          "launching the kernels one by one on this stack, so not the default)")
@@ -206,7 +209,7 @@ def other_workload(w, batch, args):
 
     def step():
         if det is not None and not train:
-            lb.lr_donn_forward(net, amp, phi, sums=True)
+            lb.lr_donn_forward(net, amp, phi, sums=True, layer_passes=args.layer_passes)
         else:
             lb.lr_donn_forward(net, amp, phi, saved=saved, sums=False, intensity=True)
         if train:
@@ -242,7 +245,8 @@ def other_workload(w, batch, args):
         "dtype": "f32",
         "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "n_fft": w.n_fft, "layers": w.layers, "batch": batch,
-                   "approx": "fresnel" if w.approx == 0 else "angular_spectrum", "kind": w.kind},
+                   "approx": "fresnel" if w.approx == 0 else "angular_spectrum", "kind": w.kind,
+                   "layer_passes": bool(args.layer_passes)},
         "kernels": {k: {"count": v["count"], "avg_us": 1e3 * v["ms"] / v["count"], "total_ms": v["ms"]}
                     for k, v in kt.items()},
     }))

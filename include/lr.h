@@ -113,7 +113,7 @@ typedef struct lr_donn {
   const lr_c64* d_H;    /* device [n_fft][n_fft], written by lr_tf_build for the same
                            wavelength / pixel_pitch / distance / approx / n_fft.
                            The Fresnel path relies on its separability. */
-  int32_t flags;        /* 0 or LR_ACCUMULATE */
+  int32_t flags;        /* 0, or LR_ACCUMULATE and / or LR_LAYER_PASSES */
   const lr_c64* d_skip; /* NULL, or device [batch][n][n]: a field added to the
                            detector-plane field before the intensity, the sums,
                            the field output or the backward seed are formed.
@@ -136,6 +136,16 @@ typedef struct lr_donn {
  * same d_grad_sums: the merged sums are the sum of the channels' sums, so
  * every channel receives the whole dL/dS. */
 #define LR_ACCUMULATE 1
+
+/* lr_donn.flags: lr_donn_forward runs one pass per layer even where it would
+ * otherwise keep the whole field of a sample on chip.  Without it, a forward
+ * call on the Fresnel path with n == n_fft in {64, 100, 128} (the field fits
+ * in one compute unit's shared memory), region sums as the only output, no
+ * saved state and no skip field runs every hop and modulation of a sample in
+ * one workgroup and moves only the amplitudes and the sums through memory.
+ * Both paths compute the same sums (to rounding); the flag exists to compare
+ * them. */
+#define LR_LAYER_PASSES 2
 
 /* Transfer function of one hop (§3.1.1, Eqs. (fresnel), (sommerfeld), (r01),
  * (forward_diff), (fraunhofer)).

@@ -134,7 +134,7 @@ int validate_detector(const lr_detector& d, int n) {
 
 int validate_net(const lr_donn* net, bool need_layers) {
   if (!net) return LR_E_NULL;
-  if (net->flags & ~LR_ACCUMULATE) return LR_E_ARG;
+  if (net->flags & ~(LR_ACCUMULATE | LR_LAYER_PASSES)) return LR_E_ARG;
   if (!finite_pos(net->wavelength) || !finite_pos(net->pixel_pitch) || !std::isfinite(net->distance))
     return LR_E_ARG;
   if (net->approx < LR_FRESNEL || net->approx > LR_FRAUNHOFER) return LR_E_APPROX;
@@ -806,7 +806,28 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   a.full = slot_ordered(net) ? 1 : 0;
   const int tile_t = lr::tile_shape(N, 0).T;
   int sum_tiles = L.ntiles_vec;  // tiles that wrote partial detector sums
-  if (net->approx == LR_FRESNEL) {
+  const bool whole_field = net->approx == LR_FRESNEL && n == N && lr::field_forward_supported(N) && !saved &&
+                           d_sums && !d_intensity && !d_field_out && !net->d_skip &&
+                           !(net->flags & LR_LAYER_PASSES);
+  if (whole_field) {
+    // every hop of a sample in one workgroup, the field in shared memory
+    lr::FieldArgs fa;
+    std::memset(&fa, 0, sizeof fa);
+    fa.amp = d_amp;
+    fa.mod = ws_mod;
+    for (int l = 1; l <= Lyr; ++l)
+      if (layer_transposed(net, l)) fa.mod_t |= 1ull << (l - 1);
+    fa.layers = Lyr;
+    fa.chirp_x = at<float2>(d_work, L.chirp_x);
+    fa.chirp_y = at<float2>(d_work, L.chirp_y);
+    fa.reg = host_regions(net->det);
+    fa.sums_part = at<float>(d_work, L.sums_part);
+    fa.batch = batch;
+    char name[48];
+    std::snprintf(name, sizeof name, "field_forward_N%d", N);
+    LR_TRY(run_timed(name, st, [&] { return lr::launch_field_forward(N, fa, st); }));
+    sum_tiles = 1;
+  } else if (net->approx == LR_FRESNEL) {
     a.nvec = n;
     a.ntiles = L.ntiles_vec;
     auto chirp = [&](Axis ax) { return at<float2>(d_work, ax == lr::kRow ? L.chirp_x : L.chirp_y); };

@@ -14,4 +14,5 @@ template hipError_t launch_as_n<LR_FFT_N>(AsPassKind, const PassArgs&, hipStream
 template hipError_t prep_as_n<LR_FFT_N>(const float2*, float2*, float, int, hipStream_t);
 template TileShape shape_n<LR_FFT_N>();
 template SlotMap slot_map_n<LR_FFT_N>();
+template hipError_t launch_field_fwd_n<LR_FFT_N>(const FieldArgs&, hipStream_t);
 }  // namespace lr

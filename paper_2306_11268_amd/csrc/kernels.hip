@@ -14,6 +14,7 @@ template <int N> hipError_t launch_as_n(AsPassKind, const PassArgs&, hipStream_t
 template <int N> hipError_t prep_as_n(const float2*, float2*, float, int, hipStream_t);
 template <int N> TileShape shape_n();
 template <int N> SlotMap slot_map_n();
+template <int N> hipError_t launch_field_fwd_n(const FieldArgs&, hipStream_t);
 
 // ---------------------------------------------------------------------------
 // Helper kernels
@@ -455,6 +456,17 @@ SlotMap slot_map(int N) {
     case 1000: return slot_map_n<1000>();
     case 1024: return slot_map_n<1024>();
     default: return SlotMap{0, 0, 0};
+  }
+}
+
+bool field_forward_supported(int N) { return N == 64 || N == 100 || N == 128; }
+
+hipError_t launch_field_forward(int N, const FieldArgs& a, hipStream_t st) {
+  switch (N) {
+    case 64: return launch_field_fwd_n<64>(a, st);
+    case 100: return launch_field_fwd_n<100>(a, st);
+    case 128: return launch_field_fwd_n<128>(a, st);
+    default: return hipErrorInvalidValue;
   }
 }
 

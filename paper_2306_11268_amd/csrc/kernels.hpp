@@ -136,6 +136,24 @@ struct Regions {
 };
 
 
+// Whole-field forward (field_forward_kernel): one workgroup per sample holds
+// the N x N field in shared memory through every layer, for the grids whose
+// field fits there (N = 64, 100, 128, full aperture).  Fresnel path, region
+// sums only: partials [B][K] for launch_finish_sums with one tile.
+struct FieldArgs {
+  const float* amp;            // [B][N][N] natural amplitudes
+  const float2* mod;           // [L][N][N] gamma*exp(j*phi_l), slot order on both axes
+  unsigned long long mod_t;    // bit l-1 set: layer l's table is stored [x][y]
+  int layers;
+  const float2* chirp_x;       // separable chirps, natural frequency order, 1/N folded in
+  const float2* chirp_y;
+  Regions reg;                 // region corners (natural coordinates)
+  float* sums_part;            // [B][K]
+  int batch;
+};
+bool field_forward_supported(int N);
+hipError_t launch_field_forward(int N, const FieldArgs& a, hipStream_t st);
+
 bool fft_size_supported(int N);
 TileShape tile_shape(int N, int axis);
 

@@ -1473,6 +1473,156 @@ __global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 
 }
 
 // ---------------------------------------------------------------------------
+// Whole-field forward for grids whose field fits in one CU's shared memory
+// (N <= 128: 132 KB at N = 128).  One workgroup per sample reads the
+// amplitude once, runs every hop and modulation of Eq. (forward_diff) and
+// (phase_mod_matrix) on the resident field, and writes only the region sums
+// (§2.1), so no field crosses HBM between layers.
+//
+// The field is held in slot order on both axes (plan.hpp), f[sy][sx] with
+// pitch N + 1.  A hop is the separable 1-D propagation along x for every row,
+// then along y for every column: thread (v, j) (v = tid mod N) owns A-item j
+// of vector v, and the B-items k1 = j, j + N2, ... of that vector, as in the
+// tile passes but with all N vectors of the field in one tile; along x the
+// vector is a row (f[v][slot]), along y a column (f[slot][v]).  Consecutive
+// lanes take consecutive vectors, so with the odd pitch every shared-memory
+// access of a wave falls in distinct banks along both axes.
+// ---------------------------------------------------------------------------
+template <class PL>
+struct WholeCfg {
+  using Plan = PL;
+  static constexpr int N = PL::N;
+  static constexpr int N1 = PL::N1;
+  static constexpr int N2 = PL::N2;
+  static constexpr int P = N * N2;  // threads
+  static constexpr int TP = N + 1;  // pitch of the field in shared memory
+};
+
+template <class PL>
+__global__ void __launch_bounds__(PL::N * PL::N2) field_forward_kernel(FieldArgs a) {
+  using C = WholeCfg<PL>;
+  constexpr int N = C::N;
+  constexpr int N1 = C::N1;
+  constexpr int N2 = C::N2;
+  constexpr int P = C::P;
+  constexpr int TP = C::TP;
+  __shared__ float2 f[N * TP];
+  __shared__ float2 tx[N];  // chirps in B-item order: entry N2*k1 + k2 is frequency freq(k1, k2)
+  __shared__ float2 ty[N];
+
+  const int b = (int)blockIdx.x;
+  const int tid = (int)threadIdx.x;
+  const int v = tid % N;
+  const int j = tid / N;
+  const size_t nn = (size_t)N * N;
+
+  for (int i = tid; i < N; i += P) {
+    const int fr = PL::freq(i / N2, i % N2);
+    tx[i] = a.chirp_x[fr];
+    ty[i] = a.chirp_y[fr];
+  }
+  // amplitudes (natural, zero phase) into slot order: stored (sy, sx) holds
+  // natural pixel (pos_of_slot(sy), pos_of_slot(sx)); consecutive threads take
+  // consecutive natural x
+  {
+    const float* __restrict__ amp = a.amp + (size_t)b * nn;
+    for (int e = tid; e < N * N; e += P) {
+      const int y = e / N;
+      const int x = e - y * N;
+      f[PL::slot_of_pos(y) * TP + PL::slot_of_pos(x)] = c2(amp[e], 0.f);
+    }
+  }
+  __syncthreads();
+
+  // 1-D propagation of every vector along one axis, in place
+  auto prop = [&](auto axis_c, const float2* tab) {
+    constexpr bool ROWS = decltype(axis_c)::value == kRow;
+    auto at = [&](int vec, int slot) -> float2& { return ROWS ? f[vec * TP + slot] : f[slot * TP + vec]; };
+    float2 x[N1];
+    static_for<0, N1>([&](auto k) { x[k.value] = at(v, j + N2 * k.value); });
+    Dft<N1, -1>::run(x);
+    static_for<0, N1>([&](auto k) { at(v, j + N2 * k.value) = x[k.value]; });
+    __syncthreads();
+    for (int k1 = j; k1 < N1; k1 += N2) {
+      float2 y[N2];
+      static_for<0, N2>([&](auto q) { y[q.value] = at(v, N2 * k1 + q.value); });
+      b_forward<C>(k1, y);
+      static_for<0, N2>([&](auto q) { y[q.value] = cmul(y[q.value], tab[N2 * k1 + q.value]); });
+      b_inverse<C>(k1, y);
+      static_for<0, N2>([&](auto q) { at(v, N2 * k1 + q.value) = y[q.value]; });
+    }
+    __syncthreads();
+    static_for<0, N1>([&](auto k) { x[k.value] = at(v, j + N2 * k.value); });
+    Dft<N1, 1>::run(x);
+    static_for<0, N1>([&](auto k) { at(v, j + N2 * k.value) = x[k.value]; });
+    __syncthreads();
+  };
+
+  for (int hop = 1; hop <= a.layers + 1; ++hop) {
+    prop(std::integral_constant<int, kRow>{}, tx);
+    prop(std::integral_constant<int, kCol>{}, ty);
+    if (hop <= a.layers) {
+      // U_l = gamma exp(j phi_l) A_l; the table is in slot order, [y][x] or
+      // [x][y]: consecutive threads take consecutive positions of its rows
+      const float2* __restrict__ m = a.mod + (size_t)(hop - 1) * nn;
+      const bool tr = (a.mod_t >> (hop - 1)) & 1ull;
+      for (int e = tid; e < N * N; e += P) {
+        const int r = e / N;
+        const int c = e - r * N;
+        float2& u = tr ? f[c * TP + r] : f[r * TP + c];
+        u = cmul(u, m[e]);
+      }
+      __syncthreads();
+    }
+  }
+
+  // S_k = sum of |U_D|^2 over region k: wave w sums regions w, w + waves, ...
+  // over natural pixels in a fixed order (lane stride 64, then a fixed
+  // butterfly), so the sums are reproducible
+  constexpr int NW = P / 64;  // whole waves (at N = 100 the last wave is partial and sums nothing)
+  const int wv = tid >> 6;
+  const int lane = tid & 63;
+  const int side = a.reg.s;
+  for (int k = wv; wv < NW && k < a.reg.K; k += NW) {
+    const int y0 = a.reg.y0[k];
+    const int x0 = a.reg.x0[k];
+    float acc = 0.f;
+    for (int e = lane; e < side * side; e += 64) {
+      const int dy = e / side;
+      const int y = y0 + dy;
+      const int x = x0 + (e - dy * side);
+      const float2 u = f[PL::slot_of_pos(y) * TP + PL::slot_of_pos(x)];
+      acc = fmaf(u.x, u.x, fmaf(u.y, u.y, acc));
+    }
+    for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
+    if (lane == 0) a.sums_part[(size_t)b * a.reg.K + k] = acc;
+  }
+}
+
+template <int N>
+constexpr bool whole_field_size() {
+  return N == 64 || N == 100 || N == 128;
+}
+
+template <int N>
+hipError_t launch_field_fwd_n(const FieldArgs& a, hipStream_t st) {
+  if constexpr (whole_field_size<N>()) {
+    using PL = typename PlanFor<N>::type;
+    static_assert(std::is_same_v<PL, typename RowPlanFor<N>::type>, "one plan on both axes");
+    if (a.batch < 1 || a.layers < 0 || a.layers > 64 || a.reg.K < 1 || a.reg.K > kMaxRegions) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((field_forward_kernel<PL>), dim3(a.batch), dim3(PL::N * PL::N2), 0, st, a);
+    return hipGetLastError();
+  } else {
+    return hipErrorInvalidValue;
+  }
+}
+
+template <int N>
+constexpr bool field_fwd_supported_n() {
+  return whole_field_size<N>();
+}
+
+// ---------------------------------------------------------------------------
 // Helper kernels
 // ---------------------------------------------------------------------------
 

@@ -116,8 +116,11 @@ def test_entry_points_reject_bad_arguments_without_touching_the_gpu():
     assert _ws(_net(approx=5), 4, 0) == -4
     # flags: unknown bits; accumulating outputs cannot include the field
     bad = _net()
-    bad.flags = 2
+    bad.flags = 4
     assert _ws(bad, 4, 1) == -3
+    ok = _net()
+    ok.flags = 3  # LR_ACCUMULATE | LR_LAYER_PASSES
+    assert _ws(ok, 4, 1) > 0
     acc = _net(det=lb.LrDetector(0, 1, None, None))
     acc.flags = 1
     assert lib.lr_donn_forward(ctypes.byref(acc), 2, dummy, dummy, None, None, None, P(0x3000), dummy, 1 << 30,
