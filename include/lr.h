@@ -140,11 +140,11 @@ typedef struct lr_donn {
 /* lr_donn.flags: lr_donn_forward runs one pass per layer even where it would
  * otherwise keep the whole field of a sample on chip.  Without it, a forward
  * call on the Fresnel path with n == n_fft in {64, 100, 128} (the field fits
- * in one compute unit's shared memory), region sums as the only output, no
- * saved state and no skip field runs every hop and modulation of a sample in
- * one workgroup and moves only the amplitudes and the sums through memory.
- * Both paths compute the same sums (to rounding); the flag exists to compare
- * them. */
+ * in one compute unit's shared memory), no saved state and no skip field
+ * runs every hop and modulation of a sample in one workgroup and moves only
+ * the amplitudes and the requested outputs (sums, intensity map, detector
+ * field) through memory.  Both paths compute the same outputs (to
+ * rounding); the flag exists to compare them. */
 #define LR_LAYER_PASSES 2
 
 /* Transfer function of one hop (§3.1.1, Eqs. (fresnel), (sommerfeld), (r01),

@@ -296,7 +296,8 @@ def lr_donn_forward(net: Network, amp, phi, saved=None, sums: bool = True, inten
     (LR_ACCUMULATE), which must then be given.  skip: complex64 [B, n, n]
     added to the detector-plane field (lr_donn.d_skip); give the same field
     to lr_donn_backward.  layer_passes: one pass per layer even where the
-    whole-field kernel would run (LR_LAYER_PASSES)."""
+    whole-field kernel would run (LR_LAYER_PASSES: Fresnel, n == n_fft in
+    {64, 100, 128}, no saved state, no skip)."""
     torch = _torch()
     b = int(amp.shape[0])
     n, L = net.n, net.num_layers

@@ -807,7 +807,7 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   const int tile_t = lr::tile_shape(N, 0).T;
   int sum_tiles = L.ntiles_vec;  // tiles that wrote partial detector sums
   const bool whole_field = net->approx == LR_FRESNEL && n == N && lr::field_forward_supported(N) && !saved &&
-                           d_sums && !d_intensity && !d_field_out && !net->d_skip &&
+                           (d_sums || d_intensity || d_field_out) && !net->d_skip &&
                            !(net->flags & LR_LAYER_PASSES);
   if (whole_field) {
     // every hop of a sample in one workgroup, the field in shared memory
@@ -820,8 +820,13 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
     fa.layers = Lyr;
     fa.chirp_x = at<float2>(d_work, L.chirp_x);
     fa.chirp_y = at<float2>(d_work, L.chirp_y);
-    fa.reg = host_regions(net->det);
-    fa.sums_part = at<float>(d_work, L.sums_part);
+    if (d_sums) {
+      fa.reg = host_regions(net->det);
+      fa.sums_part = at<float>(d_work, L.sums_part);
+    }
+    fa.intensity = d_intensity;
+    fa.field_out = reinterpret_cast<float2*>(d_field_out);
+    fa.accumulate = accumulate ? 1 : 0;
     fa.batch = batch;
     char name[48];
     std::snprintf(name, sizeof name, "field_forward_N%d", N);

@@ -138,8 +138,9 @@ struct Regions {
 
 // Whole-field forward (field_forward_kernel): one workgroup per sample holds
 // the N x N field in shared memory through every layer, for the grids whose
-// field fits there (N = 64, 100, 128, full aperture).  Fresnel path, region
-// sums only: partials [B][K] for launch_finish_sums with one tile.
+// field fits there (N = 64, 100, 128, full aperture), Fresnel path.  Outputs:
+// region-sum partials [B][K] (for launch_finish_sums with one tile), the
+// intensity map and the detector-plane field.
 struct FieldArgs {
   const float* amp;            // [B][N][N] natural amplitudes
   const float2* mod;           // [L][N][N] gamma*exp(j*phi_l), slot order on both axes
@@ -147,8 +148,11 @@ struct FieldArgs {
   int layers;
   const float2* chirp_x;       // separable chirps, natural frequency order, 1/N folded in
   const float2* chirp_y;
-  Regions reg;                 // region corners (natural coordinates)
+  Regions reg;                 // region corners (natural coordinates); K = 0: no sums
   float* sums_part;            // [B][K]
+  float* intensity;            // [B][N][N] natural, or NULL
+  float2* field_out;           // [B][N][N] natural, or NULL
+  int accumulate;              // intensity is added to the output
   int batch;
 };
 bool field_forward_supported(int N);

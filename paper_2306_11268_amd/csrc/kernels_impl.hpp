@@ -1597,6 +1597,21 @@ __global__ void __launch_bounds__(PL::N * PL::N2) field_forward_kernel(FieldArgs
     for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
     if (lane == 0) a.sums_part[(size_t)b * a.reg.K + k] = acc;
   }
+  // full-map outputs in natural order (consecutive threads, consecutive x)
+  if (a.intensity || a.field_out) {
+    float* __restrict__ io = a.intensity ? a.intensity + (size_t)b * nn : nullptr;
+    float2* __restrict__ fo = a.field_out ? a.field_out + (size_t)b * nn : nullptr;
+    for (int e = tid; e < N * N; e += P) {
+      const int y = e / N;
+      const int x = e - y * N;
+      const float2 u = f[PL::slot_of_pos(y) * TP + PL::slot_of_pos(x)];
+      if (io) {
+        const float in = fmaf(u.x, u.x, u.y * u.y);
+        io[e] = a.accumulate ? io[e] + in : in;
+      }
+      if (fo) fo[e] = u;
+    }
+  }
 }
 
 template <int N>
@@ -1609,7 +1624,9 @@ hipError_t launch_field_fwd_n(const FieldArgs& a, hipStream_t st) {
   if constexpr (whole_field_size<N>()) {
     using PL = typename PlanFor<N>::type;
     static_assert(std::is_same_v<PL, typename RowPlanFor<N>::type>, "one plan on both axes");
-    if (a.batch < 1 || a.layers < 0 || a.layers > 64 || a.reg.K < 1 || a.reg.K > kMaxRegions) return hipErrorInvalidValue;
+    if (a.batch < 1 || a.layers < 0 || a.layers > 64 || a.reg.K < 0 || a.reg.K > kMaxRegions ||
+        (a.reg.K > 0 && !a.sums_part))
+      return hipErrorInvalidValue;
     hipLaunchKernelGGL((field_forward_kernel<PL>), dim3(a.batch), dim3(PL::N * PL::N2), 0, st, a);
     return hipGetLastError();
   } else {

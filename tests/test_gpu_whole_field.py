@@ -22,8 +22,8 @@ TOL = 1e-4
 
 
 def rel(a, b):
-    a = np.asarray(a, dtype=np.float64)
-    b = np.asarray(b, dtype=np.float64)
+    a = np.asarray(a, dtype=np.complex128)
+    b = np.asarray(b, dtype=np.complex128)
     r = float(np.linalg.norm((a - b).ravel()) / max(np.linalg.norm(b.ravel()), 1e-300))
     print(f"  rel-L2 {r:.3e} over {b.size} values")
     return r
@@ -79,3 +79,23 @@ def test_whole_field_forward_accumulates_and_covers_one_layer(lrb):
     out = dev(base)
     lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True, out_sums=out, accumulate=True)
     assert rel(host(out) - base, ref["sums"]) < TOL
+
+
+@pytest.mark.parametrize("m,layers,b", [(64, 1, 4), (100, 3, 5), (128, 2, 3)])
+def test_whole_field_forward_full_map_outputs(lrb, m, layers, b):
+    # intensity map and detector-plane field (workload 1's outputs at 64 x 64),
+    # with and without the sums, against the oracle and the layer passes
+    net, amp, phi, ref = setup(lrb, m, b, layers=layers, gamma=1.0)
+    for sums in (False, True):
+        out = lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=sums, intensity=True, field=True)
+        lp = lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=sums, intensity=True, field=True, layer_passes=True)
+        assert rel(host(out["intensity"]), ref["intensity"]) < TOL
+        assert rel(host(out["field"]), ref["field"]) < TOL
+        assert rel(host(out["intensity"]), host(lp["intensity"])) < TOL
+        if sums:
+            assert rel(host(out["sums"]), ref["sums"]) < TOL
+    # accumulated intensity
+    base = np.full((b, m, m), 0.75, dtype=np.float32)
+    acc = dev(base)
+    lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=False, intensity=True, out_intensity=acc, accumulate=True)
+    assert rel(host(acc) - base, ref["intensity"]) < TOL
