@@ -1285,6 +1285,10 @@ struct WaveTile {
   static constexpr int N1 = PL::N1;
   static_assert(PL::N2 == 8, "wave tiles pair 8 A-items with 8 vectors");
   static constexpr int NC = (N1 + 7) / 8;  // exchange chunks
+  // the last chunk holds one B-item per vector, whose values the 8 lanes of
+  // a row hold one each (rows: lanes 8v .. 8v+7); Good-Thomas plans only
+  // (no B-step twiddles)
+  static constexpr bool LAST_ACROSS = AXIS == kRow && PL::PFA && N1 % 8 == 1 && NC > 1;
   static __device__ __forceinline__ int v_of(int lane) { return AXIS == kCol ? (lane & 7) : (lane >> 3); }
   static __device__ __forceinline__ int j_of(int lane) { return AXIS == kCol ? (lane >> 3) : (lane & 7); }
   // Exchange buffer index of (B-item offset s, A-item j, vector v), in
@@ -1295,6 +1299,63 @@ struct WaveTile {
   static constexpr int PS = AXIS == kCol ? 72 : 65;
   static constexpr int XCH = 7 * PS + 64;
 };
+
+// Exchange with the lane whose index differs in bit D (D = 1, 2, 4) inside
+// each group of 8 lanes (a swizzle: no shared-memory access).
+template <int D>
+__device__ __forceinline__ float2 lane_xor(float2 v) {
+  constexpr int kPattern = (D << 10) | 0x1F;  // bit mode: and 0x1F, or 0, xor D
+  return c2(__int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v.x), kPattern)),
+            __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v.y), kPattern)));
+}
+
+// The spectral B-step of one 8-value B-item held one value per lane by 8
+// consecutive lanes (lane j: element j): forward DFT8 by decimation in
+// frequency (lane j ends with frequency bitrev(j)), times the chirp entry of
+// that frequency (tk: the item's 8 entries by frequency; conjugated when
+// cj), then the inverse transform as the mirrored network with conjugate
+// twiddles (bit-reversed in, natural out, unnormalised).
+__device__ __forceinline__ float2 b_item_across_lanes(float2 u, int j, const float2* tk, bool cj) {
+  constexpr float c = 0.70710678118654752440f;
+  const bool u4 = (j & 4) != 0;
+  const bool u2 = (j & 2) != 0;
+  const bool u1 = (j & 1) != 0;
+  const int m = j & 3;
+  // exp(-2 pi i m / 8) for the pairs of the first stage, exp(-2 pi i (j&1) / 4) for the second
+  const float2 w1 = c2(m == 0 ? 1.f : (m == 1 ? c : (m == 2 ? 0.f : -c)), m == 0 ? 0.f : (m == 2 ? -1.f : -c));
+  const float2 w2 = u1 ? c2(0.f, -1.f) : c2(1.f, 0.f);
+  {
+    const float2 p = lane_xor<4>(u);
+    const float2 d = u4 ? csub(p, u) : cadd(p, u);
+    u = u4 ? cmul(d, w1) : d;
+  }
+  {
+    const float2 p = lane_xor<2>(u);
+    const float2 d = u2 ? csub(p, u) : cadd(p, u);
+    u = u2 ? cmul(d, w2) : d;
+  }
+  {
+    const float2 p = lane_xor<1>(u);
+    u = u1 ? csub(p, u) : cadd(p, u);
+  }
+  const int br = ((j & 1) << 2) | (j & 2) | ((j >> 2) & 1);
+  u = cj ? cmulc(u, tk[br]) : cmul(u, tk[br]);
+  {
+    const float2 p = lane_xor<1>(u);
+    u = u1 ? csub(p, u) : cadd(u, p);
+  }
+  {
+    const float2 p = lane_xor<2>(u);
+    const float2 t = cmulc(u2 ? u : p, w2);
+    u = u2 ? csub(p, t) : cadd(u, t);
+  }
+  {
+    const float2 p = lane_xor<4>(u);
+    const float2 t = cmulc(u4 ? u : p, w1);
+    u = u4 ? csub(p, t) : cadd(u, t);
+  }
+  return u;
+}
 
 // Byte offset of element (stored index j, vector vec) of an N x N array
 // oriented [q][vec] (tables, dphi partials, column fields) or [vec][q] (row
@@ -1351,6 +1412,13 @@ __global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 
     const int bb = jj * WT::PS + vv * WT::PV;  // B side: + j' * PJ
     static_for<0, WT::NC>([&](auto cc) {
       constexpr int c = decltype(cc)::value;
+      if constexpr (WT::LAST_ACROSS && c == WT::NC - 1) {
+        // a last chunk of one B-item per vector (N1 = 8 (NC - 1) + 1): its 8
+        // values sit one per lane in the 8 lanes of the vector, so the lanes
+        // transform it together instead of 1 lane in 8 doing the whole item
+        x[8 * c] = b_item_across_lanes(x[8 * c], jj, tab + 9 * (8 * c), cj);
+        return;
+      }
       static_for<0, 8>([&](auto sc) {
         constexpr int k1 = 8 * c + decltype(sc)::value;
         if constexpr (k1 < N1) xch[decltype(sc)::value * WT::PS + wb] = x[k1];
