@@ -165,9 +165,10 @@ __device__ __forceinline__ void zero_padding(float2* lds, int n, int off) {
 //     (lane, m) is a per-lane constant plus v.  Every (row, run) slot is
 //     visited, without branches: for slots outside the tile ok is false, li
 //     is the spare shared-memory row (position q >= n) or an unused vector of
-//     the tile (v >= nvalid), and global accesses take kOutOfRange;
-//   other tiles (column tiles, rows that do not split evenly over the
-//     waves): only elements of the tile are visited (ok is true); column
+//     the tile (v >= nvalid), and global accesses take kOutOfRange.  When the
+//     T rows do not split evenly over the NW waves, the last round is partial
+//     and the waves past row T - 1 skip it;
+//   column tiles: only elements of the tile are visited (ok is true); column
 //     thread tid handles elements e = tid + i*P, i < N1, with
 //     (v, q) = (e mod T, e div T): every access of a wave covers T
 //     consecutive columns of a few rows.
@@ -184,8 +185,8 @@ __device__ __forceinline__ void zero_padding(float2* lds, int n, int off) {
 template <class C>
 struct RowLanes {
   static constexpr int NW = C::P / 64;                 // waves per workgroup
-  static constexpr bool OK = C::T % NW == 0;           // rows split evenly over the waves
-  static constexpr int RPW = OK ? C::T / NW : 1;       // rows per wave
+  static constexpr bool EVEN = C::T % NW == 0;         // rows split evenly over the waves
+  static constexpr int RPW = (C::T + NW - 1) / NW;     // rows per wave (the last round may be partial)
   static constexpr int NCH = (C::N + 63) / 64;         // 64-position runs per row
 };
 
@@ -193,7 +194,7 @@ constexpr int kAll = 1 << 20;
 
 template <class C, int AXIS, int W>
 struct WalkShape {
-  static constexpr bool ROWS = AXIS == kRow && RowLanes<C>::OK;
+  static constexpr bool ROWS = AXIS == kRow;
   static constexpr int NCH = RowLanes<C>::NCH;
   static constexpr int RPW = RowLanes<C>::RPW;
   // rows: chunks of whole rows; columns: chunks of W elements
@@ -224,36 +225,16 @@ __device__ __forceinline__ void tile_walk2(int n, int off, int nvalid, F1&& firs
           constexpr int r = decltype(c)::value * WS::RCH + decltype(rr)::value;
           if constexpr (r < RL::RPW) {
             const int v = wv + RL::NW * r;
-            const bool vok = v < nvalid;
-            static_for<0, RL::NCH>([&](auto m) {
-              const int q = lane + 64 * decltype(m)::value;
-              f(std::integral_constant<int, decltype(rr)::value * RL::NCH + decltype(m)::value>{}, v, q,
-                lofs[m.value] + v, vok && qok[m.value]);
-            });
-          }
-        });
-      };
-      visit(first);
-      visit(second);
-    });
-  } else if constexpr (AXIS == kRow) {
-    // rows that do not split evenly over the waves: flat walk over the tile
-    const int total = nvalid * n;
-    const int dv = C::P / n;
-    const int dq = C::P - dv * n;
-    static_for<0, WS::NCHUNK>([&](auto c) {
-      constexpr int e0 = decltype(c)::value * WS::CH * C::P;
-      auto visit = [&](auto& f) {
-        const int tid = opaque_tid();
-        int v = (tid + e0) / n;
-        int q = (tid + e0) - v * n;
-        static_for<0, WS::CH>([&](auto i) {
-          constexpr int ii = decltype(c)::value * WS::CH + decltype(i)::value;
-          if constexpr (ii < C::N1) {
-            if (tid + ii * C::P < total) f(i, v, q, ST ? q * C::TP + v : lds_index<C>(q + off, v), true);
-            q += dq;
-            v += dv;
-            if (q >= n) { q -= n; ++v; }
+            // rows that do not split evenly: in the last round the waves
+            // past the tile's last row skip it (a wave-uniform branch)
+            if (RL::EVEN || r + 1 < RL::RPW || v < C::T) {
+              const bool vok = v < nvalid;
+              static_for<0, RL::NCH>([&](auto m) {
+                const int q = lane + 64 * decltype(m)::value;
+                f(std::integral_constant<int, decltype(rr)::value * RL::NCH + decltype(m)::value>{}, v, q,
+                  lofs[m.value] + v, vok && qok[m.value]);
+              });
+            }
           }
         });
       };
