@@ -1748,7 +1748,7 @@ struct LayerTile {
   static constexpr int T = TileT<N>::T;
 };
 template <> struct LayerTile<200, kFwdMid, kCol> { static constexpr int T = 32; };
-template <> struct LayerTile<200, kPropOnce, kRow> { static constexpr int T = 8; };
+template <> struct LayerTile<200, kPropOnce, kRow> { static constexpr int T = 16; };
 template <> struct LayerTile<200, kFwdMid, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kBwdMid, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kBwdLast, kCol> { static constexpr int T = 32; };
