@@ -42,8 +42,8 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="depth of a runtime-study variant")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--layer-passes", action="store_true",
-                    help="forward workloads: one pass per layer even where the whole-field kernel applies "
-                         "(Fresnel, n = n_fft <= 128, sums only)")
+                    help="one pass per layer in the forward call even where the whole-field kernel applies "
+                         "(Fresnel, n = n_fft in 64, 100, 128)")
     ap.add_argument("--graph", action="store_true",
                     help="record the step once as a HIP graph and time its replays (measured slower than "
                          "launching the kernels one by one on this stack, so not the default)")
@@ -293,7 +293,7 @@ def main():
     net.workspace(batch, lb.LR_OP_BACKWARD)
 
     def step():
-        lb.lr_donn_forward(net, amp, phi, saved=saved, sums=True, out_sums=sums)
+        lb.lr_donn_forward(net, amp, phi, saved=saved, sums=True, out_sums=sums, layer_passes=args.layer_passes)
         return lb.lr_donn_backward(net, phi, saved, sums=sums, labels=labels, out_grad_phi=grad)
 
     for _ in range(args.warmup):

@@ -141,7 +141,9 @@ typedef struct lr_donn {
  * otherwise keep the whole field of a sample on chip.  Without it, a forward
  * call on the Fresnel path with n == n_fft in {64, 100, 128} (the field fits
  * in one compute unit's shared memory), no saved state and no skip field
- * runs every hop and modulation of a sample in one workgroup and moves only
+ * (and, at 100 and 128, at least one sample per compute unit of the
+ * device) runs every hop and modulation of a sample in one workgroup and
+ * moves only
  * the amplitudes and the requested outputs (sums, intensity map, detector
  * field) through memory.  Both paths compute the same outputs (to
  * rounding); the flag exists to compare them. */

@@ -813,7 +813,7 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   a.full = slot_ordered(net) ? 1 : 0;
   const int tile_t = lr::tile_shape(N, 0).T;
   int sum_tiles = L.ntiles_vec;  // tiles that wrote partial detector sums
-  const bool whole_field = net->approx == LR_FRESNEL && n == N && lr::field_forward_supported(N) && !saved &&
+  const bool whole_field = net->approx == LR_FRESNEL && n == N && lr::field_forward_preferred(N, batch) && !saved &&
                            (d_sums || d_intensity || d_field_out) && !net->d_skip &&
                            !(net->flags & LR_LAYER_PASSES);
   if (whole_field) {

@@ -461,6 +461,17 @@ SlotMap slot_map(int N) {
 
 bool field_forward_supported(int N) { return N == 64 || N == 100 || N == 128; }
 
+bool field_forward_preferred(int N, int batch) {
+  if (!field_forward_supported(N)) return false;
+  if (N == 64) return true;
+  int dev = 0;
+  int cus = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1)
+    return false;
+  return batch >= cus;
+}
+
 hipError_t launch_field_forward(int N, const FieldArgs& a, hipStream_t st) {
   switch (N) {
     case 64: return launch_field_fwd_n<64>(a, st);

@@ -156,6 +156,12 @@ struct FieldArgs {
   int batch;
 };
 bool field_forward_supported(int N);
+// Whether a forward call of this size and batch should take the whole-field
+// kernel: it runs one sample per workgroup, so below one sample per CU it
+// leaves CUs idle and the layer passes are faster, except at N = 64 where
+// the passes are launch-bound (5-layer forward, batch 64: 42 against 44 us
+// at N = 64, 103 against 88 us at N = 100, 107 against 84 us at N = 128).
+bool field_forward_preferred(int N, int batch);
 hipError_t launch_field_forward(int N, const FieldArgs& a, hipStream_t st);
 
 bool fft_size_supported(int N);

@@ -1555,8 +1555,11 @@ __global__ void __launch_bounds__(PL::N * PL::N2) field_forward_kernel(FieldArgs
   constexpr int N2 = C::N2;
   constexpr int P = C::P;
   constexpr int TP = C::TP;
+  // The field, and in its padding column (x = N) the x chirp; the y chirp
+  // apart.  Both in B-item order: entry N2*k1 + k2 is frequency
+  // freq(k1, k2).  (At N = 100 this keeps a workgroup within 80 KB, two
+  // per CU.)
   __shared__ float2 f[N * TP];
-  __shared__ float2 tx[N];  // chirps in B-item order: entry N2*k1 + k2 is frequency freq(k1, k2)
   __shared__ float2 ty[N];
 
   const int b = (int)blockIdx.x;
@@ -1567,7 +1570,7 @@ __global__ void __launch_bounds__(PL::N * PL::N2) field_forward_kernel(FieldArgs
 
   for (int i = tid; i < N; i += P) {
     const int fr = PL::freq(i / N2, i % N2);
-    tx[i] = a.chirp_x[fr];
+    f[i * TP + N] = a.chirp_x[fr];
     ty[i] = a.chirp_y[fr];
   }
   // amplitudes (natural, zero phase) into slot order: stored (sy, sx) holds
@@ -1584,7 +1587,7 @@ __global__ void __launch_bounds__(PL::N * PL::N2) field_forward_kernel(FieldArgs
   __syncthreads();
 
   // 1-D propagation of every vector along one axis, in place
-  auto prop = [&](auto axis_c, const float2* tab) {
+  auto prop = [&](auto axis_c, const float2* tab, int tstride) {
     constexpr bool ROWS = decltype(axis_c)::value == kRow;
     auto at = [&](int vec, int slot) -> float2& { return ROWS ? f[vec * TP + slot] : f[slot * TP + vec]; };
     float2 x[N1];
@@ -1596,7 +1599,7 @@ __global__ void __launch_bounds__(PL::N * PL::N2) field_forward_kernel(FieldArgs
       float2 y[N2];
       static_for<0, N2>([&](auto q) { y[q.value] = at(v, N2 * k1 + q.value); });
       b_forward<C>(k1, y);
-      static_for<0, N2>([&](auto q) { y[q.value] = cmul(y[q.value], tab[N2 * k1 + q.value]); });
+      static_for<0, N2>([&](auto q) { y[q.value] = cmul(y[q.value], tab[(N2 * k1 + q.value) * tstride]); });
       b_inverse<C>(k1, y);
       static_for<0, N2>([&](auto q) { at(v, N2 * k1 + q.value) = y[q.value]; });
     }
@@ -1608,8 +1611,8 @@ __global__ void __launch_bounds__(PL::N * PL::N2) field_forward_kernel(FieldArgs
   };
 
   for (int hop = 1; hop <= a.layers + 1; ++hop) {
-    prop(std::integral_constant<int, kRow>{}, tx);
-    prop(std::integral_constant<int, kCol>{}, ty);
+    prop(std::integral_constant<int, kRow>{}, f + N, TP);
+    prop(std::integral_constant<int, kCol>{}, ty, 1);
     if (hop <= a.layers) {
       // U_l = gamma exp(j phi_l) A_l; the table is in slot order, [y][x] or
       // [x][y]: consecutive threads take consecutive positions of its rows

@@ -3,9 +3,11 @@ through every layer) against the float64 oracle and against the one-pass-per-
 layer path on the same inputs.
 
 It runs for forward calls on the Fresnel path with n == n_fft in
-{64, 100, 128}, region sums only, no saved state; LR_LAYER_PASSES forces the
-layer passes.  Tolerance: relative L2 1e-4 on the sums (the stated bound for
-intensities).
+{64, 100, 128}, no saved state, no skip field, and at 100 and 128 at least
+one sample per CU (256 on MI355X; smaller batches take the layer passes);
+LR_LAYER_PASSES forces the layer passes.  Every case checks, from the
+library's own launch record, which path ran.  Tolerance: relative L2 1e-4
+(the stated bound for fields and intensities).
 """
 
 import numpy as np
@@ -46,6 +48,18 @@ def host(t):
     return t.detach().cpu().numpy()
 
 
+def ran_whole_field(lrb, fn):
+    """Run fn with the library's launch timing on; True if the whole-field kernel ran."""
+    lrb.kernel_timing(True)
+    try:
+        fn()
+        torch.cuda.synchronize()
+        names = set(lrb.kernel_timing_report())
+    finally:
+        lrb.kernel_timing(False)
+    return any(k.startswith("field_forward") for k in names)
+
+
 def setup(lrb, m, b, layers=5, gamma=0.9):
     det = wl.layout_grid(m, 4, max(2, m // 10))
     w = wl.Workload(94, "test", 532e-9, 36e-6, 0.3, od.FRESNEL, m, m, layers, b, "forward", det, "sums", "uniform")
@@ -59,10 +73,13 @@ def setup(lrb, m, b, layers=5, gamma=0.9):
 
 
 @pytest.mark.parametrize("m", [64, 100, 128])
-@pytest.mark.parametrize("b", [256, 3])
+@pytest.mark.parametrize("b", [256, 259, 3])
 def test_whole_field_forward_matches_oracle_and_layer_passes(lrb, m, b):
     net, amp, phi, ref = setup(lrb, m, b)
-    whole = host(lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True)["sums"])
+    out = {}
+    took = ran_whole_field(lrb, lambda: out.update(lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True)))
+    assert took == (m == 64 or b >= 256)
+    whole = host(out["sums"])
     passes = host(lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True, layer_passes=True)["sums"])
     assert rel(whole, ref["sums"]) < TOL
     assert rel(passes, ref["sums"]) < TOL
@@ -74,20 +91,22 @@ def test_whole_field_forward_matches_oracle_and_layer_passes(lrb, m, b):
 
 def test_whole_field_forward_accumulates_and_covers_one_layer(lrb):
     # LR_ACCUMULATE adds into the given sums; one layer (two hops) and gamma != 1
-    net, amp, phi, ref = setup(lrb, 128, 5, layers=1, gamma=1.3)
+    net, amp, phi, ref = setup(lrb, 128, 256, layers=1, gamma=1.3)
     base = np.full(ref["sums"].shape, 2.5, dtype=np.float32)
     out = dev(base)
     lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True, out_sums=out, accumulate=True)
     assert rel(host(out) - base, ref["sums"]) < TOL
 
 
-@pytest.mark.parametrize("m,layers,b", [(64, 1, 4), (100, 3, 5), (128, 2, 3)])
+@pytest.mark.parametrize("m,layers,b", [(64, 1, 4), (100, 3, 256), (128, 2, 257)])
 def test_whole_field_forward_full_map_outputs(lrb, m, layers, b):
     # intensity map and detector-plane field (workload 1's outputs at 64 x 64),
     # with and without the sums, against the oracle and the layer passes
     net, amp, phi, ref = setup(lrb, m, b, layers=layers, gamma=1.0)
     for sums in (False, True):
-        out = lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=sums, intensity=True, field=True)
+        out = {}
+        assert ran_whole_field(lrb, lambda: out.update(
+            lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=sums, intensity=True, field=True)))
         lp = lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=sums, intensity=True, field=True, layer_passes=True)
         assert rel(host(out["intensity"]), ref["intensity"]) < TOL
         assert rel(host(out["field"]), ref["field"]) < TOL
