@@ -1525,8 +1525,9 @@ __global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 
 // Whole-field forward for grids whose field fits in one CU's shared memory
 // (N <= 128: 132 KB at N = 128).  One workgroup per sample reads the
 // amplitude once, runs every hop and modulation of Eq. (forward_diff) and
-// (phase_mod_matrix) on the resident field, and writes only the region sums
-// (§2.1), so no field crosses HBM between layers.
+// (phase_mod_matrix) on the resident field, and writes only the detector-
+// plane outputs (region sums of §2.1, and the intensity map and field when
+// asked for), so no field crosses HBM between layers.
 //
 // The field is held in slot order on both axes (plan.hpp), f[sy][sx] with
 // pitch N + 1.  A hop is the separable 1-D propagation along x for every row,
@@ -1684,11 +1685,6 @@ hipError_t launch_field_fwd_n(const FieldArgs& a, hipStream_t st) {
   } else {
     return hipErrorInvalidValue;
   }
-}
-
-template <int N>
-constexpr bool field_fwd_supported_n() {
-  return whole_field_size<N>();
 }
 
 // ---------------------------------------------------------------------------
