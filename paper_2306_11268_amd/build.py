@@ -35,19 +35,29 @@ COMMON = [
 ]
 
 
+def _code_only(text: str) -> str:
+    """C++ source without comments and with whitespace runs collapsed (string
+    and character literals kept whole)."""
+    import re
+    token = re.compile(r'"(?:\\.|[^"\\])*"|\'(?:\\.|[^\'\\])*\'|//[^\n]*|/\*.*?\*/', re.S)
+    out = token.sub(lambda m: " " if m.group(0).startswith("/") else m.group(0), text)
+    return " ".join(out.split())
+
+
 def source_digest() -> str:
-    """SHA-256 over the device sources, the public header and the compile flags.
+    """SHA-256 over the device sources, the public header and the compile flags,
+    comments and layout left out.
 
     Hardware-counter figures recorded for a kernel are only valid for the
-    sources they were taken from; a changed digest marks them stale."""
+    code they were taken from; a changed digest marks them stale."""
     import hashlib
     h = hashlib.sha256()
     files = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".hip", ".hpp")))
     files.append(os.path.join(os.path.dirname(PKG), "include", "lr.h"))
     for f in files:
         h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     h.update(" ".join(COMMON).encode())
     return h.hexdigest()[:16]
 

@@ -82,3 +82,12 @@ def test_step_byte_models():
     # prop 12, five forward layers 80, detector read 2.4, seed 4.8, layer 5 adjoint 2.4 + 16,
     # layers 4..2 adjoint 72, layer 1 adjoint 16 (units of n^2)
     assert abs(path - (12 + 80 + 2.4 + 4.8 + 18.4 + 72 + 16) * nn) < 1e-6 * nn
+
+
+def test_source_digest_ignores_comments_but_not_code():
+    from paper_2306_11268_amd import build as lb
+
+    base = 'int f(int x) { return x + 1; }  // add one\n/* note */ const char* s = "a // b";'
+    assert lb._code_only(base) == lb._code_only(base.replace("add one", "increment").replace("note", "n"))
+    assert lb._code_only(base) != lb._code_only(base.replace("x + 1", "x + 2"))
+    assert lb._code_only(base) != lb._code_only(base.replace('"a // b"', '"a // c"'))
