@@ -57,32 +57,93 @@ struct Dft<4, SIGN> {
   }
 };
 
-template <int SIGN>
-struct Dft<5, SIGN> {
+// Radix 2 and 4 on inputs given up to constant factors, as Dft5 below:
+// element p of the input is G::g(p) * a[p] (g(0) = 1).  Same instruction
+// counts as the plain codelets; the factors ride in FMA constants.
+template <int SIGN, class G>
+struct Dft2S {
   LR_HD static void run(float2* a) {
-    const float c1 = 0.30901699437494742410f;   // cos(2*pi/5)
-    const float c2v = -0.80901699437494742410f; // cos(4*pi/5)
-    const float s1 = 0.95105651629515357212f;   // sin(2*pi/5)
-    const float s2 = 0.58778525229247312917f;   // sin(4*pi/5)
-    const float2 t1 = cadd(a[1], a[4]);
-    const float2 t2 = cadd(a[2], a[3]);
-    const float2 t3 = csub(a[1], a[4]);
-    const float2 t4 = csub(a[2], a[3]);
-    const float2 b1 = c2(fmaf(c2v, t2.x, fmaf(c1, t1.x, a[0].x)), fmaf(c2v, t2.y, fmaf(c1, t1.y, a[0].y)));
-    const float2 b2 = c2(fmaf(c1, t2.x, fmaf(c2v, t1.x, a[0].x)), fmaf(c1, t2.y, fmaf(c2v, t1.y, a[0].y)));
-    const float2 u1 = mul_qturn<SIGN>(c2(fmaf(s1, t3.x, s2 * t4.x), fmaf(s1, t3.y, s2 * t4.y)));
-    const float2 u2 = mul_qturn<SIGN>(c2(fmaf(s2, t3.x, -s1 * t4.x), fmaf(s2, t3.y, -s1 * t4.y)));
-    a[0] = cadd(a[0], cadd(t1, t2));
-    a[1] = cadd(b1, u1);
-    a[4] = csub(b1, u1);
-    a[2] = cadd(b2, u2);
-    a[3] = csub(b2, u2);
+    constexpr float g1 = static_cast<float>(G::g(1));
+    const float2 t = a[1];
+    a[1] = c2(fmaf(-g1, t.x, a[0].x), fmaf(-g1, t.y, a[0].y));
+    a[0] = c2(fmaf(g1, t.x, a[0].x), fmaf(g1, t.y, a[0].y));
   }
 };
+
+template <int SIGN, class G>
+struct Dft4S {
+  LR_HD static void run(float2* a) {
+    constexpr double g1 = G::g(1), g2 = G::g(2), g3 = G::g(3);
+    constexpr float f2 = static_cast<float>(g2), r31 = static_cast<float>(g3 / g1);
+    constexpr float f1 = static_cast<float>(g1);
+    // SIGN*i*g1*v = (-SIGN*g1*v.y, SIGN*g1*v.x)
+    constexpr float h1 = static_cast<float>(SIGN < 0 ? g1 : -g1);
+    const float2 t0 = c2(fmaf(f2, a[2].x, a[0].x), fmaf(f2, a[2].y, a[0].y));
+    const float2 t1 = c2(fmaf(-f2, a[2].x, a[0].x), fmaf(-f2, a[2].y, a[0].y));
+    const float2 T2 = c2(fmaf(r31, a[3].x, a[1].x), fmaf(r31, a[3].y, a[1].y));
+    const float2 T3 = c2(fmaf(-r31, a[3].x, a[1].x), fmaf(-r31, a[3].y, a[1].y));
+    a[0] = c2(fmaf(f1, T2.x, t0.x), fmaf(f1, T2.y, t0.y));
+    a[2] = c2(fmaf(-f1, T2.x, t0.x), fmaf(-f1, T2.y, t0.y));
+    a[1] = c2(fmaf(h1, T3.y, t1.x), fmaf(-h1, T3.x, t1.y));
+    a[3] = c2(fmaf(-h1, T3.y, t1.x), fmaf(h1, T3.x, t1.y));
+  }
+};
+
+// Radix 5 on inputs given up to constant factors: element p of the input is
+// G::g(p) * a[p] (g(0) = 1), so that a Cooley-Tukey stage can leave the
+// magnitude of its twiddles to this step.  With t1 = g1 T1, t3 = g1 T3,
+// t2 = g2 T2, t4 = g2 T4 (T1, T3 = a[1] +- (g4/g1) a[4], T2, T4 likewise),
+//   X0 = a0 + t1 + t2,  X1, X4 = b1 +- SIGN i (s1 t3 + s2 t4),
+//   X2, X3 = b2 +- SIGN i (s2 t3 - s1 t4),
+// b1 = a0 + c1 t1 + c2 t2, b2 = a0 + c2 t1 + c1 t2.  Every factor g_p and
+// sine folds into a constant of an FMA: 32 instructions, scaled or not.
+struct UnitScale {
+  static constexpr double g(int) { return 1.0; }
+};
+
+template <int SIGN, class G>
+struct Dft5 {
+  LR_HD static void run(float2* a) {
+    constexpr double c1 = 0.30901699437494742410;   // cos(2*pi/5)
+    constexpr double c2v = -0.80901699437494742410; // cos(4*pi/5)
+    constexpr double s1 = 0.95105651629515357212;   // sin(2*pi/5)
+    constexpr double s2 = 0.58778525229247312917;   // sin(4*pi/5)
+    constexpr double g1 = G::g(1), g2 = G::g(2), g3 = G::g(3), g4 = G::g(4);
+    constexpr float r14 = static_cast<float>(g4 / g1);
+    constexpr float r23 = static_cast<float>(g3 / g2);
+    const float2 T1 = c2(fmaf(r14, a[4].x, a[1].x), fmaf(r14, a[4].y, a[1].y));
+    const float2 T3 = c2(fmaf(-r14, a[4].x, a[1].x), fmaf(-r14, a[4].y, a[1].y));
+    const float2 T2 = c2(fmaf(r23, a[3].x, a[2].x), fmaf(r23, a[3].y, a[2].y));
+    const float2 T4 = c2(fmaf(-r23, a[3].x, a[2].x), fmaf(-r23, a[3].y, a[2].y));
+    constexpr float e11 = static_cast<float>(c1 * g1), e12 = static_cast<float>(c2v * g2);
+    constexpr float e21 = static_cast<float>(c2v * g1), e22 = static_cast<float>(c1 * g2);
+    const float2 b1 = c2(fmaf(e12, T2.x, fmaf(e11, T1.x, a[0].x)), fmaf(e12, T2.y, fmaf(e11, T1.y, a[0].y)));
+    const float2 b2 = c2(fmaf(e22, T2.x, fmaf(e21, T1.x, a[0].x)), fmaf(e22, T2.y, fmaf(e21, T1.y, a[0].y)));
+    // s1 t3 + s2 t4 = k1 (T3 + q1 T4), s2 t3 - s1 t4 = k2 (T3 - q2 T4)
+    constexpr double k1 = s1 * g1, k2 = s2 * g1;
+    constexpr float q1 = static_cast<float>(s2 * g2 / k1), q2 = static_cast<float>(s1 * g2 / k2);
+    const float2 v1 = c2(fmaf(q1, T4.x, T3.x), fmaf(q1, T4.y, T3.y));
+    const float2 v2 = c2(fmaf(-q2, T4.x, T3.x), fmaf(-q2, T4.y, T3.y));
+    // SIGN*i*k*v = (-SIGN*k*v.y, SIGN*k*v.x)
+    constexpr float f1 = static_cast<float>(SIGN < 0 ? k1 : -k1);
+    constexpr float f2 = static_cast<float>(SIGN < 0 ? k2 : -k2);
+    constexpr float h1 = static_cast<float>(g1), h2 = static_cast<float>(g2);
+    a[0] = c2(fmaf(h2, T2.x, fmaf(h1, T1.x, a[0].x)), fmaf(h2, T2.y, fmaf(h1, T1.y, a[0].y)));
+    a[1] = c2(fmaf(f1, v1.y, b1.x), fmaf(-f1, v1.x, b1.y));
+    a[4] = c2(fmaf(-f1, v1.y, b1.x), fmaf(f1, v1.x, b1.y));
+    a[2] = c2(fmaf(f2, v2.y, b2.x), fmaf(-f2, v2.x, b2.y));
+    a[3] = c2(fmaf(-f2, v2.y, b2.x), fmaf(f2, v2.x, b2.y));
+  }
+};
+
+template <int SIGN>
+struct Dft<5, SIGN> : Dft5<SIGN, UnitScale> {};
 
 // Radix 7 as three conjugate pairs: with t_k = a[k] + a[7-k] and
 // d_k = a[k] - a[7-k] (k = 1, 2, 3),
 //   X[m], X[7-m] = a[0] + sum_k cos(2 pi k m / 7) t_k  +-  SIGN i sum_k sin(2 pi k m / 7) d_k.
+// Each odd sum is written as its first sine times a two-FMA combination, and
+// that sine is applied in the output FMA.
 template <int SIGN>
 struct Dft<7, SIGN> {
   LR_HD static void run(float2* a) {
@@ -102,32 +163,46 @@ struct Dft<7, SIGN> {
       return c2(fmaf(x3, t3.x, fmaf(x2, t2.x, fmaf(x1, t1.x, a[0].x))),
                 fmaf(x3, t3.y, fmaf(x2, t2.y, fmaf(x1, t1.y, a[0].y))));
     };
-    auto im = [&](float y1, float y2, float y3) {
-      return mul_qturn<SIGN>(c2(fmaf(y3, d3.x, fmaf(y2, d2.x, y1 * d1.x)), fmaf(y3, d3.y, fmaf(y2, d2.y, y1 * d1.y))));
+    // d1 + q2*d2 + q3*d3
+    auto odd = [&](float q2, float q3) {
+      return c2(fmaf(q3, d3.x, fmaf(q2, d2.x, d1.x)), fmaf(q3, d3.y, fmaf(q2, d2.y, d1.y)));
+    };
+    constexpr float g = SIGN < 0 ? 1.f : -1.f;
+    // b +- SIGN*i*s*v
+    auto out = [&](float2 b, float s, float2 v, float2& hi, float2& lo) {
+      hi = c2(fmaf(g * s, v.y, b.x), fmaf(-g * s, v.x, b.y));
+      lo = c2(fmaf(-g * s, v.y, b.x), fmaf(g * s, v.x, b.y));
     };
     const float2 b1 = re(c1, c2v, c3);
     const float2 b2 = re(c2v, c3, c1);
     const float2 b3 = re(c3, c1, c2v);
-    const float2 u1 = im(s1, s2, s3);
-    const float2 u2 = im(s2, -s3, -s1);
-    const float2 u3 = im(s3, -s1, s2);
+    // sums s1 d1 + s2 d2 + s3 d3, s2 d1 - s3 d2 - s1 d3, s3 d1 - s1 d2 + s2 d3
+    const float2 v1 = odd(1.24697960371746706105f, 0.55495813208737119142f);
+    const float2 v2 = odd(-0.44504186791262880858f, -0.80193773580483825247f);
+    const float2 v3 = odd(-1.80193773580483825247f, 2.24697960371746706105f);
     a[0] = cadd(a[0], cadd(t1, cadd(t2, t3)));
-    a[1] = cadd(b1, u1);
-    a[6] = csub(b1, u1);
-    a[2] = cadd(b2, u2);
-    a[5] = csub(b2, u2);
-    a[3] = cadd(b3, u3);
-    a[4] = csub(b3, u3);
+    out(b1, s1, v1, a[1], a[6]);
+    out(b2, s2, v2, a[2], a[5]);
+    out(b3, s3, v3, a[3], a[4]);
   }
 };
 
 // Cooley-Tukey N = P*Q: P transforms of length Q on the stride-P
 // subsequences, twiddle exp(SIGN*2*pi*i*p*k2/N), then Q transforms of length P;
-// output X[k2 + Q*k1].
+// output X[k2 + Q*k1].  With P = 2, 4 or 5 each twiddle is applied as
+// split_root (two FMAs, or none for the quarter turns) and its magnitude
+// factor is folded into the length-P step of column k2 (the scaled codelets
+// with TwiddleScale).
+template <int N, int SIGN, int K2>
+struct TwiddleScale {
+  static constexpr double g(int p) { return (p * K2) % N == 0 ? 1.0 : split_root_scale(p * K2, N, SIGN); }
+};
+
 template <int P, int Q, int SIGN>
 struct DftCT {
   LR_HD static void run(float2* a) {
     constexpr int N = P * Q;
+    constexpr bool SPLIT = P == 2 || P == 4 || P == 5;
     float2 t[N];
     static_for<0, P>([&](auto pc) {
       constexpr int p = decltype(pc)::value;
@@ -136,14 +211,26 @@ struct DftCT {
       Dft<Q, SIGN>::run(s);
       static_for<0, Q>([&](auto kc) {
         constexpr int k2 = decltype(kc)::value;
-        t[p * Q + k2] = twiddle_const<N, SIGN, p * k2>(s[k2]);
+        if constexpr (SPLIT) {
+          t[p * Q + k2] = split_root<N, SIGN, p * k2>(s[k2]);
+        } else {
+          t[p * Q + k2] = twiddle_const<N, SIGN, p * k2>(s[k2]);
+        }
       });
     });
     static_for<0, Q>([&](auto kc) {
       constexpr int k2 = decltype(kc)::value;
       float2 u[P];
       static_for<0, P>([&](auto pc) { u[pc.value] = t[pc.value * Q + k2]; });
-      Dft<P, SIGN>::run(u);
+      if constexpr (P == 2) {
+        Dft2S<SIGN, TwiddleScale<N, SIGN, k2>>::run(u);
+      } else if constexpr (P == 4) {
+        Dft4S<SIGN, TwiddleScale<N, SIGN, k2>>::run(u);
+      } else if constexpr (P == 5) {
+        Dft5<SIGN, TwiddleScale<N, SIGN, k2>>::run(u);
+      } else {
+        Dft<P, SIGN>::run(u);
+      }
       static_for<0, P>([&](auto jc) { a[k2 + Q * jc.value] = u[jc.value]; });
     });
   }

@@ -133,4 +133,41 @@ LR_HD float2 twiddle_const(float2 a) {
   }
 }
 
+// exp(SIGN*2*pi*i*E/N) = scale * (1 + i*r) where |cos| >= |sin| (scale =
+// cos, r = tan), else scale * (r + i) (scale = sin, r = cot).  split_root
+// multiplies by the unit-scale factor with two FMAs; the caller applies the
+// scale, which is then at least 1/sqrt(2) in magnitude and r at most 1.
+// Quarter turns: SIGN*i (scale 1), -1 (scale -1, nothing to multiply) and
+// -SIGN*i (scale -1), all exact.
+constexpr double dabs(double x) { return x < 0 ? -x : x; }
+constexpr bool split_root_cos(long long e, long long N, int sign) {
+  return dabs(unit_root(e, N, sign).re) >= dabs(unit_root(e, N, sign).im);
+}
+constexpr double split_root_scale(long long e, long long N, int sign) {
+  e %= N;
+  if (e < 0) e += N;
+  if (e == 0) return 1.0;
+  if ((4 * e) % N == 0) return (4 * e) / N == 1 ? 1.0 : -1.0;
+  return split_root_cos(e, N, sign) ? unit_root(e, N, sign).re : unit_root(e, N, sign).im;
+}
+template <int N, int SIGN, int E0>
+LR_HD float2 split_root(float2 a) {
+  constexpr int e = ((E0 % N) + N) % N;
+  if constexpr (e == 0) {
+    return a;
+  } else if constexpr ((4 * e) % N == 0) {
+    if constexpr ((4 * e) / N == 2) return a;
+    return mul_qturn<SIGN>(a);
+  } else {
+    constexpr cdbl z = unit_root(e, N, SIGN);
+    if constexpr (split_root_cos(e, N, SIGN)) {
+      constexpr float r = static_cast<float>(z.im / z.re);
+      return c2(fmaf(-r, a.y, a.x), fmaf(r, a.x, a.y));
+    } else {
+      constexpr float r = static_cast<float>(z.re / z.im);
+      return c2(fmaf(r, a.x, -a.y), fmaf(r, a.y, a.x));
+    }
+  }
+}
+
 }  // namespace lr
