@@ -189,28 +189,132 @@ __device__ __forceinline__ void b_spectral_item(const Tile<C>& t, int k1, bool c
   fence();
   write_b(t, k1, y);
 }
+// The last round of B-items when it holds a quarter of a round: with
+// N1 mod N2 = N2/4 and N2 = 4*Q, Q odd (N = 500: 25 items of 20 values over
+// 20 slots, 5 left per vector), a plain last round keeps a quarter of the
+// threads busy while the rest wait at the next barrier.  Instead every
+// left-over item goes to a quad of consecutive lanes, which splits its
+// length-N2 DFT by the Good-Thomas map 4 x Q: lane q takes the Q values
+// n = (Q*q + 4*m) mod N2, m < Q (with their Cooley-Tukey twiddles), runs a
+// length-Q DFT over m, and the length-4 DFTs over q run across the quad as
+// two radix-2 stages on lane exchanges, leaving lane q with the frequencies
+// k4 = bitrev2(q) of the 4-point step.  After the table the inverse runs the
+// mirrored network.  All P threads take part, one item per quad.
+template <class C>
+struct QuadLast {
+  static constexpr int R = C::N1 % C::N2;
+  static constexpr int Q = C::N2 / 4;
+  static constexpr bool ON = C::N2 % 4 == 0 && Q % 2 == 1 && Q > 1 && R * 4 == C::N2;
+  // output element k2 of the length-N2 DFT for (k4, k5): k4*E1 + k5*E2 mod N2
+  static constexpr int E1 = ON ? Q * inv_mod(Q % 4, 4) : 0;
+  static constexpr int E2 = ON ? 4 * inv_mod(4 % Q, Q) : 0;
+};
+
+// Value of the lane whose index differs in bit D (1 or 2) within its quad.
+template <int D>
+__device__ __forceinline__ float2 quad_xor(float2 v) {
+  constexpr int kCtrl = D == 1 ? 0xB1 : 0x4E;  // quad_perm [1,0,3,2] / [2,3,0,1]
+  return c2(__int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v.x), kCtrl, 0xF, 0xF, false)),
+            __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v.y), kCtrl, 0xF, 0xF, false)));
+}
+
+// Radix-2 butterfly across lanes differing in bit D: the lower lane keeps
+// own + partner, the upper one partner - own (sg = -1 there).
+template <int D, int Q>
+__device__ __forceinline__ void quad_butterfly(float2 (&z)[Q], float sg) {
+  static_for<0, Q>([&](auto m) {
+    const float2 p = quad_xor<D>(z[m.value]);
+    z[m.value] = c2(fmaf(sg, z[m.value].x, p.x), fmaf(sg, z[m.value].y, p.y));
+  });
+}
+
+template <class C>
+__device__ __forceinline__ void b_spectral_quad(float2* lds, bool conj_tab) {
+  using QL = QuadLast<C>;
+  using PL = typename C::Plan;
+  constexpr int Q = QL::Q;
+  // the lane index behind an empty asm statement: the addresses and roots
+  // derived from it are formed at each call, not hoisted out of the
+  // caller's loops and kept live across them
+  int tid = (int)threadIdx.x;
+  asm volatile("" : "+v"(tid));
+  const int q = tid & 3;
+  const int item = tid >> 2;
+  const int v = item % C::T;
+  const int k1 = C::N2 * (C::IB - 1) + item / C::T;
+  float2* const base = lds + (C::N2 * k1) * C::TP + v;
+  const float2* const tab = lds + (C::N2 * k1) * C::TP + C::T;
+  // element n(q, m) = (Q*q + 4*m) mod N2 of the item
+  auto elem = [&](auto m) {
+    const int e = Q * q + 4 * decltype(m)::value;
+    return e >= C::N2 ? e - C::N2 : e;
+  };
+  const float s1 = (q & 1) ? -1.f : 1.f;
+  const float s2 = (q & 2) ? -1.f : 1.f;
+  const bool l3 = q == 3;
+  float2 z[Q];
+  static_for<0, Q>([&](auto m) {
+    const int e = elem(m);
+    z[m.value] = base[e * C::TP];
+    if constexpr (!PL::PFA) z[m.value] = cmul(z[m.value], root_at<C::N>((unsigned)(k1 * e)));
+  });
+  Dft<Q, -1>::run(z);
+  // 4-point DFT over the quad by decimation in frequency: (x_q + x_{q+2}),
+  // (x_q - x_{q+2}) w4^q, then pairs; w4 = -i on lane 3
+  quad_butterfly<2, Q>(z, s2);
+  static_for<0, Q>([&](auto m) {
+    const float2 u = z[m.value];
+    z[m.value] = l3 ? c2(u.y, -u.x) : u;
+  });
+  quad_butterfly<1, Q>(z, s1);
+  const int k4 = ((q & 1) << 1) | (q >> 1);
+  static_for<0, Q>([&](auto m) {
+    int f = QL::E1 * k4 + QL::E2 * decltype(m)::value;
+    f %= C::N2;
+    const float2 h = tab[f * C::TP];
+    z[m.value] = conj_tab ? cmulc(z[m.value], h) : cmul(z[m.value], h);
+  });
+  // inverse: the mirrored network with w4 = +i, bit-reversed in, natural out
+  quad_butterfly<1, Q>(z, s1);
+  static_for<0, Q>([&](auto m) {
+    const float2 u = z[m.value];
+    z[m.value] = l3 ? c2(-u.y, u.x) : u;
+  });
+  quad_butterfly<2, Q>(z, s2);
+  Dft<Q, 1>::run(z);
+  static_for<0, Q>([&](auto m) {
+    const int e = elem(m);
+    float2 r = z[m.value];
+    if constexpr (!PL::PFA) r = cmul(r, root_at<C::N>((unsigned)(C::N - k1 * e)));
+    base[e * C::TP] = r;
+  });
+}
+
 template <class C, bool SERIAL = false>
 __device__ __forceinline__ void b_spectral(const Tile<C>& t, bool conj_tab) {
   // The B-item index behind an empty asm statement: twiddle offsets derived
   // from it are formed here, not hoisted out of the caller's loops.
   int s = t.s;
   asm volatile("" : "+v"(s));
+  constexpr bool QUAD = QuadLast<C>::ON;
+  constexpr int IBR = QUAD ? C::IB - 1 : C::IB;  // rounds of whole items
   if constexpr (C::N2 >= 16) {
     // long B-items: one at a time, so that their registers are not doubled
 #pragma unroll 1
-    for (int ic = 0; ic < C::IB; ++ic) {
+    for (int ic = 0; ic < IBR; ++ic) {
       const int k1 = s + C::S * ic;
-      if (C::B_FULL || k1 < C::N1) b_spectral_item(t, k1, conj_tab);
+      if (C::B_FULL || QUAD || k1 < C::N1) b_spectral_item(t, k1, conj_tab);
     }
   } else {
-    static_for<0, C::IB>([&](auto ic) {
+    static_for<0, IBR>([&](auto ic) {
       const int k1 = s + C::S * decltype(ic)::value;
-      if (C::B_FULL || k1 < C::N1) b_spectral_item(t, k1, conj_tab);
+      if (C::B_FULL || QUAD || k1 < C::N1) b_spectral_item(t, k1, conj_tab);
       // SERIAL: one item's registers at a time (for kernels that hold other
       // arrays across the B-step)
       if constexpr (SERIAL) __builtin_amdgcn_sched_barrier(0);
     });
   }
+  if constexpr (QUAD) b_spectral_quad<C>(t.lds, conj_tab);
 }
 
 // ---- reductions ------------------------------------------------------------
