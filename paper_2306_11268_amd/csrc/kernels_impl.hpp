@@ -1751,6 +1751,12 @@ template <> struct LayerTile<200, kPropOnce, kRow> { static constexpr int T = 16
 template <> struct LayerTile<200, kFwdMid, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kBwdMid, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kBwdLast, kCol> { static constexpr int T = 32; };
+// 500: the forward passes in one ten-wave workgroup of 32 vectors per CU
+// instead of one five-wave workgroup of 16 (a 68 KB five-wave workgroup
+// leaves no room for a second one on a CU)
+template <> struct LayerTile<500, kPropOnce, kRow> { static constexpr int T = 32; };
+template <> struct LayerTile<500, kFwdMid, kRow> { static constexpr int T = 32; };
+template <> struct LayerTile<500, kFwdMid, kCol> { static constexpr int T = 32; };
 
 template <int N, int KIND, int AXIS>
 using LayerCfg = Cfg<std::conditional_t<AXIS == kRow, typename RowPlanFor<N>::type, typename PlanFor<N>::type>,

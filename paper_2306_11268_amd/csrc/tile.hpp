@@ -36,9 +36,12 @@ struct Cfg {
   // large-N kernels took them all and hid no latency.
   static constexpr int WG_PER_CU = (160 * 1024) / LDS_BYTES;
   static constexpr int WAVES_RAW = (WG_PER_CU * (P / 64)) / 4;
-  static constexpr int WAVES = WAVES_RAW < 2 ? 2 : (WAVES_RAW > 4 ? 4 : WAVES_RAW);
+  // one workgroup must fit: ten waves put three on some SIMD (168 registers)
+  static constexpr int WAVES_MIN = (P / 64 + 3) / 4;
+  static constexpr int WAVES_FIT = WAVES_RAW < WAVES_MIN ? WAVES_MIN : WAVES_RAW;
+  static constexpr int WAVES = WAVES_FIT < 2 ? 2 : (WAVES_FIT > 4 ? 4 : WAVES_FIT);
   // kernels that also carry per-element gradient accumulators
-  static constexpr int WAVES_ACC = WAVES > 2 ? 2 : WAVES;
+  static constexpr int WAVES_ACC = WAVES > 2 ? (WAVES_MIN > 2 ? WAVES_MIN : 2) : WAVES;
   static_assert(P % 64 == 0, "workgroup must be whole wavefronts");
 };
 
