@@ -1760,6 +1760,8 @@ template <> struct LayerTile<500, kFwdMid, kCol> { static constexpr int T = 32; 
 template <> struct LayerTile<1000, kPropOnce, kRow> { static constexpr int T = 16; };
 template <> struct LayerTile<1000, kFwdMid, kRow> { static constexpr int T = 16; };
 template <> struct LayerTile<1000, kFwdMid, kCol> { static constexpr int T = 16; };
+// (its detector-plane passes measured slower at 16: 185 -> 215 us for the seed
+// pass of a 1000 x 1000 training step, batch 16)
 // (the adjoint passes keep 16: at 32 their registers, capped at 168 for ten
 // waves, spill, and the column pass measured slower; so do the detector-plane
 // passes, which transform only the covered rows and measured slower at 32)
