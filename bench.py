@@ -8,7 +8,10 @@ dL/dphi for all five masks.  Inputs are resident in HBM before timing.
 
 Prints one JSON line.  `value` is samples per second over exactly --steps
 steps bracketed by device synchronisation (with --graph the step is recorded
-once as a HIP graph and the timed steps replay it).  The per-kernel durations used for the roofline come
+once as a HIP graph and the timed steps replay it).  The defaults (100 timed
+steps after 20 warm-up steps, about 0.15 s of GPU time at the headline size)
+measure the steady state: over 20 steps after 5 the first steps' clock ramp
+costs about 3%.  The per-kernel durations used for the roofline come
 from HIP events recorded around every kernel launch on the launch stream
 during a second, instrumented run of the same steps.
 """
@@ -31,8 +34,8 @@ HBM_PEAK_GBPS = 8000.0
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", type=int, default=3,
                     help="workload id (3 = 5-layer N=200 train, batch 500, the headline line; 1, 2, 4 and 5 print "
                          "a timing line of their own)")
