@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--layer-passes", action="store_true",
                     help="one pass per layer in the forward call even where the whole-field kernel applies "
                          "(Fresnel, n = n_fft in 64, 100, 128)")
+    ap.add_argument("--whole-field", action="store_true",
+                    help="the whole-field forward kernel wherever it applies, also at n = n_fft = 200 where the "
+                         "layer passes are the default")
     ap.add_argument("--graph", action="store_true",
                     help="record the step once as a HIP graph and time its replays (measured slower than "
                          "launching the kernels one by one on this stack, so not the default)")
@@ -212,7 +215,8 @@ def other_workload(w, batch, args):
 
     def step():
         if det is not None and not train:
-            lb.lr_donn_forward(net, amp, phi, sums=True, layer_passes=args.layer_passes)
+            lb.lr_donn_forward(net, amp, phi, sums=True, layer_passes=args.layer_passes,
+                               whole_field=args.whole_field)
         else:
             lb.lr_donn_forward(net, amp, phi, saved=saved, sums=False, intensity=True)
         if train:
@@ -249,7 +253,7 @@ def other_workload(w, batch, args):
         "data": "synthetic",
         "config": {"workload": w.name, "n": w.n, "n_fft": w.n_fft, "layers": w.layers, "batch": batch,
                    "approx": "fresnel" if w.approx == 0 else "angular_spectrum", "kind": w.kind,
-                   "layer_passes": bool(args.layer_passes)},
+                   "layer_passes": bool(args.layer_passes), "whole_field": bool(args.whole_field)},
         "kernels": {k: {"count": v["count"], "avg_us": 1e3 * v["ms"] / v["count"], "total_ms": v["ms"]}
                     for k, v in kt.items()},
     }))

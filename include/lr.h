@@ -113,7 +113,7 @@ typedef struct lr_donn {
   const lr_c64* d_H;    /* device [n_fft][n_fft], written by lr_tf_build for the same
                            wavelength / pixel_pitch / distance / approx / n_fft.
                            The Fresnel path relies on its separability. */
-  int32_t flags;        /* 0, or LR_ACCUMULATE and / or LR_LAYER_PASSES */
+  int32_t flags;        /* 0, or LR_ACCUMULATE and / or one of LR_LAYER_PASSES, LR_WHOLE_FIELD */
   const lr_c64* d_skip; /* NULL, or device [batch][n][n]: a field added to the
                            detector-plane field before the intensity, the sums,
                            the field output or the backward seed are formed.
@@ -148,6 +148,14 @@ typedef struct lr_donn {
  * field) through memory.  Both paths compute the same outputs (to
  * rounding); the flag exists to compare them. */
 #define LR_LAYER_PASSES 2
+
+/* lr_donn.flags: lr_donn_forward keeps the whole field of a sample on chip
+ * also where one pass per layer is the default: Fresnel path, n == n_fft in
+ * {64, 100, 128, 200}, no saved state, no skip field.  At 200 the field
+ * (320 KB) is held half in shared memory and half in registers; the layer
+ * passes measured faster there, so only this flag selects it.  Not together
+ * with LR_LAYER_PASSES (LR_E_ARG). */
+#define LR_WHOLE_FIELD 4
 
 /* Transfer function of one hop (§3.1.1, Eqs. (fresnel), (sommerfeld), (r01),
  * (forward_diff), (fraunhofer)).

@@ -22,6 +22,7 @@ LR_RS_IR = 3
 LR_FRAUNHOFER = 4
 LR_ACCUMULATE = 1
 LR_LAYER_PASSES = 2
+LR_WHOLE_FIELD = 4
 LR_OP_PROPAGATE = 0
 LR_OP_FORWARD = 1
 LR_OP_BACKWARD = 2
@@ -290,14 +291,15 @@ def _with_skip(desc, skip, b: int, n: int):
 
 def lr_donn_forward(net: Network, amp, phi, saved=None, sums: bool = True, intensity: bool = False,
                     field: bool = False, out_sums=None, out_intensity=None, out_field=None,
-                    accumulate: bool = False, skip=None, layer_passes: bool = False):
+                    accumulate: bool = False, skip=None, layer_passes: bool = False, whole_field: bool = False):
     """Forward pass; returns a dict with the requested outputs (device tensors).
     With accumulate the sums / intensity are added into out_sums / out_intensity
     (LR_ACCUMULATE), which must then be given.  skip: complex64 [B, n, n]
     added to the detector-plane field (lr_donn.d_skip); give the same field
     to lr_donn_backward.  layer_passes: one pass per layer even where the
     whole-field kernel would run (LR_LAYER_PASSES: Fresnel, n == n_fft in
-    {64, 100, 128}, no saved state, no skip)."""
+    {64, 100, 128}, no saved state, no skip).  whole_field: the whole-field
+    kernel wherever it applies, also at n == n_fft == 200 (LR_WHOLE_FIELD)."""
     torch = _torch()
     b = int(amp.shape[0])
     n, L = net.n, net.num_layers
@@ -308,9 +310,14 @@ def lr_donn_forward(net: Network, amp, phi, saved=None, sums: bool = True, inten
             raise ValueError("accumulate needs out_sums / out_intensity and no field output")
         desc = LrDonn.from_buffer_copy(desc)
         desc.flags = LR_ACCUMULATE
+    if layer_passes and whole_field:
+        raise ValueError("layer_passes and whole_field exclude each other")
     if layer_passes:
         desc = LrDonn.from_buffer_copy(desc)
         desc.flags |= LR_LAYER_PASSES
+    if whole_field:
+        desc = LrDonn.from_buffer_copy(desc)
+        desc.flags |= LR_WHOLE_FIELD
     if sums and net.detector.num > 0 and out_sums is None:
         out_sums = torch.empty((b, net.detector.num), dtype=torch.float32, device=dev)
     if intensity and out_intensity is None:

@@ -134,7 +134,8 @@ int validate_detector(const lr_detector& d, int n) {
 
 int validate_net(const lr_donn* net, bool need_layers) {
   if (!net) return LR_E_NULL;
-  if (net->flags & ~(LR_ACCUMULATE | LR_LAYER_PASSES)) return LR_E_ARG;
+  if (net->flags & ~(LR_ACCUMULATE | LR_LAYER_PASSES | LR_WHOLE_FIELD)) return LR_E_ARG;
+  if ((net->flags & LR_LAYER_PASSES) && (net->flags & LR_WHOLE_FIELD)) return LR_E_ARG;
   if (!finite_pos(net->wavelength) || !finite_pos(net->pixel_pitch) || !std::isfinite(net->distance))
     return LR_E_ARG;
   if (net->approx < LR_FRESNEL || net->approx > LR_FRAUNHOFER) return LR_E_APPROX;
@@ -813,7 +814,8 @@ int lr_donn_forward(const lr_donn* net, int32_t batch, const float* d_amp, const
   a.full = slot_ordered(net) ? 1 : 0;
   const int tile_t = lr::tile_shape(N, 0).T;
   int sum_tiles = L.ntiles_vec;  // tiles that wrote partial detector sums
-  const bool whole_field = net->approx == LR_FRESNEL && n == N && lr::field_forward_preferred(N, batch) && !saved &&
+  const bool whole_field = net->approx == LR_FRESNEL && n == N && lr::field_forward_supported(N) &&
+                           ((net->flags & LR_WHOLE_FIELD) || lr::field_forward_preferred(N, batch)) && !saved &&
                            (d_sums || d_intensity || d_field_out) && !net->d_skip &&
                            !(net->flags & LR_LAYER_PASSES);
   if (whole_field) {

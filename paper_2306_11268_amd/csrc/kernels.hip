@@ -459,10 +459,10 @@ SlotMap slot_map(int N) {
   }
 }
 
-bool field_forward_supported(int N) { return N == 64 || N == 100 || N == 128; }
+bool field_forward_supported(int N) { return N == 64 || N == 100 || N == 128 || N == 200; }
 
 bool field_forward_preferred(int N, int batch) {
-  if (!field_forward_supported(N)) return false;
+  if (!field_forward_supported(N) || N == 200) return false;
   if (N == 64) return true;
   int dev = 0;
   int cus = 0;
@@ -477,6 +477,7 @@ hipError_t launch_field_forward(int N, const FieldArgs& a, hipStream_t st) {
     case 64: return launch_field_fwd_n<64>(a, st);
     case 100: return launch_field_fwd_n<100>(a, st);
     case 128: return launch_field_fwd_n<128>(a, st);
+    case 200: return launch_field_fwd_n<200>(a, st);
     default: return hipErrorInvalidValue;
   }
 }

@@ -137,8 +137,10 @@ struct Regions {
 
 
 // Whole-field forward (field_forward_kernel): one workgroup per sample holds
-// the N x N field in shared memory through every layer, for the grids whose
-// field fits there (N = 64, 100, 128, full aperture), Fresnel path.  Outputs:
+// the N x N field on chip through every layer, for the grids whose field
+// fits there (N = 64, 100, 128 in shared memory; N = 200 half in shared
+// memory and half in registers, field_forward_split_kernel), full aperture,
+// Fresnel path.  Outputs:
 // region-sum partials [B][K] (for launch_finish_sums with one tile), the
 // intensity map and the detector-plane field.
 struct FieldArgs {
@@ -161,6 +163,7 @@ bool field_forward_supported(int N);
 // leaves CUs idle and the layer passes are faster, except at N = 64 where
 // the passes are launch-bound (5-layer forward, batch 64: 42 against 44 us
 // at N = 64, 103 against 88 us at N = 100, 107 against 84 us at N = 128).
+// Never at N = 200, where the layer passes measured faster.
 bool field_forward_preferred(int N, int batch);
 hipError_t launch_field_forward(int N, const FieldArgs& a, hipStream_t st);
 

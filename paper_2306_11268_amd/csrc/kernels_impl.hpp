@@ -1667,9 +1667,308 @@ __global__ void __launch_bounds__(PL::N * PL::N2) field_forward_kernel(FieldArgs
   }
 }
 
+// ---------------------------------------------------------------------------
+// Whole-field forward at N = 200 (25 x 8 Good-Thomas): the 320 KB field is
+// twice a CU's shared memory, so half of it lives there and half in
+// registers.  Thread (v, j), v < 100, j < 8 (800 threads), holds in R[25]
+// A-item j of vector 100 + v; shared memory holds vectors 0..99.  Along x
+// ("row phase") the vectors are rows; along y ("column phase") columns.
+//
+// Shared layout: row r < 100 of the stored field (slot order on both axes)
+// at rowaddr(r) = 200 r + r / 4 (the skew keeps the 32 rows a half wave
+// touches at once in distinct bank pairs).  Quadrants by slot: Q1 (sy, sx
+// < 100) stays at rowaddr(sy) + sx in both phases; Q2 (sy < 100 <= sx) is
+// at rowaddr(sy) + sx in the row phase, in registers (by column) in the
+// column phase; Q3 (sx < 100 <= sy) is in registers (by row) in the row
+// phase and at rowaddr(sy - 100) + 100 + sx (Q2's place) in the column
+// phase; Q4 is always in registers.  A phase change moves Q2, Q3 and Q4
+// through shared memory in four steps (read the quadrant leaving shared
+// memory into the new register layout, park Q4 in the freed region, read
+// it back in the new layout, store the quadrant entering shared memory).
+//
+// A 1-D propagation of the whole field transforms the shared half (A-step
+// from and to shared memory, B-step there, inverse A-step into registers x),
+// then the register half through the same shared buffer, then writes x back.
+// After the last hop the intensities of all 40000 pixels replace the field in
+// shared memory (4 bytes each), and the region sums and intensity map read
+// them there.
+// ---------------------------------------------------------------------------
+template <class PL>
+struct SplitCfg {
+  using Plan = PL;
+  static constexpr int N = PL::N;
+  static constexpr int N1 = PL::N1;
+  static constexpr int N2 = PL::N2;
+  static constexpr int H = N / 2;   // vectors in shared memory
+  static constexpr int P = H * N2;  // threads
+  static constexpr int LDS = H * N + H / 4;
+  static_assert(N == 200 && N1 == 25 && N2 == 8 && PL::PFA, "the split whole-field layout is written for 25 x 8");
+  static_assert(N * N * 4 <= LDS * 8, "the intensity map must fit where the field half was");
+  __device__ static constexpr int rowaddr(int r) { return r * N + (r >> 2); }
+  // rowaddr(j + 8x) = rowaddr(j) + XS * x for j < 8
+  static constexpr int XS = 8 * N + 2;
+  // rowaddr(s - H) + H = rowaddr(s) - SHIFT for s >= H
+  static constexpr int SHIFT = H * N + H / 4 - H;
+  // first A-item element with slot j + 8x >= H: x = 12 for j >= 4, 13 below
+  static constexpr int XH = H / N2;  // 12
+};
+
+template <class PL>
+__global__ void __launch_bounds__(SplitCfg<PL>::P) field_forward_split_kernel(FieldArgs a) {
+  using C = SplitCfg<PL>;
+  constexpr int N = C::N;
+  constexpr int N1 = C::N1;
+  constexpr int N2 = C::N2;
+  constexpr int H = C::H;
+  constexpr int P = C::P;
+  constexpr int XS = C::XS;
+  constexpr int SHIFT = C::SHIFT;
+  constexpr int XH = C::XH;
+  __shared__ float2 f[C::LDS];
+  __shared__ float2 tabx[N];
+  __shared__ float2 taby[N];
+
+  const int b = (int)blockIdx.x;
+  const int tid = (int)threadIdx.x;
+  const int v = tid % H;
+  const int j = tid / H;
+  const size_t nn = (size_t)N * N;
+  // element XH of the A-item lies in the upper half (slot >= H) for j >= N2 / 2
+  const bool up12 = j + N2 * XH >= H;
+
+  for (int i = tid; i < N; i += P) {
+    const int fr = PL::freq(i / N2, i % N2);
+    tabx[i] = a.chirp_x[fr];
+    taby[i] = a.chirp_y[fr];
+  }
+  // amplitudes (natural, zero phase) into the row phase: shared rows sy < H,
+  // registers rows H + v
+  const float* __restrict__ amp = a.amp + (size_t)b * nn;
+  for (int e = tid; e < H * N; e += P) {
+    const int sy = e / N;
+    const int sx = e - sy * N;
+    f[C::rowaddr(sy) + sx] = c2(amp[(size_t)PL::pos_of_slot(sy) * N + PL::pos_of_slot(sx)], 0.f);
+  }
+  float2 R[N1];
+  {
+    const int y = PL::pos_of_slot(H + v);
+    static_for<0, N1>([&](auto x) { R[x.value] = c2(amp[(size_t)y * N + PL::pos_of_slot(j + N2 * x.value)], 0.f); });
+  }
+  __syncthreads();
+
+  // A-item j of shared vector v, element x: row phase rowaddr(v) + j + 8x;
+  // column phase rowaddr(j + 8x) + v, less SHIFT in the upper half
+  const int arow = C::rowaddr(v) + j;
+  const int acol = C::rowaddr(j) + v;
+  auto a_addr = [&](auto rows_c, auto x_c) -> int {
+    constexpr int x = decltype(x_c)::value;
+    if constexpr (decltype(rows_c)::value) {
+      return arow + N2 * x;
+    } else if constexpr (x < XH) {
+      return acol + XS * x;
+    } else if constexpr (x > XH) {
+      return acol + XS * x - SHIFT;
+    } else {
+      return acol + XS * x - (up12 ? SHIFT : 0);
+    }
+  };
+  auto a_load = [&](auto rows_c, float2(&x)[N1]) {
+    static_for<0, N1>([&](auto k) { x[k.value] = f[a_addr(rows_c, k)]; });
+  };
+  auto a_store = [&](auto rows_c, const float2(&x)[N1]) {
+    static_for<0, N1>([&](auto k) { f[a_addr(rows_c, k)] = x[k.value]; });
+  };
+  // spectral B-step of the shared half: B-items k1 = j, j + 8, ... of vector v
+  auto b_step = [&](auto rows_c) {
+    constexpr bool ROWS = decltype(rows_c)::value;
+    const float2* tab = ROWS ? tabx : taby;
+    for (int k1 = j; k1 < N1; k1 += N2) {
+      int base;
+      int off_lo = 0;
+      int off_hi = 0;
+      if constexpr (ROWS) {
+        base = C::rowaddr(v) + N2 * k1;
+      } else {
+        // rowaddr(8 k1 + q) = XS k1 + N q + q / 4; slots >= H shift down
+        base = XS * k1 + v;
+        off_lo = N2 * k1 >= H ? -SHIFT : 0;           // elements q < 4
+        off_hi = N2 * k1 + N2 / 2 >= H ? -SHIFT : 0;  // elements q >= 4
+      }
+      auto addr = [&](auto q_c) {
+        constexpr int q = decltype(q_c)::value;
+        if constexpr (ROWS) {
+          return base + q;
+        } else {
+          return base + N * q + (q >> 2) + (q < N2 / 2 ? off_lo : off_hi);
+        }
+      };
+      float2 y[N2];
+      static_for<0, N2>([&](auto q) { y[q.value] = f[addr(q)]; });
+      Dft<N2, -1>::run(y);
+      static_for<0, N2>([&](auto q) { y[q.value] = cmul(y[q.value], tab[N2 * k1 + q.value]); });
+      Dft<N2, 1>::run(y);
+      static_for<0, N2>([&](auto q) { f[addr(q)] = y[q.value]; });
+    }
+  };
+  // 1-D propagation of the whole field along the phase's axis
+  auto prop = [&](auto rows_c) {
+    float2 x[N1];
+    a_load(rows_c, x);
+    Dft<N1, -1>::run(x);
+    a_store(rows_c, x);
+    __syncthreads();
+    b_step(rows_c);
+    __syncthreads();
+    a_load(rows_c, x);
+    Dft<N1, 1>::run(x);
+    __syncthreads();
+    Dft<N1, -1>::run(R);
+    a_store(rows_c, R);
+    __syncthreads();
+    b_step(rows_c);
+    __syncthreads();
+    a_load(rows_c, R);
+    Dft<N1, 1>::run(R);
+    __syncthreads();
+    a_store(rows_c, x);
+    __syncthreads();
+  };
+  // phase changes; T[x] holds the new register layout's element x
+  auto to_cols = [&] {
+    float2 T[N1];
+    // Q2 (shared, row phase) -> registers by column: column H + v, slot j + 8x < H
+    static_for<0, XH + 1>([&](auto x) {
+      if (x.value < XH || !up12) T[x.value] = f[acol + XS * x.value + H];
+    });
+    __syncthreads();
+    // Q4 (registers by row: row H + v, slot j + 8x >= H) parked at rowaddr(v) + j + 8x
+    static_for<XH, N1>([&](auto x) {
+      if (x.value > XH || up12) f[arow + N2 * x.value] = R[x.value];
+    });
+    __syncthreads();
+    // Q4 by column: column H + v, slot sy = j + 8x >= H, parked at rowaddr(sy - H) + H + v
+    static_for<XH, N1>([&](auto x) {
+      if (x.value > XH || up12) T[x.value] = f[acol + XS * x.value - SHIFT];
+    });
+    __syncthreads();
+    // Q3 (registers by row: row H + v, slot j + 8x < H) to rowaddr(v) + H + j + 8x
+    static_for<0, XH + 1>([&](auto x) {
+      if (x.value < XH || !up12) f[arow + N2 * x.value + H] = R[x.value];
+    });
+    static_for<0, N1>([&](auto x) { R[x.value] = T[x.value]; });
+    __syncthreads();
+  };
+  auto to_rows = [&] {
+    float2 T[N1];
+    // Q3 (shared, column phase, at rowaddr(v) + H + sx) -> registers by row
+    static_for<0, XH + 1>([&](auto x) {
+      if (x.value < XH || !up12) T[x.value] = f[arow + N2 * x.value + H];
+    });
+    __syncthreads();
+    // Q4 (registers by column: column H + v, slot sy = j + 8x >= H) parked at rowaddr(sy - H) + H + v
+    static_for<XH, N1>([&](auto x) {
+      if (x.value > XH || up12) f[acol + XS * x.value - SHIFT] = R[x.value];
+    });
+    __syncthreads();
+    // Q4 by row: row H + v, slot sx = j + 8x >= H, parked at rowaddr(v) + sx
+    static_for<XH, N1>([&](auto x) {
+      if (x.value > XH || up12) T[x.value] = f[arow + N2 * x.value];
+    });
+    __syncthreads();
+    // Q2 (registers by column: column H + v, slot sy = j + 8x < H) to rowaddr(sy) + H + v
+    static_for<0, XH + 1>([&](auto x) {
+      if (x.value < XH || !up12) f[acol + XS * x.value + H] = R[x.value];
+    });
+    static_for<0, N1>([&](auto x) { R[x.value] = T[x.value]; });
+    __syncthreads();
+  };
+
+  for (int hop = 1; hop <= a.layers + 1; ++hop) {
+    prop(std::true_type{});
+    to_cols();
+    prop(std::false_type{});
+    if (hop <= a.layers) {
+      // U_l = gamma exp(j phi_l) A_l on both halves; table [sy][sx] or [sx][sy] in slot order
+      const float2* __restrict__ m = a.mod + (size_t)(hop - 1) * nn;
+      const bool tr = (a.mod_t >> (hop - 1)) & 1ull;
+      for (int e = tid; e < H * N; e += P) {
+        const int sy = e / H;
+        const int sx = e - sy * H;
+        float2& u = f[sy < H ? C::rowaddr(sy) + sx : C::rowaddr(sy - H) + H + sx];
+        u = cmul(u, m[tr ? (size_t)sx * N + sy : (size_t)sy * N + sx]);
+      }
+      static_for<0, N1>([&](auto x) {
+        const int sy = j + N2 * x.value;
+        const int sx = H + v;
+        R[x.value] = cmul(R[x.value], m[tr ? (size_t)sx * N + sy : (size_t)sy * N + sx]);
+      });
+      __syncthreads();
+      to_rows();
+    }
+  }
+
+  // detector plane (column phase): the complex field out, then every
+  // pixel's intensity into shared memory, slot order [sy][sx]
+  float2* __restrict__ fo = a.field_out ? a.field_out + (size_t)b * nn : nullptr;
+  float il[N1];
+  float ir[N1];
+  static_for<0, N1>([&](auto i) {
+    const int e = tid + P * i.value;
+    const int sy = e / H;
+    const int sx = e - sy * H;
+    const float2 u = f[sy < H ? C::rowaddr(sy) + sx : C::rowaddr(sy - H) + H + sx];
+    il[i.value] = fmaf(u.x, u.x, u.y * u.y);
+    if (fo) fo[(size_t)PL::pos_of_slot(sy) * N + PL::pos_of_slot(sx)] = u;
+  });
+  static_for<0, N1>([&](auto x) {
+    const float2 u = R[x.value];
+    ir[x.value] = fmaf(u.x, u.x, u.y * u.y);
+    if (fo) fo[(size_t)PL::pos_of_slot(j + N2 * x.value) * N + PL::pos_of_slot(H + v)] = u;
+  });
+  __syncthreads();
+  float* const inten = reinterpret_cast<float*>(f);
+  static_for<0, N1>([&](auto i) {
+    const int e = tid + P * i.value;
+    const int sy = e / H;
+    const int sx = e - sy * H;
+    inten[sy * N + sx] = il[i.value];
+  });
+  static_for<0, N1>([&](auto x) { inten[(j + N2 * x.value) * N + H + v] = ir[x.value]; });
+  __syncthreads();
+
+  // S_k = sum of I over region k: wave w sums regions w, w + waves, ... over
+  // natural pixels in a fixed order (lane stride 64, then a fixed butterfly)
+  constexpr int NW = P / 64;  // whole waves (the last one has 32 lanes and sums nothing)
+  const int wv = tid >> 6;
+  const int lane = tid & 63;
+  const int side = a.reg.s;
+  for (int k = wv; wv < NW && k < a.reg.K; k += NW) {
+    const int y0 = a.reg.y0[k];
+    const int x0 = a.reg.x0[k];
+    float acc = 0.f;
+    for (int e = lane; e < side * side; e += 64) {
+      const int dy = e / side;
+      const int y = y0 + dy;
+      const int x = x0 + (e - dy * side);
+      acc += inten[PL::slot_of_pos(y) * N + PL::slot_of_pos(x)];
+    }
+    for (int o = 32; o >= 1; o >>= 1) acc += __shfl_xor(acc, o, 64);
+    if (lane == 0) a.sums_part[(size_t)b * a.reg.K + k] = acc;
+  }
+  if (a.intensity) {
+    float* __restrict__ io = a.intensity + (size_t)b * nn;
+    for (int e = tid; e < N * N; e += P) {
+      const int y = e / N;
+      const int x = e - y * N;
+      const float in = inten[PL::slot_of_pos(y) * N + PL::slot_of_pos(x)];
+      io[e] = a.accumulate ? io[e] + in : in;
+    }
+  }
+}
+
 template <int N>
 constexpr bool whole_field_size() {
-  return N == 64 || N == 100 || N == 128;
+  return N == 64 || N == 100 || N == 128 || N == 200;
 }
 
 template <int N>
@@ -1680,7 +1979,11 @@ hipError_t launch_field_fwd_n(const FieldArgs& a, hipStream_t st) {
     if (a.batch < 1 || a.layers < 0 || a.layers > 64 || a.reg.K < 0 || a.reg.K > kMaxRegions ||
         (a.reg.K > 0 && !a.sums_part))
       return hipErrorInvalidValue;
-    hipLaunchKernelGGL((field_forward_kernel<PL>), dim3(a.batch), dim3(PL::N * PL::N2), 0, st, a);
+    if constexpr (N == 200) {
+      hipLaunchKernelGGL((field_forward_split_kernel<PL>), dim3(a.batch), dim3(SplitCfg<PL>::P), 0, st, a);
+    } else {
+      hipLaunchKernelGGL((field_forward_kernel<PL>), dim3(a.batch), dim3(PL::N * PL::N2), 0, st, a);
+    }
     return hipGetLastError();
   } else {
     return hipErrorInvalidValue;

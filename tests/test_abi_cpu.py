@@ -114,12 +114,16 @@ def test_entry_points_reject_bad_arguments_without_touching_the_gpu():
     assert _ws(far, 4, 1) == -4 and _ws(far, 4, 2) == -4
     assert lib.lr_propagate(ctypes.byref(far), 2, dummy, P(0x3000), 1, dummy, 1 << 30, None) == 3
     assert _ws(_net(approx=5), 4, 0) == -4
-    # flags: unknown bits; accumulating outputs cannot include the field
+    # flags: unknown bits, both path flags at once; accumulating outputs cannot include the field
     bad = _net()
-    bad.flags = 4
+    bad.flags = 8
+    assert _ws(bad, 4, 1) == -3
+    bad.flags = 6  # LR_LAYER_PASSES | LR_WHOLE_FIELD
     assert _ws(bad, 4, 1) == -3
     ok = _net()
     ok.flags = 3  # LR_ACCUMULATE | LR_LAYER_PASSES
+    assert _ws(ok, 4, 1) > 0
+    ok.flags = 5  # LR_ACCUMULATE | LR_WHOLE_FIELD
     assert _ws(ok, 4, 1) > 0
     acc = _net(det=lb.LrDetector(0, 1, None, None))
     acc.flags = 1

@@ -5,8 +5,10 @@ layer path on the same inputs.
 It runs for forward calls on the Fresnel path with n == n_fft in
 {64, 100, 128}, no saved state, no skip field, and at 100 and 128 at least
 one sample per CU (256 on MI355X; smaller batches take the layer passes);
-LR_LAYER_PASSES forces the layer passes.  Every case checks, from the
-library's own launch record, which path ran.  Tolerance: relative L2 1e-4
+LR_LAYER_PASSES forces the layer passes.  At n == n_fft == 200 the field is
+held half in shared memory and half in registers, and only LR_WHOLE_FIELD
+selects it.  Every case checks, from the library's own launch record, which
+path ran.  Tolerance: relative L2 1e-4
 (the stated bound for fields and intensities).
 """
 
@@ -118,3 +120,45 @@ def test_whole_field_forward_full_map_outputs(lrb, m, layers, b):
     acc = dev(base)
     lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=False, intensity=True, out_intensity=acc, accumulate=True)
     assert rel(host(acc) - base, ref["intensity"]) < TOL
+
+
+@pytest.mark.parametrize("b", [256, 3])
+def test_whole_field_forward_200_split_field(lrb, b):
+    # the 200 x 200 field half in shared memory, half in registers
+    net, amp, phi, ref = setup(lrb, 200, b)
+    assert not ran_whole_field(lrb, lambda: lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True))
+    out = {}
+    assert ran_whole_field(lrb, lambda: out.update(
+        lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True, whole_field=True)))
+    whole = host(out["sums"])
+    passes = host(lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True)["sums"])
+    assert rel(whole, ref["sums"]) < TOL
+    assert rel(whole, passes) < TOL
+    again = host(lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True, whole_field=True)["sums"])
+    assert np.array_equal(whole, again)
+
+
+@pytest.mark.parametrize("layers,b", [(1, 2), (2, 3), (4, 5)])
+def test_whole_field_forward_200_full_map_outputs(lrb, layers, b):
+    # every pixel of both halves: intensity map and detector-plane field against
+    # the oracle, with and without the sums, and the accumulated intensity
+    net, amp, phi, ref = setup(lrb, 200, b, layers=layers, gamma=1.1)
+    for sums in (False, True):
+        out = {}
+        assert ran_whole_field(lrb, lambda: out.update(
+            lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=sums, intensity=True, field=True, whole_field=True)))
+        assert rel(host(out["intensity"]), ref["intensity"]) < TOL
+        assert rel(host(out["field"]), ref["field"]) < TOL
+        if sums:
+            assert rel(host(out["sums"]), ref["sums"]) < TOL
+    base = np.full((b, 200, 200), 0.5, dtype=np.float32)
+    acc = dev(base)
+    lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=False, intensity=True, out_intensity=acc, accumulate=True,
+                        whole_field=True)
+    assert rel(host(acc) - base, ref["intensity"]) < TOL
+
+
+def test_whole_field_flags_exclude_each_other(lrb):
+    net, amp, phi, _ = setup(lrb, 64, 2, layers=1)
+    with pytest.raises(ValueError):
+        lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True, layer_passes=True, whole_field=True)
