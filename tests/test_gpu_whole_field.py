@@ -158,6 +158,17 @@ def test_whole_field_forward_200_full_map_outputs(lrb, layers, b):
     assert rel(host(acc) - base, ref["intensity"]) < TOL
 
 
+@pytest.mark.parametrize("m", [100, 128])
+def test_whole_field_flag_below_one_sample_per_cu(lrb, m):
+    # LR_WHOLE_FIELD takes the whole-field kernel where the default would not
+    # (a batch below the CU count at 100 and 128 points)
+    net, amp, phi, ref = setup(lrb, m, 3)
+    out = {}
+    assert ran_whole_field(lrb, lambda: out.update(
+        lrb.lr_donn_forward(net, dev(amp), dev(phi), sums=True, whole_field=True)))
+    assert rel(host(out["sums"]), ref["sums"]) < TOL
+
+
 def test_whole_field_flags_exclude_each_other(lrb):
     net, amp, phi, _ = setup(lrb, 64, 2, layers=1)
     with pytest.raises(ValueError):
