@@ -2,7 +2,8 @@
 // FFT length and tile width the kernels can use, the entry of (slot, vector)
 // -- including the table column v = T -- is distinct and inside the buffer
 // (below the spare slot), the spare slot fits, and the workgroup's shared
-// memory fits a CU.  The bank spread of the A- and B-step accesses (lanes per
+// memory fits a CU, and the register budget (waves per SIMD the kernels ask
+// the compiler for) lets one workgroup's waves fit the CU's four SIMDs.  The bank spread of the A- and B-step accesses (lanes per
 // 8-byte bank pair; two is the minimum for 8-byte accesses) is printed for
 // the record.  Runs on the host only; no kernel is launched.
 #include <cstdio>
@@ -24,6 +25,12 @@ static bool check_cfg() {
   }
   if (C::SPARE + C::TP > C::LDS_ELEMS) ok = false;
   if (C::LDS_BYTES > 160 * 1024) ok = false;
+  // the register budget the kernels ask for lets one workgroup fit a CU: its
+  // waves spread over 4 SIMDs need ceil(waves / 4) per SIMD (512 / that
+  // registers), with and without gradient accumulators
+  const int waves = C::P / 64;
+  const int need = (waves + 3) / 4;
+  if (C::WAVES < need || C::WAVES_ACC < need) ok = false;
   // B-step access: lane l of a wave works on B-item k1 = l / T (+ wave offset)
   // and vector v = l % T, all at the same element j
   int worst = 0;
@@ -72,6 +79,9 @@ int main() {
   ok &= check_size<256>(); ok &= check_size<350>(); ok &= check_size<400>(); ok &= check_size<500>(); ok &= check_size<512>();
   ok &= check_size<1000>(); ok &= check_size<1024>();
   ok &= check_cfg<lr::PlanFor<200>::type, 24>();
+  // the ten-wave forward tiles of 500 and 1000 points
+  ok &= check_cfg<lr::PlanFor<500>::type, 32>();
+  ok &= check_cfg<lr::PlanFor<1000>::type, 16>();
   std::printf(ok ? "ALL OK\n" : "FAILURES\n");
   return ok ? 0 : 1;
 }
