@@ -233,10 +233,12 @@ T* at(void* base, size_t off) {
 
 // The separable path alternates axes: pass p (1-based) runs along rows for odd p.
 Axis pass_axis(int p) { return (p & 1) ? lr::kRow : lr::kCol; }
-// Layer l (1-based) is modulated in pass l+1: transposed storage when that pass is a row pass.
+// Layer l (1-based) is modulated in pass l+1: transposed storage when that pass is a row pass,
+// except on the wide row tiles of the 500-point plan (full aperture), which read rows.
 int layer_transposed(const lr_donn* net, int l) {
   if (net->approx != LR_FRESNEL) return 1;
-  return pass_axis(l + 1) == lr::kRow ? 1 : 0;
+  if (pass_axis(l + 1) != lr::kRow) return 0;
+  return lr::wide_row_tiles(net->n_fft) && net->n == net->n_fft ? 0 : 1;
 }
 
 const char* kind_name(int k) {

@@ -459,6 +459,8 @@ SlotMap slot_map(int N) {
   }
 }
 
+bool wide_row_tiles(int N) { return N == 500; }
+
 bool field_forward_supported(int N) { return N == 64 || N == 100 || N == 128 || N == 200; }
 
 bool field_forward_preferred(int N, int batch) {

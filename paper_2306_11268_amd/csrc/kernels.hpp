@@ -157,6 +157,10 @@ struct FieldArgs {
   int accumulate;              // intensity is added to the output
   int batch;
 };
+// Whether the row layer passes of this FFT length run on the wide row tiles
+// (wide_row_pass, N = 500, full aperture), whose modulation tables and dphi
+// partials are [row][col] instead of the row passes' [col][row].
+bool wide_row_tiles(int N);
 bool field_forward_supported(int N);
 // Whether a forward call of this size and batch should take the whole-field
 // kernel: it runs one sample per workgroup, so below one sample per CU it

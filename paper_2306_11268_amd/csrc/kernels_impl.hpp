@@ -1522,6 +1522,201 @@ __global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 
 }
 
 // ---------------------------------------------------------------------------
+// Row layer passes at N = 500 (25 x 20 Cooley-Tukey) on wave tiles.  The
+// 16-vector workgroup tiles this plan needs are five waves of 68 KB, which
+// run alone on their CU; here a workgroup is one wave of 17 KB and
+// transforms 3 whole rows.  Lane (r, j), r = lane / 20, j = lane mod 20,
+// holds A-item j of row r in registers (lanes 60..63 read row 0's items,
+// write nothing and touch no global memory).  The exchange runs through a
+// private buffer, slot s of row r at r * 525 + s + s / 20, so that the
+// elements of the A-items and the 20 B-items a wave reads at once start in
+// distinct bank pairs; B-items k1 < 20 go one per lane, the five left
+// (k1 = 20..24) one per lane quad, split by Good-Thomas 4 x 5 as in
+// b_spectral_quad.  Fields, this layer's modulation table and the dphi
+// partials are [vec][q] (rows, slot order): consecutive lanes read
+// consecutive slots of a row.  Forward (kFwdMid): one item per workgroup;
+// adjoint (kBwdMid): persistent, as fresnel_pass.
+// ---------------------------------------------------------------------------
+template <class PL>
+struct WideRows {
+  static constexpr int N = PL::N;
+  static constexpr int N1 = PL::N1;
+  static constexpr int N2 = PL::N2;
+  static constexpr int R = 64 / N2;      // rows per wave
+  static constexpr int P1 = N2 + 1;      // buffer stride of a B-item
+  static constexpr int PR = P1 * N1;     // buffer pitch of a row
+  static constexpr int Q = N2 / 4;       // the quad split's odd factor
+  static constexpr int E1 = Q * inv_mod(Q % 4, 4);
+  static constexpr int E2 = 4 * inv_mod(4 % Q, Q);
+  static_assert(N == 500 && N1 == 25 && N2 == 20 && !PL::PFA, "wide row tiles are written for 25 x 20");
+  static_assert(N1 - N2 == Q, "the last round is one item per quad");
+};
+
+template <class PL, int KIND>
+__global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(PassArgs a) {
+  using W = WideRows<PL>;
+  constexpr int N = W::N;
+  constexpr int N1 = W::N1;
+  constexpr int N2 = W::N2;
+  constexpr int R = W::R;
+  constexpr int P1 = W::P1;
+  constexpr int PR = W::PR;
+  constexpr int Q = W::Q;
+  constexpr bool ACC = KIND == kBwdMid;
+  static_assert(KIND == kFwdMid || KIND == kBwdMid, "wide row tiles run the middle layer kinds");
+  __shared__ float2 tab[PR];       // chirp: B-item k1, frequency k2 at P1 * k1 + k2
+  __shared__ float2 xch[R * PR];   // R rows
+
+  const int rank = (int)blockIdx.x;
+  if (rank >= a.workers) return;
+  const int lane = (int)threadIdx.x;
+  const bool act = lane < R * N2;
+  const int r = act ? lane / N2 : 0;
+  const int j = act ? lane - r * N2 : lane - R * N2;
+  const int total = a.ntiles * a.batch;
+  const size_t nn = (size_t)N * N;
+  const bool cj = a.conj_tab != 0;
+
+  for (int i = lane; i < N; i += 64) tab[P1 * (i / N2) + i % N2] = a.tab[PL::freq(i / N2, i % N2)];
+  float acc[ACC ? N1 : 1];
+  if constexpr (ACC) {
+    static_for<0, N1>([&](auto k) { acc[k.value] = 0.f; });
+  }
+
+  // one 1-D propagation of this lane's A-item along its row.  The lane's
+  // indices pass through an empty asm statement at every call, so the
+  // twiddles and addresses derived from them are formed here and not kept
+  // live across the item loop; scheduling barriers keep each phase's loads
+  // (data, twiddles, table) next to their use, as in b_spectral_item.
+  auto prop = [&](float2(&v)[N1], bool conj_t) {
+    int jo = j;
+    int ro = r;
+    asm volatile("" : "+v"(jo), "+v"(ro));
+    Dft<N1, -1>::run(v);
+    float2* const xr = xch + ro * PR;
+    if (act) {
+      static_for<0, N1>([&](auto x) { xr[P1 * x.value + jo] = v[x.value]; });
+    }
+    __syncthreads();
+    if (act) {
+      // B-item k1 = j of row r
+      float2* const yb = xr + P1 * jo;
+      const float2* const tk = tab + P1 * jo;
+      float2 y[N2];
+      static_for<0, N2>([&](auto q) { y[q.value] = yb[q.value]; });
+      static_for<1, N2>([&](auto q) { y[q.value] = cmul(y[q.value], root_at<N>((unsigned)(jo * q.value))); });
+      Dft<N2, -1>::run(y);
+      __builtin_amdgcn_sched_barrier(0);
+      if (conj_t) {
+        static_for<0, N2>([&](auto q) { y[q.value] = cmulc(y[q.value], tk[q.value]); });
+      } else {
+        static_for<0, N2>([&](auto q) { y[q.value] = cmul(y[q.value], tk[q.value]); });
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      Dft<N2, 1>::run(y);
+      static_for<1, N2>(
+          [&](auto q) { y[q.value] = cmul(y[q.value], root_at<N>((unsigned)(N - jo * q.value))); });
+      static_for<0, N2>([&](auto q) { yb[q.value] = y[q.value]; });
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (lane < R * N2) {
+      // B-items k1 = N2 .. N1-1: item qi = lane / 4 (row qi / Q, k1 = N2 + qi mod Q), one per quad
+      // (the last quad, lanes 60..63, has none)
+      int t = lane;
+      asm volatile("" : "+v"(t));
+      const int qi = t >> 2;
+      const int qq = t & 3;
+      const int qrow = qi / Q;
+      const int k1 = N2 + qi - qrow * Q;
+      float2* const base = xch + qrow * PR + P1 * k1;
+      const float2* const tq = tab + P1 * k1;
+      auto elem = [&](auto m) {
+        const int e = Q * qq + 4 * decltype(m)::value;
+        return e >= N2 ? e - N2 : e;
+      };
+      const float s1 = (qq & 1) ? -1.f : 1.f;
+      const float s2 = (qq & 2) ? -1.f : 1.f;
+      const bool l3 = qq == 3;
+      float2 z[Q];
+      static_for<0, Q>([&](auto m) {
+        const int e = elem(m);
+        z[m.value] = cmul(base[e], root_at<N>((unsigned)(k1 * e)));
+      });
+      Dft<Q, -1>::run(z);
+      quad_butterfly<2, Q>(z, s2);
+      static_for<0, Q>([&](auto m) {
+        const float2 u = z[m.value];
+        z[m.value] = l3 ? c2(u.y, -u.x) : u;
+      });
+      quad_butterfly<1, Q>(z, s1);
+      const int k4 = ((qq & 1) << 1) | (qq >> 1);
+      static_for<0, Q>([&](auto m) {
+        const int f = (W::E1 * k4 + W::E2 * decltype(m)::value) % N2;
+        z[m.value] = conj_t ? cmulc(z[m.value], tq[f]) : cmul(z[m.value], tq[f]);
+      });
+      quad_butterfly<1, Q>(z, s1);
+      static_for<0, Q>([&](auto m) {
+        const float2 u = z[m.value];
+        z[m.value] = l3 ? c2(-u.y, u.x) : u;
+      });
+      quad_butterfly<2, Q>(z, s2);
+      Dft<Q, 1>::run(z);
+      static_for<0, Q>([&](auto m) {
+        const int e = elem(m);
+        base[e] = cmul(z[m.value], root_at<N>((unsigned)(N - k1 * e)));
+      });
+    }
+    __syncthreads();
+    static_for<0, N1>([&](auto x) { v[x.value] = xr[P1 * x.value + jo]; });
+    Dft<N1, 1>::run(v);
+  };
+
+  // element x of this lane's A-item: [vec][q] offset vec * N + j + N2 * x
+  for (int it = rank; it < total; it += a.workers) {
+    const int tile = it % a.ntiles;
+    const int b = it / a.ntiles;
+    const int vec = tile * R + r;
+    const bool vok = act && vec < a.nvec;
+    const unsigned base = vok ? (unsigned)(vec * N + j) * 8u : kOutOfRange;
+    const Rsrc rin = make_rsrc(static_cast<const float2*>(a.in) + (size_t)b * nn, (unsigned)nn * 8u);
+    const Rsrc rmod = make_rsrc(a.mod, (unsigned)nn * 8u);
+    float2 x[N1];
+    if constexpr (ACC) {
+      // A_l from the saved input of the forward pass, then G's half hop
+      float2 ar[N1];
+      const Rsrc ract = make_rsrc(a.act_in + (size_t)b * nn, (unsigned)nn * 8u);
+      static_for<0, N1>([&](auto k) { ar[k.value] = bload_so(ract, base, N2 * 8 * k.value); });
+      prop(ar, false);
+      static_for<0, N1>([&](auto k) { x[k.value] = bload_so(rin, base, N2 * 8 * k.value); });
+      prop(x, true);
+      // conj(M_l) G_l and dphi_l += Im(conj(A_l) conj(M_l) G_l)
+      static_for<0, N1>([&](auto k) {
+        const float2 h = cmulc(x[k.value], bload_keep_so(rmod, base, N2 * 8 * k.value));
+        acc[k.value] += ar[k.value].x * h.y - ar[k.value].y * h.x;
+        x[k.value] = h;
+      });
+      prop(x, true);
+    } else {
+      static_for<0, N1>([&](auto k) { x[k.value] = bload_so(rin, base, N2 * 8 * k.value); });
+      prop(x, cj);
+      // U_l = M_l A_l
+      static_for<0, N1>([&](auto k) { x[k.value] = cmul(x[k.value], bload_keep_so(rmod, base, N2 * 8 * k.value)); });
+      prop(x, cj);
+    }
+    const Rsrc rout = make_rsrc(a.out + (size_t)b * nn, (unsigned)nn * 8u);
+    static_for<0, N1>([&](auto k) { bstore_so(rout, base, N2 * 8 * k.value, x[k.value]); });
+  }
+  if constexpr (ACC) {
+    // one partial per lane for the tile this wave kept
+    const int vec = (rank % a.ntiles) * R + r;
+    const bool vok = act && vec < a.nvec;
+    const unsigned base = vok ? (unsigned)(vec * N + j) * 4u : kOutOfRange;
+    const Rsrc dp = make_rsrc(a.dphi_part + (size_t)(rank / a.ntiles) * nn, (unsigned)nn * 4u);
+    static_for<0, N1>([&](auto k) { bstore_f_so(dp, base, N2 * 4 * k.value, acc[k.value]); });
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Whole-field forward for grids whose field fits in one CU's shared memory
 // (N <= 128: 132 KB at N = 128).  One workgroup per sample reads the
 // amplitude once, runs every hop and modulation of Eq. (forward_diff) and
@@ -2085,9 +2280,19 @@ constexpr bool wave_tile_kind() {
          (KIND == kFwdMid || KIND == kBwdMid || KIND == kBwdLast);
 }
 
+// Row layer kinds at 500 points run on the wide row tiles (wide_row_pass).
+template <int N, int KIND, int AXIS>
+constexpr bool wide_row_kind() {
+  return N == 500 && AXIS == kRow && (KIND == kFwdMid || KIND == kBwdMid);
+}
+
 template <int N, int KIND, int AXIS, bool FULL>
 hipError_t launch_fr(const PassArgs& a, hipStream_t st) {
-  if constexpr (FULL && wave_tile_kind<N, KIND, AXIS>()) {
+  if constexpr (FULL && wide_row_kind<N, KIND, AXIS>()) {
+    if (a.workers < 1) return hipErrorInvalidValue;
+    const dim3 grid(8 * ((a.workers + 7) / 8));
+    hipLaunchKernelGGL((wide_row_pass<typename PlanFor<N>::type, KIND>), grid, dim3(64), 0, st, a);
+  } else if constexpr (FULL && wave_tile_kind<N, KIND, AXIS>()) {
     if (a.workers < 1) return hipErrorInvalidValue;
     const dim3 grid(8 * ((a.workers + 7) / 8));
     hipLaunchKernelGGL((wave_pass<typename PlanFor<N>::type, KIND, AXIS>), grid, dim3(64), 0, st, a);
@@ -2140,7 +2345,9 @@ template <int N, int KIND, int AXIS, bool FULL>
 int slots_fr() {
   static int per_cu = 0;
   if (per_cu == 0) {
-    if constexpr (FULL && wave_tile_kind<N, KIND, AXIS>()) {
+    if constexpr (FULL && wide_row_kind<N, KIND, AXIS>()) {
+      per_cu = resident_per_cu(reinterpret_cast<const void*>(&wide_row_pass<typename PlanFor<N>::type, KIND>), 64);
+    } else if constexpr (FULL && wave_tile_kind<N, KIND, AXIS>()) {
       per_cu = resident_per_cu(reinterpret_cast<const void*>(&wave_pass<typename PlanFor<N>::type, KIND, AXIS>), 64);
     } else {
       using C = LayerCfg<N, KIND, AXIS>;
@@ -2158,6 +2365,9 @@ int slots_fr_axis(Axis axis, bool full) {
 
 template <int N, int KIND>
 int tile_fr_axis(Axis axis, bool full) {
+  if constexpr (wide_row_kind<N, KIND, kRow>()) {
+    if (axis == kRow && full) return WideRows<typename PlanFor<N>::type>::R;
+  }
   if (axis == kRow) return full && wave_tile_kind<N, KIND, kRow>() ? 8 : LayerTile<N, KIND, kRow>::T;
   return full && wave_tile_kind<N, KIND, kCol>() ? 8 : LayerTile<N, KIND, kCol>::T;
 }
