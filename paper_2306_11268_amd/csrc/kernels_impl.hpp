@@ -1534,8 +1534,9 @@ __global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 
 // (k1 = 20..24) one per lane quad, split by Good-Thomas 4 x 5 as in
 // b_spectral_quad.  Fields, this layer's modulation table and the dphi
 // partials are [vec][q] (rows, slot order): consecutive lanes read
-// consecutive slots of a row.  Forward (kFwdMid): one item per workgroup;
-// adjoint (kBwdMid): persistent, as fresnel_pass.
+// consecutive slots of a row.  First pass (kPropOnce, real amplitudes in)
+// and forward (kFwdMid): one item per workgroup; adjoint (kBwdMid):
+// persistent, as fresnel_pass.
 // ---------------------------------------------------------------------------
 template <class PL>
 struct WideRows {
@@ -1563,7 +1564,7 @@ __global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(Pas
   constexpr int PR = W::PR;
   constexpr int Q = W::Q;
   constexpr bool ACC = KIND == kBwdMid;
-  static_assert(KIND == kFwdMid || KIND == kBwdMid, "wide row tiles run the middle layer kinds");
+  static_assert(KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid, "wide row tiles run the layer kinds");
   __shared__ float2 tab[PR];       // chirp: B-item k1, frequency k2 at P1 * k1 + k2
   __shared__ float2 xch[R * PR];   // R rows
 
@@ -1696,6 +1697,14 @@ __global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(Pas
         x[k.value] = h;
       });
       prop(x, true);
+    } else if constexpr (KIND == kPropOnce) {
+      // real amplitudes in; along a row slot order is natural order (Cooley-Tukey plan)
+      const Rsrc ramp = make_rsrc(static_cast<const float*>(a.in) + (size_t)b * nn, (unsigned)nn * 4u);
+      const unsigned base4 = vok ? (unsigned)(vec * N + j) * 4u : kOutOfRange;
+      static_for<0, N1>([&](auto k) {
+        x[k.value] = c2(__builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ramp, (int)base4, N2 * 4 * k.value, 2)), 0.f);
+      });
+      prop(x, cj);
     } else {
       static_for<0, N1>([&](auto k) { x[k.value] = bload_so(rin, base, N2 * 8 * k.value); });
       prop(x, cj);
@@ -2283,7 +2292,7 @@ constexpr bool wave_tile_kind() {
 // Row layer kinds at 500 points run on the wide row tiles (wide_row_pass).
 template <int N, int KIND, int AXIS>
 constexpr bool wide_row_kind() {
-  return N == 500 && AXIS == kRow && (KIND == kFwdMid || KIND == kBwdMid);
+  return N == 500 && AXIS == kRow && (KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid);
 }
 
 template <int N, int KIND, int AXIS, bool FULL>
