@@ -1565,8 +1565,13 @@ __global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(Pas
   constexpr int Q = W::Q;
   constexpr bool ACC = KIND == kBwdMid;
   static_assert(KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid, "wide row tiles run the layer kinds");
-  __shared__ float2 tab[PR];       // chirp: B-item k1, frequency k2 at P1 * k1 + k2
-  __shared__ float2 xch[R * PR];   // R rows
+  // The adjoint stages the chirp in shared memory (B-item k1, frequency k2
+  // at P1 * k1 + k2; its registers allow 8 waves per CU either way); the
+  // forward kinds read it from the (cached) table in global memory, which
+  // leaves 12.6 KB of shared memory per wave: 12 waves per CU.
+  constexpr bool TAB_LDS = ACC;
+  __shared__ float2 tab[TAB_LDS ? PR : 1];
+  __shared__ float2 xch[R * PR];  // R rows
 
   const int rank = (int)blockIdx.x;
   if (rank >= a.workers) return;
@@ -1578,7 +1583,18 @@ __global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(Pas
   const size_t nn = (size_t)N * N;
   const bool cj = a.conj_tab != 0;
 
-  for (int i = lane; i < N; i += 64) tab[P1 * (i / N2) + i % N2] = a.tab[PL::freq(i / N2, i % N2)];
+  if constexpr (TAB_LDS) {
+    for (int i = lane; i < N; i += 64) tab[P1 * (i / N2) + i % N2] = a.tab[PL::freq(i / N2, i % N2)];
+  }
+  // chirp entry of B-item k1, element k2 (frequency k1 + N1 * k2)
+  const float2* __restrict__ gtab = a.tab;
+  auto chirp = [&](int k1, int k2) -> float2 {
+    if constexpr (TAB_LDS) {
+      return tab[P1 * k1 + k2];
+    } else {
+      return gtab[k1 + N1 * k2];
+    }
+  };
   float acc[ACC ? N1 : 1];
   if constexpr (ACC) {
     static_for<0, N1>([&](auto k) { acc[k.value] = 0.f; });
@@ -1602,16 +1618,15 @@ __global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(Pas
     if (act) {
       // B-item k1 = j of row r
       float2* const yb = xr + P1 * jo;
-      const float2* const tk = tab + P1 * jo;
       float2 y[N2];
       static_for<0, N2>([&](auto q) { y[q.value] = yb[q.value]; });
       static_for<1, N2>([&](auto q) { y[q.value] = cmul(y[q.value], root_at<N>((unsigned)(jo * q.value))); });
       Dft<N2, -1>::run(y);
       __builtin_amdgcn_sched_barrier(0);
       if (conj_t) {
-        static_for<0, N2>([&](auto q) { y[q.value] = cmulc(y[q.value], tk[q.value]); });
+        static_for<0, N2>([&](auto q) { y[q.value] = cmulc(y[q.value], chirp(jo, q.value)); });
       } else {
-        static_for<0, N2>([&](auto q) { y[q.value] = cmul(y[q.value], tk[q.value]); });
+        static_for<0, N2>([&](auto q) { y[q.value] = cmul(y[q.value], chirp(jo, q.value)); });
       }
       __builtin_amdgcn_sched_barrier(0);
       Dft<N2, 1>::run(y);
@@ -1630,7 +1645,6 @@ __global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(Pas
       const int qrow = qi / Q;
       const int k1 = N2 + qi - qrow * Q;
       float2* const base = xch + qrow * PR + P1 * k1;
-      const float2* const tq = tab + P1 * k1;
       auto elem = [&](auto m) {
         const int e = Q * qq + 4 * decltype(m)::value;
         return e >= N2 ? e - N2 : e;
@@ -1653,7 +1667,8 @@ __global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(Pas
       const int k4 = ((qq & 1) << 1) | (qq >> 1);
       static_for<0, Q>([&](auto m) {
         const int f = (W::E1 * k4 + W::E2 * decltype(m)::value) % N2;
-        z[m.value] = conj_t ? cmulc(z[m.value], tq[f]) : cmul(z[m.value], tq[f]);
+        const float2 h = chirp(k1, f);
+        z[m.value] = conj_t ? cmulc(z[m.value], h) : cmul(z[m.value], h);
       });
       quad_butterfly<1, Q>(z, s1);
       static_for<0, Q>([&](auto m) {
