@@ -61,13 +61,23 @@ typedef int lr_v2i __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ Rsrc make_rsrc(const void* base, unsigned bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
-// Field loads carry the non-temporal hint (cache policy bit 1): every field
-// is read once per pass, and the hint keeps those lines from displacing the
-// field the previous pass just wrote, which the large last-level cache can
-// still hold when this pass reads it.  Tables shared by the batch load
-// without it (bload_keep).
+// Field loads carry the non-temporal hint (cache policy bit 1) by default:
+// every field is read once per pass, and the hint keeps those lines from
+// displacing the field the previous pass just wrote, which the large
+// last-level cache can still hold when this pass reads it.  Tables shared by
+// the batch load without it (bload_keep).  field_load_policy drops the hint
+// at 400-512 points, whose fields of a few hundred samples (0.6-1 GB) are
+// several times the 256 MB last-level cache: there the hinted row and column
+// passes measured slower (5-layer training step, batch 500: 400 points 5.20
+// against 4.90 ms, 500 points 11.61 against 11.43 ms), while at 200 points
+// (160 MB) and 1000 points (batch 16, 128 MB) the hint saves 2-3%.
+template <int N>
+constexpr int field_load_policy() {
+  return (N >= 400 && N <= 512) ? 0 : 2;
+}
+template <int POL = 2>
 __device__ __forceinline__ float2 bload(Rsrc r, unsigned off) {
-  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 2));
+  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, POL));
 }
 __device__ __forceinline__ float2 bload_keep(Rsrc r, unsigned off) {
   return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0));
@@ -82,8 +92,9 @@ __device__ __forceinline__ void bstore_f(Rsrc r, unsigned off, float v) {
 // per-lane offset at or past kOutOfRange stays out of range with any scalar
 // offset used here (at most a few MB), whether or not the hardware's range
 // check includes the scalar part.
+template <int POL = 2>
 __device__ __forceinline__ float2 bload_so(Rsrc r, unsigned off, int soff) {
-  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, soff, 2));
+  return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, soff, POL));
 }
 __device__ __forceinline__ float2 bload_keep_so(Rsrc r, unsigned off, int soff) {
   return __builtin_bit_cast(float2, __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, soff, 0));
@@ -291,7 +302,7 @@ __device__ __forceinline__ void load_tile(float2* lds, const void* src, bool rea
     const Rsrc r = make_rsrc(src, (unsigned)(n * n) * 8u);
     float2 buf[BUF];
     tile_walk2<C, AXIS, kAll, ST>(n, off, nvalid,
-        [&](auto i, int v, int q, int, bool ok) { buf[i.value] = bload(r, elem_off<AXIS, 8>(ok, n, vf(v), q)); },
+        [&](auto i, int v, int q, int, bool ok) { buf[i.value] = bload<field_load_policy<C::N>()>(r, elem_off<AXIS, 8>(ok, n, vf(v), q)); },
         [&](auto i, int, int, int li, bool) { lds[li] = buf[i.value]; });
   }
 }
@@ -312,7 +323,7 @@ __device__ __forceinline__ void tile_issue(TileBuf<C, AXIS>& buf, const void* sr
   } else {
     const Rsrc r = make_rsrc(src, (unsigned)(n * n) * 8u);
     tile_walk2<C, AXIS, kAll, false>(n, 0, nvalid,
-        [&](auto i, int v, int q, int, bool ok) { buf[i.value] = bload(r, elem_off<AXIS, 8>(ok, n, vf(v), q)); },
+        [&](auto i, int v, int q, int, bool ok) { buf[i.value] = bload<field_load_policy<C::N>()>(r, elem_off<AXIS, 8>(ok, n, vf(v), q)); },
         [](auto, int, int, int, bool) {});
   }
 }
@@ -521,10 +532,10 @@ __device__ __forceinline__ void load_a_direct(const float2* __restrict__ in, int
   const Rsrc r = make_rsrc(in, (unsigned)(n * pitch) * 8u);
   if constexpr (ST) {
     const unsigned base = a_base_st<C, 8>(vec, vok);
-    static_for<0, C::N1>([&](auto k) { x[k.value] = bload_so(r, base, a_soff_st<C, 8, k.value>()); });
+    static_for<0, C::N1>([&](auto k) { x[k.value] = bload_so<field_load_policy<C::N>()>(r, base, a_soff_st<C, 8, k.value>()); });
   } else {
     for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
-      x[k.value] = bload(r, valid ? (unsigned)idx * 8u : kOutOfRange);
+      x[k.value] = bload<field_load_policy<C::N>()>(r, valid ? (unsigned)idx * 8u : kOutOfRange);
     });
   }
 }
@@ -550,11 +561,12 @@ __device__ __forceinline__ void load_a_direct_masked(const float2* __restrict__ 
   if constexpr (ST) {
     const unsigned base = a_base_st<C, 8>(vec, vok);
     static_for<0, C::N1>([&](auto k) {
-      x[k.value] = bload_so(r, ((mask >> k.value) & 1u) ? base : kOutOfRange, a_soff_st<C, 8, k.value>());
+      x[k.value] = bload_so<field_load_policy<C::N>()>(r, ((mask >> k.value) & 1u) ? base : kOutOfRange,
+                                                      a_soff_st<C, 8, k.value>());
     });
   } else {
     for_a_elems<C>(off, n, pitch, vec, vok, [&](auto k, int idx, bool valid) {
-      x[k.value] = bload(r, valid && ((mask >> k.value) & 1u) ? (unsigned)idx * 8u : kOutOfRange);
+      x[k.value] = bload<field_load_policy<C::N>()>(r, valid && ((mask >> k.value) & 1u) ? (unsigned)idx * 8u : kOutOfRange);
     });
   }
 }
@@ -1467,7 +1479,8 @@ __global__ void __launch_bounds__(64, (KIND == kBwdMid || KIND == kBwdLast) ? 3 
     const Rsrc rmod = make_rsrc(a.mod, (unsigned)nn * 8u);
     auto load_field = [&](Rsrc r, unsigned mask, float2(&x)[N1]) {
       static_for<0, N1>([&](auto k) {
-        x[k.value] = bload_so(r, ((mask >> k.value) & 1u) ? fb : kOutOfRange, wt_soff<N, 8, FQ, k.value>());
+        x[k.value] = bload_so<field_load_policy<N>()>(r, ((mask >> k.value) & 1u) ? fb : kOutOfRange,
+                                                      wt_soff<N, 8, FQ, k.value>());
       });
     };
     auto load_mod = [&](float2(&m)[N1]) {
@@ -1565,6 +1578,7 @@ __global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(Pas
   constexpr int Q = W::Q;
   constexpr bool ACC = KIND == kBwdMid;
   static_assert(KIND == kPropOnce || KIND == kFwdMid || KIND == kBwdMid, "wide row tiles run the layer kinds");
+  constexpr int POL = field_load_policy<N>();
   // The adjoint stages the chirp in shared memory (B-item k1, frequency k2
   // at P1 * k1 + k2; its registers allow 8 waves per CU either way); the
   // forward kinds read it from the (cached) table in global memory, which
@@ -1701,9 +1715,9 @@ __global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(Pas
       // A_l from the saved input of the forward pass, then G's half hop
       float2 ar[N1];
       const Rsrc ract = make_rsrc(a.act_in + (size_t)b * nn, (unsigned)nn * 8u);
-      static_for<0, N1>([&](auto k) { ar[k.value] = bload_so(ract, base, N2 * 8 * k.value); });
+      static_for<0, N1>([&](auto k) { ar[k.value] = bload_so<POL>(ract, base, N2 * 8 * k.value); });
       prop(ar, false);
-      static_for<0, N1>([&](auto k) { x[k.value] = bload_so(rin, base, N2 * 8 * k.value); });
+      static_for<0, N1>([&](auto k) { x[k.value] = bload_so<POL>(rin, base, N2 * 8 * k.value); });
       prop(x, true);
       // conj(M_l) G_l and dphi_l += Im(conj(A_l) conj(M_l) G_l)
       static_for<0, N1>([&](auto k) {
@@ -1717,11 +1731,11 @@ __global__ void __launch_bounds__(64, KIND == kBwdMid ? 2 : 3) wide_row_pass(Pas
       const Rsrc ramp = make_rsrc(static_cast<const float*>(a.in) + (size_t)b * nn, (unsigned)nn * 4u);
       const unsigned base4 = vok ? (unsigned)(vec * N + j) * 4u : kOutOfRange;
       static_for<0, N1>([&](auto k) {
-        x[k.value] = c2(__builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ramp, (int)base4, N2 * 4 * k.value, 2)), 0.f);
+        x[k.value] = c2(__builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(ramp, (int)base4, N2 * 4 * k.value, POL)), 0.f);
       });
       prop(x, cj);
     } else {
-      static_for<0, N1>([&](auto k) { x[k.value] = bload_so(rin, base, N2 * 8 * k.value); });
+      static_for<0, N1>([&](auto k) { x[k.value] = bload_so<POL>(rin, base, N2 * 8 * k.value); });
       prop(x, cj);
       // U_l = M_l A_l
       static_for<0, N1>([&](auto k) { x[k.value] = cmul(x[k.value], bload_keep_so(rmod, base, N2 * 8 * k.value)); });
