@@ -2287,6 +2287,15 @@ template <> struct LayerTile<200, kPropOnce, kRow> { static constexpr int T = 16
 template <> struct LayerTile<200, kFwdMid, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kBwdMid, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kBwdLast, kCol> { static constexpr int T = 32; };
+// 400: the column layer passes at 16 vectors (pitch 17: the A-item and
+// B-item reads of a 16-lane group fall in distinct bank pairs; at 8 vectors
+// two B-items share each group's pairs), four-wave workgroups of 55 KB, 8
+// waves per CU against 10; the row passes keep 8 (5-layer training step,
+// batch 500: adjoint column passes 576 -> 485 us and 391 -> 337 us; rows at 16
+// measured slower, 360 -> 380 us forward, and so did every pass at 512)
+template <> struct LayerTile<400, kFwdMid, kCol> { static constexpr int T = 16; };
+template <> struct LayerTile<400, kBwdMid, kCol> { static constexpr int T = 16; };
+template <> struct LayerTile<400, kBwdLast, kCol> { static constexpr int T = 16; };
 // 500: the forward passes in one ten-wave workgroup of 32 vectors per CU
 // instead of one five-wave workgroup of 16 (a 68 KB five-wave workgroup
 // leaves no room for a second one on a CU)
