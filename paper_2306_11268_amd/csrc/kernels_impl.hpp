@@ -2261,7 +2261,7 @@ template <int N> struct TileT;
 template <> struct TileT<64>   { static constexpr int T = 16; };
 template <> struct TileT<100>  { static constexpr int T = 16; };
 template <> struct TileT<128>  { static constexpr int T = 16; };
-template <> struct TileT<200>  { static constexpr int T = 16; };
+template <> struct TileT<200>  { static constexpr int T = 32; };  // detector-plane passes: 47.7 -> 45.7 and 30.6 -> 29.7 us against 16
 template <> struct TileT<256>  { static constexpr int T = 8; };
 template <> struct TileT<350>  { static constexpr int T = 32; };  // 14 slots: T * 14 threads must be whole waves
 template <> struct TileT<400>  { static constexpr int T = 8; };
@@ -2283,7 +2283,8 @@ struct LayerTile {
   static constexpr int T = TileT<N>::T;
 };
 template <> struct LayerTile<200, kFwdMid, kCol> { static constexpr int T = 32; };
-template <> struct LayerTile<200, kPropOnce, kRow> { static constexpr int T = 16; };
+template <> struct LayerTile<200, kPropOnce, kRow> { static constexpr int T = 32; };
+template <> struct LayerTile<200, kBwdMid, kCol> { static constexpr int T = 16; };
 template <> struct LayerTile<200, kFwdMid, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kBwdMid, kRow> { static constexpr int T = 8; };
 template <> struct LayerTile<200, kBwdLast, kCol> { static constexpr int T = 32; };
