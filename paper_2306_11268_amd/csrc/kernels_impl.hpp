@@ -134,6 +134,17 @@ __device__ __forceinline__ WorkItem work_item(int ntiles, int ngroups) {
 }
 inline int work_grid(int ntiles, int ngroups) { return 8 * ((ntiles * ngroups + 7) / 8); }
 
+// Persistent passes (workers = lanes * ntiles; rank r keeps tile r % ntiles
+// and lane r / ntiles) with the XCD-contiguous index rx of the workgroup taken
+// tile-major (tile rx / lanes, lane rx % lanes): the workgroups of one XCD
+// hold every lane of a contiguous range of tiles.  An index past the workers
+// is returned unchanged.
+__device__ __forceinline__ int persistent_rank(int l, int G, int ntiles, int lanes) {
+  const int rx = (l & 7) * (G >> 3) + (l >> 3);
+  if (lanes < 1 || rx >= ntiles * lanes) return rx;
+  return (rx % lanes) * ntiles + rx / lanes;
+}
+
 // Offsets inside one sample fit in 32 bits (n <= 1024).
 template <int AXIS>
 __device__ __forceinline__ int nat_index(int n, int vec, int q) {
@@ -629,7 +640,13 @@ __global__ void __launch_bounds__(C::P, C::WAVES_ACC)
   // XCD-contiguous ranks let neighbouring column tiles share cache lines in
   // one XCD's L2; row tiles read whole rows and stream faster in dispatch
   // order (a memory-only probe of the row pattern: 6.4 against 5.8 TB/s)
-  const int rank = AXIS == kCol ? (l & 7) * (G >> 3) + (l >> 3) : l;
+  // The 1000-point adjoint row passes take the tile-major persistent order
+  // (one XCD keeps whole tiles: 245 -> 231 us, workload 5 1.505 -> 1.493 ms;
+  // at 200-500 points it measured neutral or slower)
+  constexpr bool TILE_MAJOR = ACC && AXIS == kRow && C::N == 1000;
+  const int rank = TILE_MAJOR       ? persistent_rank(l, G, a.ntiles, a.lanes)
+                   : AXIS == kCol ? (l & 7) * (G >> 3) + (l >> 3)
+                                  : l;
   if (rank >= a.workers) return;
   const int n = a.n;
   const int off = a.off;
@@ -2303,6 +2320,10 @@ template <> struct LayerTile<400, kBwdLast, kCol> { static constexpr int T = 16;
 template <> struct LayerTile<500, kPropOnce, kRow> { static constexpr int T = 32; };
 template <> struct LayerTile<500, kFwdMid, kRow> { static constexpr int T = 32; };
 template <> struct LayerTile<500, kFwdMid, kCol> { static constexpr int T = 32; };
+// 512: the first and the adjoint row passes at 16 vectors (5-layer training
+// step, batch 500: 446 -> 429 and 1113 -> 1077 us, step 11.22 -> 11.11 ms)
+template <> struct LayerTile<512, kPropOnce, kRow> { static constexpr int T = 16; };
+template <> struct LayerTile<512, kBwdMid, kRow> { static constexpr int T = 16; };
 template <> struct LayerTile<1000, kPropOnce, kRow> { static constexpr int T = 16; };
 template <> struct LayerTile<1000, kFwdMid, kRow> { static constexpr int T = 16; };
 template <> struct LayerTile<1000, kFwdMid, kCol> { static constexpr int T = 16; };
